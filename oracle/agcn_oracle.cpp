@@ -1,0 +1,301 @@
+// CPU oracle for the Accel-GCN aggregation path (arXiv 2308.11825).
+//
+// TEST INFRASTRUCTURE ONLY: the plain statement of what the device path must
+// compute, used by the tests, the smoke check and the CPU-baseline timing.
+// Nothing here is shared with the device library. The readings R1-R9 of the
+// paper that this file follows are listed in agcn_oracle.h.
+//
+// Style: single-threaded, straight loops in the paper's order, float64
+// accumulation. Built with -O2 -ffp-contract=off.
+#include "agcn_oracle.h"
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+namespace {
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool rowptr_ok(int32_t n_rows, const int32_t* rowptr) {
+  if (n_rows < 0 || rowptr == nullptr) return false;
+  if (rowptr[0] != 0) return false;
+  for (int32_t i = 0; i < n_rows; ++i)
+    if (rowptr[i + 1] < rowptr[i]) return false;
+  return true;
+}
+
+// Alg. 1 written out: walk the factors of max_block_warps in ascending order;
+// a degree takes the first factor whose warps (each holding max_warp_nzs
+// nnz) can cover it. Degrees run 1..deg_bound inclusive (R4).
+void patterns(int32_t W, int32_t Z, std::vector<int32_t>& block_rows,
+              std::vector<int32_t>& warp_nzs) {
+  const int32_t deg_bound = W * Z;
+  std::vector<int32_t> factors;
+  for (int32_t f = 1; f <= W; ++f)
+    if (W % f == 0) factors.push_back(f);
+  block_rows.assign(deg_bound + 1, 0);
+  warp_nzs.assign(deg_bound + 1, 0);
+  size_t i = 0;
+  int32_t deg = 1;
+  while (deg <= deg_bound) {
+    if ((int64_t)factors[i] * Z >= deg) {
+      block_rows[deg] = W / factors[i];
+      warp_nzs[deg] = (int32_t)ceil_div(deg, factors[i]);
+      ++deg;
+    } else {
+      ++i;  // the last factor is W itself and W * Z = deg_bound, so i stays in range
+    }
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+// Sec. III-C, degree sorting: (1) degrees from the row pointer, (2) a stable
+// counting sort by degree, ascending (R1).
+int oracle_degree_sort(int32_t n_rows, const int32_t* rowptr, int32_t* perm) {
+  if (!rowptr_ok(n_rows, rowptr) || (n_rows > 0 && perm == nullptr)) return -1;
+  int32_t max_deg = 0;
+  for (int32_t i = 0; i < n_rows; ++i) {
+    int32_t d = rowptr[i + 1] - rowptr[i];
+    if (d > max_deg) max_deg = d;
+  }
+  // count[d] = number of rows of degree d; start[d] = exclusive prefix sum.
+  std::vector<int64_t> start((size_t)max_deg + 2, 0);
+  for (int32_t i = 0; i < n_rows; ++i) start[rowptr[i + 1] - rowptr[i] + 1] += 1;
+  for (size_t d = 1; d < start.size(); ++d) start[d] += start[d - 1];
+  // Visiting rows in original order keeps ties in original order.
+  for (int32_t i = 0; i < n_rows; ++i) {
+    int32_t d = rowptr[i + 1] - rowptr[i];
+    perm[start[d]++] = i;
+  }
+  return 0;
+}
+
+// Sec. III-C, degree sorting step (3) with R2: rows copied in sorted order.
+int oracle_relayout(int32_t n_rows, const int32_t* rowptr, const int32_t* colidx,
+                    const float* vals, const int32_t* perm, int32_t* rowptr_s,
+                    int32_t* colidx_s, float* vals_s) {
+  if (!rowptr_ok(n_rows, rowptr) || rowptr_s == nullptr) return -1;
+  rowptr_s[0] = 0;
+  for (int32_t r = 0; r < n_rows; ++r) {
+    int32_t i = perm[r];
+    if (i < 0 || i >= n_rows) return -1;
+    int32_t d = rowptr[i + 1] - rowptr[i];
+    rowptr_s[r + 1] = rowptr_s[r] + d;
+    for (int32_t t = 0; t < d; ++t) {
+      colidx_s[rowptr_s[r] + t] = colidx[rowptr[i] + t];
+      vals_s[rowptr_s[r] + t] = vals[rowptr[i] + t];
+    }
+  }
+  return 0;
+}
+
+int oracle_patterns(int32_t max_block_warps, int32_t max_warp_nzs, int32_t* block_rows,
+                    int32_t* warp_nzs) {
+  if (max_block_warps < 1 || max_warp_nzs < 1 || block_rows == nullptr || warp_nzs == nullptr)
+    return -1;
+  if ((int64_t)max_block_warps * max_warp_nzs > (1 << 24)) return -1;
+  std::vector<int32_t> br, wn;
+  patterns(max_block_warps, max_warp_nzs, br, wn);
+  std::memcpy(block_rows, br.data(), br.size() * sizeof(int32_t));
+  std::memcpy(warp_nzs, wn.data(), wn.size() * sizeof(int32_t));
+  return 0;
+}
+
+// Alg. 2: one pass over the degree classes of the sorted rows, ascending.
+int64_t oracle_partition(int32_t n_rows, const int32_t* rowptr_s, int32_t max_block_warps,
+                         int32_t max_warp_nzs, int32_t hub_chunk_nnz, int32_t* meta,
+                         int64_t cap) {
+  if (!rowptr_ok(n_rows, rowptr_s) || max_block_warps < 1 || max_warp_nzs < 1) return -1;
+  const int64_t W = max_block_warps;
+  const int64_t deg_bound = W * max_warp_nzs;
+  if (deg_bound > (1 << 24) || max_block_warps > 0xFFFF || max_warp_nzs > 0xFFFF) return -1;
+  const int64_t H = hub_chunk_nnz > 0 ? hub_chunk_nnz : deg_bound;
+  std::vector<int32_t> block_rows, warp_nzs;
+  patterns(max_block_warps, max_warp_nzs, block_rows, warp_nzs);
+
+  int64_t count = 0;
+  auto emit = [&](int64_t deg, int64_t loc, int64_t row, int64_t info) {
+    if (meta != nullptr) {
+      if (count >= cap) return false;
+      meta[4 * count + 0] = (int32_t)deg;
+      meta[4 * count + 1] = (int32_t)loc;
+      meta[4 * count + 2] = (int32_t)row;
+      meta[4 * count + 3] = (int32_t)info;
+    }
+    ++count;
+    return true;
+  };
+
+  int64_t r = 0;  // cursor over sorted rows
+  while (r < n_rows) {
+    const int64_t deg = rowptr_s[r + 1] - rowptr_s[r];
+    int64_t rows_of_deg = 0;  // size of this degree class (sorted => contiguous)
+    while (r + rows_of_deg < n_rows &&
+           rowptr_s[r + rows_of_deg + 1] - rowptr_s[r + rows_of_deg] == deg)
+      ++rows_of_deg;
+    if (deg <= deg_bound) {
+      // Degree 0 (R7): rows of W, nothing to gather.
+      const int64_t br = deg == 0 ? W : block_rows[deg];
+      const int64_t wn = deg == 0 ? 0 : warp_nzs[deg];
+      int64_t rows_remaining = rows_of_deg;
+      while (rows_remaining >= br) {
+        if (!emit(deg, rowptr_s[r], r, (wn << 16) | br)) return -2;
+        r += br;
+        rows_remaining -= br;
+      }
+      if (rows_remaining > 0) {  // R6: no empty residual entry
+        if (!emit(deg, rowptr_s[r], r, (wn << 16) | rows_remaining)) return -2;
+        r += rows_remaining;
+      }
+    } else {
+      // R8: every row of this degree is cut into chunks of H nnz.
+      for (int64_t k = 0; k < rows_of_deg; ++k, ++r) {
+        int64_t loc = rowptr_s[r];
+        int64_t deg_remaining = deg;
+        while (deg_remaining >= H) {
+          if (!emit(deg, loc, r, H)) return -2;
+          loc += H;
+          deg_remaining -= H;
+        }
+        if (deg_remaining > 0) {
+          if (!emit(deg, loc, r, deg_remaining)) return -2;
+        }
+      }
+    }
+  }
+  return count;
+}
+
+// Sec. II-A/II-B: the aggregation A' Y by its definition.
+int oracle_spmm(int32_t n_rows, int32_t n_cols, int32_t F, const int32_t* rowptr,
+                const int32_t* colidx, const float* vals, const float* X, int64_t ldx,
+                float* Y, int64_t ldy, double* Yd, double* S) {
+  if (!rowptr_ok(n_rows, rowptr) || F < 0 || ldx < F || ldy < F) return -1;
+  std::vector<double> acc((size_t)F), mag((size_t)F);
+  for (int32_t i = 0; i < n_rows; ++i) {
+    std::fill(acc.begin(), acc.end(), 0.0);
+    std::fill(mag.begin(), mag.end(), 0.0);
+    for (int32_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+      const int32_t j = colidx[e];
+      if (j < 0 || j >= n_cols) return -1;
+      const double a = (double)vals[e];
+      const float* xr = X + (int64_t)j * ldx;
+      for (int32_t k = 0; k < F; ++k) {
+        const double p = a * (double)xr[k];
+        acc[k] += p;
+        mag[k] += p < 0 ? -p : p;
+      }
+    }
+    for (int32_t k = 0; k < F; ++k) {
+      Y[(int64_t)i * ldy + k] = (float)acc[k];
+      if (Yd) Yd[(int64_t)i * F + k] = acc[k];
+      if (S) S[(int64_t)i * F + k] = mag[k];
+    }
+  }
+  return 0;
+}
+
+int oracle_spmm_rows(int32_t n_rows, int32_t n_cols, int32_t F, const int32_t* rowptr,
+                     const int32_t* colidx, const float* vals, const float* X, int64_t ldx,
+                     const int32_t* rows, int32_t m, float* Y, double* S) {
+  if (n_rows < 0 || rowptr == nullptr || F < 0 || ldx < F || m < 0) return -1;
+  std::vector<double> acc((size_t)F), mag((size_t)F);
+  for (int32_t q = 0; q < m; ++q) {
+    const int32_t i = rows[q];
+    if (i < 0 || i >= n_rows || rowptr[i + 1] < rowptr[i]) return -1;
+    std::fill(acc.begin(), acc.end(), 0.0);
+    std::fill(mag.begin(), mag.end(), 0.0);
+    for (int32_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+      const int32_t j = colidx[e];
+      if (j < 0 || j >= n_cols) return -1;
+      const double a = (double)vals[e];
+      const float* xr = X + (int64_t)j * ldx;
+      for (int32_t k = 0; k < F; ++k) {
+        const double p = a * (double)xr[k];
+        acc[k] += p;
+        mag[k] += p < 0 ? -p : p;
+      }
+    }
+    for (int32_t k = 0; k < F; ++k) {
+      Y[(int64_t)q * F + k] = (float)acc[k];
+      if (S) S[(int64_t)q * F + k] = mag[k];
+    }
+  }
+  return 0;
+}
+
+// Sec. III-C, last paragraph: a warp's workload follows from its block's entry.
+int oracle_replay_meta(int32_t n_rows, int32_t n_cols, int32_t F, const int32_t* rowptr_s,
+                       const int32_t* colidx_s, const float* vals_s, const int32_t* perm,
+                       const int32_t* meta, int64_t n_entries, int32_t max_block_warps,
+                       int32_t max_warp_nzs, const float* X, int64_t ldx, float* Y,
+                       int32_t* cover, int32_t* row_hits, int32_t* hub_chunks) {
+  if (!rowptr_ok(n_rows, rowptr_s) || max_block_warps < 1 || max_warp_nzs < 1 || F < 0)
+    return -1;
+  const int64_t W = max_block_warps;
+  const int64_t deg_bound = W * max_warp_nzs;
+  const int64_t nnz = rowptr_s[n_rows];
+  std::vector<double> acc((size_t)n_rows * (size_t)F, 0.0);
+  std::memset(cover, 0, (size_t)nnz * sizeof(int32_t));
+  std::memset(row_hits, 0, (size_t)n_rows * sizeof(int32_t));
+  std::memset(hub_chunks, 0, (size_t)n_rows * sizeof(int32_t));
+
+  auto visit = [&](int64_t r, int64_t begin, int64_t len) {
+    if (r < 0 || r >= n_rows || begin < rowptr_s[r] || begin + len > rowptr_s[r + 1]) return false;
+    double* a = acc.data() + (size_t)r * F;
+    for (int64_t e = begin; e < begin + len; ++e) {
+      cover[e] += 1;
+      const int32_t j = colidx_s[e];
+      if (j < 0 || j >= n_cols) return false;
+      const float* xr = X + (int64_t)j * ldx;
+      for (int32_t k = 0; k < F; ++k) a[k] += (double)vals_s[e] * (double)xr[k];
+    }
+    return true;
+  };
+
+  for (int64_t b = 0; b < n_entries; ++b) {
+    const int64_t deg = meta[4 * b + 0], loc = meta[4 * b + 1];
+    const int64_t row = meta[4 * b + 2], info = (uint32_t)meta[4 * b + 3];
+    if (deg < 0) return -1;
+    if (deg <= deg_bound) {
+      const int64_t wn = info >> 16, rows = info & 0xFFFF;
+      if (row < 0 || row + rows > n_rows) return -1;
+      if (deg == 0) {
+        for (int64_t k = 0; k < rows; ++k) row_hits[row + k] += 1;
+        continue;
+      }
+      if (wn <= 0) return -1;
+      const int64_t wpr = ceil_div(deg, wn);  // warps per row
+      for (int64_t v = 0; v < rows * wpr; ++v) {
+        const int64_t rl = v / wpr, part = v % wpr;
+        const int64_t begin = loc + rl * deg + part * wn;
+        const int64_t len = std::min<int64_t>(wn, deg - part * wn);
+        if (part == 0) row_hits[row + rl] += 1;
+        if (!visit(row + rl, begin, len)) return -1;
+      }
+    } else {
+      if (row < 0 || row >= n_rows) return -1;
+      hub_chunks[row] += 1;
+      const int64_t s = ceil_div(info, W);
+      for (int64_t v = 0; v < W; ++v) {
+        const int64_t begin = loc + v * s;
+        const int64_t end = std::min<int64_t>(loc + (v + 1) * s, loc + info);
+        if (end > begin && !visit(row, begin, end - begin)) return -1;
+      }
+    }
+  }
+  for (int32_t r = 0; r < n_rows; ++r) {
+    const int32_t i = perm[r];
+    if (i < 0 || i >= n_rows) return -1;
+    for (int32_t k = 0; k < F; ++k)
+      Y[(int64_t)i * F + k] = (float)acc[(size_t)r * F + k];
+  }
+  return 0;
+}
+
+}  // extern "C"

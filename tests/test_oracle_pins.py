@@ -1,0 +1,391 @@
+"""Pins for the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: the paper's
+worked example, Alg. 1's hand-derived table, library routines (numpy stable
+argsort, scipy CSR row indexing and products, dense matmul), closed forms
+(identity, all-ones features), invariances (row permutation, linearity) and
+the coverage invariants of the block-level partition.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+
+import graphgen
+import oracle
+
+
+def _golden(name):
+    from conftest import GOLDEN
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _csr_from_rowptr(rowptr, seed=0, n_cols=None):
+    rowptr = np.asarray(rowptr, dtype=np.int32)
+    nnz = int(rowptr[-1])
+    rng = np.random.default_rng(seed)
+    n = rowptr.size - 1
+    n_cols = n if n_cols is None else n_cols
+    colidx = rng.integers(0, n_cols, nnz).astype(np.int32)
+    vals = rng.standard_normal(nnz).astype(np.float32)
+    return rowptr, colidx, vals
+
+
+def _scipy(g):
+    return sp.csr_matrix((g.vals.astype(np.float64), g.colidx, g.rowptr), shape=(g.n_rows, g.n_cols))
+
+
+def _mixed_graph(seed, n=300, n_cols=None, max_deg=900, dupes=False):
+    """Degrees from several regimes: empty rows, small, mid, and hub rows."""
+    rng = np.random.default_rng(seed)
+    n_cols = n if n_cols is None else n_cols
+    deg = rng.choice([0, 1, 2, 3, 5, 8, 17, 31, 32, 33, 64, 100, 383, 384, 385], size=n)
+    hubs = rng.choice(n, size=max(1, n // 50), replace=False)
+    deg[hubs] = rng.integers(385, max_deg + 1, size=hubs.size)
+    if not dupes:
+        deg = np.minimum(deg, n_cols)
+    return graphgen.random_csr(n, n_cols, deg, seed=seed + 1, dupes=dupes)
+
+
+# --------------------------------------------------------------------------
+# Worked example of Sec. III-C (golden)
+# --------------------------------------------------------------------------
+
+def test_worked_example_sort_relayout_partition():
+    g = _golden("worked_example_w2_z2.json")
+    W, Z = g["max_block_warps"], g["max_warp_nzs"]
+    rowptr, colidx, vals = _csr_from_rowptr(g["rowptr"], seed=3)
+    perm = oracle.degree_sort(rowptr)
+    assert perm.tolist() == g["expected_perm"]
+    rowptr_s, colidx_s, vals_s = oracle.relayout(rowptr, colidx, vals, perm)
+    assert rowptr_s.tolist() == g["expected_rowptr_s"]
+    # Sorted row 2 is original row 1: its nnz moved to positions 4..7.
+    assert colidx_s[4:8].tolist() == colidx[2:6].tolist()
+    br, wn = oracle.patterns(W, Z)
+    for d, (b, w) in g["expected_patterns"].items():
+        assert (br[int(d)], wn[int(d)]) == (b, w), d
+    meta = oracle.partition(rowptr_s, W, Z)
+    assert meta.tolist() == g["expected_meta"]
+
+
+def test_worked_example_warp_workloads_and_storage_ratio():
+    g = _golden("worked_example_w2_z2.json")
+    W, Z = g["max_block_warps"], g["max_warp_nzs"]
+    rowptr, colidx, vals = _csr_from_rowptr(g["rowptr"], seed=4)
+    p = oracle.plan(rowptr, colidx, vals, W, Z)
+    # Replay the metadata with one-hot features so each warp's slice is visible.
+    X = np.eye(3, dtype=np.float32)
+    Y, cover, row_hits, hub_chunks = oracle.replay_meta(
+        p["rowptr_s"], p["colidx_s"], p["vals_s"], p["perm"], p["meta"], W, Z, X)
+    assert cover.tolist() == [1] * 8
+    assert row_hits.tolist() == [1, 1, 1] and hub_chunks.tolist() == [0, 0, 0]
+    # Slices the decode rule assigns, from the entries themselves.
+    slices = []
+    for deg, loc, row, info in p["meta"].tolist():
+        w, rows = info >> 16, info & 0xFFFF
+        wpr = -(-deg // w)
+        for v in range(rows * wpr):
+            rl, part = divmod(v, wpr)
+            b = loc + rl * deg + part * w
+            slices.append([row + rl, b, b + min(w, deg - part * w)])
+    assert slices == g["expected_warp_slices"]
+    # Eq. 1: block-level metadata / warp-level metadata = blocks / warps.
+    assert len(p["meta"]) / g["warp_level_warps"] == pytest.approx(0.5)
+
+
+# --------------------------------------------------------------------------
+# Alg. 1
+# --------------------------------------------------------------------------
+
+def test_patterns_w12_z32_table():
+    g = _golden("patterns_w12_z32.json")
+    br, wn = oracle.patterns(g["max_block_warps"], g["max_warp_nzs"])
+    assert br.size == g["deg_bound"] + 1
+    for r in g["ranges"]:
+        ds = np.arange(r["deg_lo"], r["deg_hi"] + 1)
+        assert np.all(br[ds] == r["block_rows"])
+        assert wn[ds].min() == r["warp_nzs_lo"] and wn[ds].max() == r["warp_nzs_hi"]
+        # warp_nzs = ceil(deg / factor) across the whole range
+        assert np.all(wn[ds] * r["factor"] >= ds) and np.all((wn[ds] - 1) * r["factor"] < ds)
+    for d, (b, w) in g["spot_values"].items():
+        assert (br[int(d)], wn[int(d)]) == (b, w)
+
+
+@pytest.mark.parametrize("W,Z", [(1, 1), (2, 2), (12, 32), (16, 32), (8, 64), (12, 2), (6, 3),
+                                 (7, 5), (16, 64), (30, 4)])
+def test_patterns_cover_properties(W, Z):
+    br, wn = oracle.patterns(W, Z)
+    factors = [f for f in range(1, W + 1) if W % f == 0]
+    for d in range(1, W * Z + 1):
+        f = W // br[d]
+        assert f * br[d] == W and f in factors
+        assert f * Z >= d                      # f warps of Z nnz hold the row
+        assert all(g * Z < d for g in factors if g < f)   # no smaller factor would
+        assert wn[d] <= Z and f * wn[d] >= d and f * (wn[d] - 1) < d
+        assert br[d] * d <= W * Z              # a block holds at most deg_bound nnz
+
+
+def test_patterns_reject_bad_params():
+    with pytest.raises(oracle.OracleError):
+        oracle.patterns(0, 4)
+    with pytest.raises(oracle.OracleError):
+        oracle.patterns(4, 0)
+
+
+# --------------------------------------------------------------------------
+# Degree sort and relayout
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(6))
+def test_degree_sort_is_stable_ascending(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 3000))
+    deg = rng.choice([0, 1, 1, 2, 3, 3, 3, 7, 50, 1000], size=n)
+    rowptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int32)
+    perm = oracle.degree_sort(rowptr)
+    assert perm.tolist() == np.argsort(deg, kind="stable").tolist()
+
+
+def test_degree_sort_edge_cases():
+    assert oracle.degree_sort(np.array([0], np.int32)).size == 0
+    assert oracle.degree_sort(np.array([0, 0, 0, 0], np.int32)).tolist() == [0, 1, 2]
+    assert oracle.degree_sort(np.array([0, 3, 3, 4], np.int32)).tolist() == [1, 2, 0]
+    with pytest.raises(oracle.OracleError):
+        oracle.degree_sort(np.array([0, 3, 2], np.int32))
+    with pytest.raises(oracle.OracleError):
+        oracle.degree_sort(np.array([1, 3], np.int32))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_relayout_equals_scipy_row_permutation(seed):
+    g = _mixed_graph(seed, n=400, dupes=bool(seed % 2))
+    perm = oracle.degree_sort(g.rowptr)
+    rowptr_s, colidx_s, vals_s = oracle.relayout(g.rowptr, g.colidx, g.vals, perm)
+    A = sp.csr_matrix((g.vals, g.colidx, g.rowptr), shape=(g.n_rows, g.n_cols))
+    B = A[perm]       # scipy keeps each row's internal order
+    assert rowptr_s.tolist() == B.indptr.tolist()
+    assert colidx_s.tolist() == B.indices.tolist()
+    assert np.array_equal(vals_s.view(np.uint32), B.data.astype(np.float32).view(np.uint32))
+
+
+# --------------------------------------------------------------------------
+# SpMM by definition
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(8))
+def test_spmm_matches_dense_bruteforce(seed):
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(1, 65))
+    n_cols = int(rng.integers(1, 65))
+    deg = rng.integers(0, 12, size=n)
+    deg[rng.random(n) < 0.2] = 0                        # empty rows
+    g = graphgen.random_csr(n, n_cols, deg, seed=seed, dupes=True)   # repeated columns
+    F = int(rng.integers(1, 20))
+    X = rng.standard_normal((n_cols, F)).astype(np.float32)
+    Y, Yd, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, n_cols=n_cols, want_double=True,
+                           want_scale=True)
+    A = np.zeros((n, n_cols))
+    Aabs = np.zeros((n, n_cols))
+    for i in range(n):
+        for e in range(g.rowptr[i], g.rowptr[i + 1]):
+            A[i, g.colidx[e]] += float(g.vals[e])         # repeated entries add up
+            Aabs[i, g.colidx[e]] += abs(float(g.vals[e]))
+    ref = A @ X.astype(np.float64)
+    assert np.allclose(Yd, ref, rtol=0, atol=1e-12 * (1 + np.abs(ref).max()))
+    assert np.array_equal(Y, Yd.astype(np.float32))
+    assert np.allclose(S, Aabs @ np.abs(X.astype(np.float64)), rtol=1e-12, atol=1e-300)
+    assert np.all(S + 1e-300 >= np.abs(Yd))
+    assert np.all(Y[deg == 0] == 0)
+
+
+def test_spmm_matches_scipy_on_mixed_graph():
+    g = _mixed_graph(7, n=500)
+    rng = np.random.default_rng(8)
+    X = rng.standard_normal((g.n_cols, 33)).astype(np.float32)
+    Yd = oracle.spmm(g.rowptr, g.colidx, g.vals, X, want_double=True)[1]
+    ref = _scipy(g) @ X.astype(np.float64)
+    assert np.allclose(Yd, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_spmm_identity_is_exact():
+    n, F = 257, 19
+    g = graphgen.identity_csr(n)
+    X = np.random.default_rng(1).standard_normal((n, F)).astype(np.float32)
+    Y = oracle.spmm(g.rowptr, g.colidx, g.vals, X)
+    assert np.array_equal(Y.view(np.uint32), X.view(np.uint32))
+
+
+def test_spmm_all_ones_gives_row_sums():
+    g = graphgen.make("tiny_er")
+    X = np.ones((g.n_cols, 3), dtype=np.float32)
+    Yd = oracle.spmm(g.rowptr, g.colidx, g.vals, X, want_double=True)[1]
+    sums = np.add.reduceat(g.vals.astype(np.float64), g.rowptr[:-1]) if g.nnz else np.zeros(g.n_rows)
+    for k in range(3):
+        assert np.allclose(Yd[:, k], sums, rtol=1e-14, atol=0)
+    # symmetric normalisation: row sums are not all 1
+    assert np.abs(sums - 1).max() > 1e-3
+
+
+def test_spmm_row_permutation_equivariance_bit_exact():
+    g = _mixed_graph(11, n=300, dupes=True)
+    rng = np.random.default_rng(12)
+    X = rng.standard_normal((g.n_cols, 24)).astype(np.float32)
+    p = rng.permutation(g.n_rows)
+    Y = oracle.spmm(g.rowptr, g.colidx, g.vals, X)
+    gp = graphgen.permute_rows(g, p)
+    Yp = oracle.spmm(gp.rowptr, gp.colidx, gp.vals, X)
+    assert np.array_equal(Yp.view(np.uint32), Y[p].view(np.uint32))
+
+
+def test_spmm_linearity():
+    g = _mixed_graph(13, n=200)
+    rng = np.random.default_rng(14)
+    X1 = rng.standard_normal((g.n_cols, 8)).astype(np.float32)
+    X2 = rng.standard_normal((g.n_cols, 8)).astype(np.float32)
+    a, b = 0.75, -2.0          # exact in float32, so a X1 + b X2 rounds once
+    _, Y1, S1 = oracle.spmm(g.rowptr, g.colidx, g.vals, X1, want_double=True, want_scale=True)
+    _, Y2, S2 = oracle.spmm(g.rowptr, g.colidx, g.vals, X2, want_double=True, want_scale=True)
+    X3 = (a * X1.astype(np.float64) + b * X2.astype(np.float64)).astype(np.float32)
+    Y3 = oracle.spmm(g.rowptr, g.colidx, g.vals, X3, want_double=True)[1]
+    scale = abs(a) * S1 + abs(b) * S2
+    assert np.all(np.abs(Y3 - (a * Y1 + b * Y2)) <= 1e-6 * scale + 1e-12)
+
+
+def test_spmm_column_slice_and_spmv():
+    g = _mixed_graph(15, n=150)
+    X = np.random.default_rng(16).standard_normal((g.n_cols, 40)).astype(np.float32)
+    Y = oracle.spmm(g.rowptr, g.colidx, g.vals, X)
+    Y5 = oracle.spmm(g.rowptr, g.colidx, g.vals, np.ascontiguousarray(X[:, :5]))
+    assert np.array_equal(Y5, Y[:, :5])
+    y1 = oracle.spmm(g.rowptr, g.colidx, g.vals, np.ascontiguousarray(X[:, 7:8]))
+    ref = _scipy(g) @ X[:, 7].astype(np.float64)
+    assert np.allclose(y1[:, 0], ref, rtol=1e-6, atol=1e-6)
+
+
+def test_spmm_rows_matches_full():
+    g = _mixed_graph(17, n=220)
+    X = np.random.default_rng(18).standard_normal((g.n_cols, 12)).astype(np.float32)
+    Y, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, want_scale=True)
+    rows = np.array([0, 5, 219, 7, 7, 100], np.int32)
+    Yr, Sr = oracle.spmm_rows(g.rowptr, g.colidx, g.vals, X, rows)
+    assert np.array_equal(Yr, Y[rows]) and np.array_equal(Sr, S[rows])
+
+
+def test_spmm_rejects_out_of_range_column():
+    g = graphgen.random_csr(4, 4, [1, 1, 1, 1], seed=0)
+    g.colidx[2] = 4
+    with pytest.raises(oracle.OracleError):
+        oracle.spmm(g.rowptr, g.colidx, g.vals, np.zeros((4, 2), np.float32))
+
+
+# --------------------------------------------------------------------------
+# Block-level partition (Alg. 2) invariants
+# --------------------------------------------------------------------------
+
+PARAMS = [(12, 32, 0), (16, 32, 0), (8, 64, 0), (2, 2, 0), (12, 2, 0), (6, 3, 0), (16, 32, 100),
+          (4, 8, 7), (16, 64, 2048)]
+
+
+def _check_partition(rowptr_s, meta, W, Z, H):
+    deg_s = np.diff(rowptr_s.astype(np.int64))
+    n = deg_s.size
+    DB = W * Z
+    H = H if H > 0 else DB
+    br_tab, wn_tab = oracle.patterns(W, Z)
+    covered_rows = np.zeros(n, np.int64)
+    chunks = np.zeros(n, np.int64)
+    prev = None
+    for b, (deg, loc, row, info) in enumerate(meta.tolist()):
+        if deg <= DB:
+            wn, rows = (info >> 16) & 0xFFFF, info & 0xFFFF
+            assert rows >= 1                                              # I4
+            assert np.all(deg_s[row:row + rows] == deg)                   # I2
+            assert loc == rowptr_s[row]
+            if deg == 0:
+                assert wn == 0 and rows <= W
+            else:
+                assert wn == wn_tab[deg] and rows <= br_tab[deg]
+                assert rows * deg <= DB and rows * (-(-deg // wn)) <= W   # I3
+            covered_rows[row:row + rows] += 1
+            key = (deg, row, loc)
+        else:
+            assert deg_s[row] == deg and 1 <= info <= H                   # I4
+            assert rowptr_s[row] <= loc and loc + info <= rowptr_s[row + 1]
+            chunks[row] += 1
+            key = (deg, row, loc)
+        if prev is not None:
+            assert key > prev                                             # I5
+        prev = key
+    small = deg_s <= DB
+    assert np.all(covered_rows[small] == 1) and np.all(covered_rows[~small] == 0)
+    assert np.all(chunks[~small] == -(-deg_s[~small] // H)) and np.all(chunks[small] == 0)  # I7
+    # I6: closed-form entry count
+    want = 0
+    for d in np.unique(deg_s[small]):
+        c = int((deg_s == d).sum())
+        want += -(-c // (W if d == 0 else int(br_tab[d])))
+    want += int((-(-deg_s[~small] // H)).sum())
+    assert len(meta) == want
+
+
+@pytest.mark.parametrize("W,Z,H", PARAMS)
+@pytest.mark.parametrize("seed", [0, 1])
+def test_partition_invariants_and_replay(W, Z, H, seed):
+    g = _mixed_graph(20 + seed, n=350, max_deg=1500, dupes=True)
+    p = oracle.plan(g.rowptr, g.colidx, g.vals, W, Z, H)
+    _check_partition(p["rowptr_s"], p["meta"], W, Z, H)
+    X = np.random.default_rng(seed).standard_normal((g.n_cols, 5)).astype(np.float32)
+    Y, cover, row_hits, hub_chunks = oracle.replay_meta(
+        p["rowptr_s"], p["colidx_s"], p["vals_s"], p["perm"], p["meta"], W, Z, X)
+    assert np.all(cover == 1)                                             # I1
+    # Replaying visits each row's nnz in ascending order, so the float64 sums
+    # match the definition exactly.
+    assert np.array_equal(Y, oracle.spmm(g.rowptr, g.colidx, g.vals, X))
+
+
+def test_partition_all_empty_rows():
+    rowptr = np.zeros(40, np.int32)       # 39 rows, no nnz
+    meta = oracle.partition(rowptr, 16, 32)
+    assert meta.tolist() == [[0, 0, 0, 16], [0, 0, 16, 16], [0, 0, 32, 7]]
+    assert oracle.partition(np.zeros(1, np.int32), 16, 32).shape == (0, 4)
+
+
+def test_partition_hub_boundaries():
+    W, Z = 4, 8                      # deg_bound 32
+    for d, H, want_chunks in [(32, 0, None), (33, 0, [32, 1]), (64, 0, [32, 32]), (65, 0, [32, 32, 1]),
+                              (100, 7, [7] * 14 + [2])]:
+        rowptr = np.array([0, d], np.int32)
+        meta = oracle.partition(rowptr, W, Z, H)
+        if want_chunks is None:
+            assert meta.tolist() == [[d, 0, 0, (8 << 16) | 1]]
+        else:
+            assert [m[3] for m in meta.tolist()] == want_chunks
+            assert [m[1] for m in meta.tolist()] == list(np.cumsum([0] + want_chunks[:-1]))
+
+
+def test_metadata_storage_ratio_eq1():
+    """Sec. III-C, Eq. 1 and the storage example: with 12 warps per block and
+    well-populated degree classes, block metadata is ~1/12 (about 8%) of the
+    per-warp metadata."""
+    rng = np.random.default_rng(5)
+    deg = rng.integers(1, 385, size=200_000)
+    rowptr = np.concatenate([[0], np.cumsum(deg)]).astype(np.int32)
+    perm = oracle.degree_sort(rowptr)
+    rowptr_s = np.concatenate([[0], np.cumsum(deg[perm])]).astype(np.int32)
+    meta = oracle.partition(rowptr_s, 12, 32)
+    warps = 0
+    for deg_, loc, row, info in meta.tolist():
+        wn, rows = info >> 16, info & 0xFFFF
+        warps += rows * (-(-deg_ // wn))
+    ratio = len(meta) / warps
+    assert 0.080 <= ratio <= 0.086
+
+
+def test_partition_rejects_bad_input():
+    with pytest.raises(oracle.OracleError):
+        oracle.partition(np.array([0, 5, 3], np.int32), 16, 32)
+    with pytest.raises(oracle.OracleError):
+        oracle.partition(np.array([0, 1], np.int32), 0, 32)
