@@ -1,0 +1,251 @@
+"""Benchmark of the Accel-GCN aggregation path on one MI355X.
+
+One step = the whole path over one synthetic graph: the device plan (degree
+sort, relayout, Alg. 1/2 partition, one host sync) followed by the SpMM at
+every feature width of the workload (default: the 230,000-node Chung-Lu
+power-law graph, mean degree 50, F = 16, 32, 64, 128, 256), then the plan is
+released. Inputs (CSR and X for every F) are resident in HBM before timing.
+
+Prints ONE JSON line. value = whole-step throughput in GFLOP/s, FLOPs being
+2 * nnz * F summed over the F sweep (the plan adds time, not FLOPs).
+Extra keys: per-F execute timings, plan time, the roofline of the dominant
+kernel (measured with HIP events recorded by the library around that kernel
+in every timed step) and the single-threaded CPU oracle on a row sample.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--F 16,32,...] [--no-cpu-baseline] [--copy-probe]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import graphgen  # noqa: E402
+
+METRIC = "SpMM GFLOP/s (2·nnz·F) and % of HBM roofline, F=16..256"
+HBM_PEAK_GBPS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2308_11825_amd", "csrc", "agcn_spmm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_traffic.json")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_bytes(st, F, n_ref):
+    """Algorithmic HBM bytes of one launch of each execute kernel.
+
+    k_spmm:       8 nnz (sorted column index + value) + 16 per entry (metadata)
+                  + 4 per non-hub row (perm) + 4 F per referenced X row (each once)
+                  + 4 F per non-hub Y row + 4 F per hub chunk (partial row written)
+    k_hub_reduce: 4 F per hub chunk (partial row read) + 4 F per hub row (Y)
+                  + 8 per hub row (perm, chunk offset)
+    """
+    nonhub = st.n_rows - st.n_hub_rows
+    k7 = (8 * st.nnz + 16 * st.n_entries + 4 * nonhub + 4 * F * n_ref + 4 * F * nonhub
+          + 4 * F * st.n_hub_chunks)
+    k8 = 4 * F * st.n_hub_chunks + 4 * F * st.n_hub_rows + 8 * st.n_hub_rows
+    return k7, k8
+
+
+def source_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def cpu_baseline(g, name, Fs, params, frac, seed=0):
+    """Single-threaded oracle: full plan + SpMM of a random row sample for
+    every F, extrapolated to all rows by nnz."""
+    import oracle
+    W, Z, H = params
+    t0 = time.perf_counter()
+    p = oracle.plan(g.rowptr, g.colidx, g.vals, W, Z, H)
+    t_plan = time.perf_counter() - t0
+    del p
+    rng = np.random.default_rng(seed)
+    rows = np.sort(rng.choice(g.n_rows, size=max(1, int(frac * g.n_rows)), replace=False)).astype(np.int32)
+    nnz_s = int(g.degrees[rows].sum())
+    t_spmm = 0.0
+    for F in Fs:
+        X = graphgen.workload_features(name, g, F)
+        t0 = time.perf_counter()
+        oracle.spmm_rows(g.rowptr, g.colidx, g.vals, X, rows)
+        t_spmm += time.perf_counter() - t0
+    scale = g.nnz / max(nnz_s, 1)
+    t_step = t_plan + t_spmm * scale
+    flops = sum(2.0 * g.nnz * F for F in Fs)
+    return {
+        "value": round(flops / t_step / 1e9, 4), "unit": "GFLOP/s", "cores": 1, "kind": "oracle",
+        "sample": (f"full oracle plan ({t_plan:.2f}s) + oracle SpMM over {rows.size} random rows "
+                   f"({nnz_s} nnz, {100 * nnz_s / g.nnz:.1f}% of nnz) for F={Fs} "
+                   f"({t_spmm:.2f}s), extrapolated by nnz to the full step"),
+        "measured_s": round(t_plan + t_spmm, 3),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="sweep_powerlaw", choices=sorted(graphgen.CONFIGS))
+    ap.add_argument("--F", default=None, help="comma-separated feature widths")
+    ap.add_argument("--W", type=int, default=None)
+    ap.add_argument("--Z", type=int, default=None)
+    ap.add_argument("--H", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-frac", type=float, default=0.2)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="after timing, run a plain device copy of 1 GiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(sharding is described in DESIGN.md but not built).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2308_11825_amd as agcn
+
+    name = args.workload
+    Fs = [int(f) for f in args.F.split(",")] if args.F else list(graphgen.CONFIGS[name]["F"])
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = graphgen.make(name, verbose=False)
+    log(f"workload {name}: {graphgen.stats(g)}")
+    n_ref = int(np.count_nonzero(np.bincount(g.colidx, minlength=g.n_cols)))
+
+    prm = agcn.agcn_default_params()
+    if args.W is not None:
+        prm.max_block_waves = args.W
+    if args.Z is not None:
+        prm.max_wave_nzs = args.Z
+    if args.H is not None:
+        prm.hub_chunk_nnz = args.H
+
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    d_rowptr, d_colidx, d_vals = t(g.rowptr), t(g.colidx), t(g.vals)
+    Xs = {F: t(graphgen.workload_features(name, g, F)) for F in Fs}
+    Ys = {F: torch.empty((g.n_rows, F), dtype=torch.float32, device=dev) for F in Fs}
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+
+    # Workspace sized from a probe plan (same parameters, same graph).
+    probe = agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
+                                  d_colidx.data_ptr(), d_vals.data_ptr(), prm, sh)
+    st = agcn.agcn_plan_info(probe)
+    ws_bytes = agcn.agcn_spmm_workspace_size(probe, max(Fs))
+    agcn.agcn_plan_destroy(probe)
+    ws = torch.empty(max(1, (ws_bytes + 3) // 4), dtype=torch.float32, device=dev)
+    log(f"plan: entries={st.n_entries} hub_rows={st.n_hub_rows} hub_chunks={st.n_hub_chunks} "
+        f"W={st.max_block_waves} Z={st.max_wave_nzs} H={st.hub_chunk_nnz} ws={ws_bytes}B")
+
+    def new_event():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)  # creates the underlying hipEvent_t
+        return e
+
+    def step(evs):
+        plan = agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
+                                     d_colidx.data_ptr(), d_vals.data_ptr(), prm, sh)
+        for F in Fs:
+            e = evs[F] if evs is not None else (None, None, None)
+            agcn.agcn_spmm_timed(plan, F, Xs[F].data_ptr(), F, Ys[F].data_ptr(), F,
+                                 ws.data_ptr(), sh, *[x.cuda_event if x is not None else None
+                                                      for x in e])
+        agcn.agcn_plan_destroy(plan)
+
+    for i in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    events = [{F: (new_event(), new_event(), new_event()) for F in Fs} for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(events[k])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+    log(f"timed {args.steps} steps: {ms_step:.4f} ms/step")
+
+    per_f = {}
+    flops_step = 0.0
+    exec_ms_sum = 0.0
+    for F in Fs:
+        k7 = np.array([events[k][F][0].elapsed_time(events[k][F][1]) for k in range(args.steps)])
+        k8 = np.array([events[k][F][1].elapsed_time(events[k][F][2]) for k in range(args.steps)])
+        b7, b8 = kernel_bytes(st, F, n_ref)
+        ex_ms = float(np.mean(k7 + k8))
+        exec_ms_sum += ex_ms
+        fl = 2.0 * g.nnz * F
+        flops_step += fl
+        per_f[F] = {
+            "exec_ms": round(ex_ms, 5), "spmm_ms": round(float(k7.mean()), 5),
+            "hub_reduce_ms": round(float(k8.mean()), 5),
+            "gflops": round(fl / (ex_ms * 1e-3) / 1e9, 2),
+            "alg_GBps": round((b7 + b8) / (ex_ms * 1e-3) / 1e9, 1),
+            "frac_hbm": round((b7 + b8) / (ex_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "spmm_bytes": int(b7), "spmm_GBps": round(b7 / (k7.mean() * 1e-3) / 1e9, 1),
+        }
+    plan_ms = ms_step - exec_ms_sum
+    dom = max(Fs, key=lambda F: per_f[F]["spmm_ms"])
+    ach = per_f[dom]["spmm_GBps"]
+    traffic = None
+    try:
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("source_hash") == source_hash() and tr.get("workload") == name:
+            traffic = tr.get("per_launch_bytes", {}).get(str(dom))
+    except (OSError, ValueError):
+        pass
+    roofline = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                "kernel": f"k_spmm<4> F={dom}", "alg_bytes_per_launch": per_f[dom]["spmm_bytes"],
+                "avg_launch_ms": per_f[dom]["spmm_ms"]}
+
+    if args.copy_probe:
+        src = torch.empty(256 * 2**20, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy probe: 3 x 1 GiB device copies")
+
+    out = {
+        "metric": METRIC, "value": round(flops_step / (ms_step * 1e-3) / 1e9, 3), "unit": "GFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": name, "n_rows": g.n_rows, "nnz": g.nnz, "F": Fs,
+                   "max_block_waves": st.max_block_waves, "max_wave_nzs": st.max_wave_nzs,
+                   "hub_chunk_nnz": st.hub_chunk_nnz, "n_entries": st.n_entries,
+                   "n_hub_rows": st.n_hub_rows, "parallelism": "single GPU"},
+        "plan_ms": round(plan_ms, 4),
+        "spmm_only_gflops": round(flops_step / (exec_ms_sum * 1e-3) / 1e9, 2),
+        "per_F": per_f,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(g, name, Fs, (st.max_block_waves, st.max_wave_nzs,
+                                                         st.hub_chunk_nnz), args.cpu_frac)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

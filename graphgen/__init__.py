@@ -258,6 +258,9 @@ def random_csr(n_rows: int, n_cols: int, degrees, seed: int, dupes: bool = False
     cols = []
     for i in range(n_rows):
         d = int(deg[i])
+        if d == 0:
+            cols.append(np.zeros(0, np.int32))
+            continue
         if dupes:
             c = rng.integers(0, n_cols, size=d)
         else:

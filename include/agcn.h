@@ -1,0 +1,167 @@
+/*
+ * agcn.h -- C ABI of libagcn, the MI355X (gfx950) implementation of the
+ * Accel-GCN neighbour-aggregation SpMM (arXiv 2308.11825).
+ *
+ * The path computes Y = A X, where A is an n_rows x n_cols sparse matrix in
+ * CSR (int32 row pointer and column indices, float32 values) -- in a GCN
+ * layer, the normalised adjacency A' of Sec. II-A -- and X is a dense
+ * row-major n_cols x F float32 matrix. It has two calls, following the
+ * paper's split between preprocessing and kernel (Sec. III-C / III-D):
+ *
+ *   agcn_plan_create  degree sort (Sec. III-C "Degree Sorting") and
+ *                     block-level partitioning (Alg. 1, Alg. 2), all on the
+ *                     device; independent of F.
+ *   agcn_spmm         the SpMM for one F (Sec. III-D): per-block staging of
+ *                     the block's column indices and values, warp workloads
+ *                     deduced from the block's metadata entry, lanes laid
+ *                     across F ("combined warp"), fixed-order partial sums
+ *                     in place of the paper's atomics.
+ *
+ * Conventions for every call:
+ *   - Pointers named d_* are device pointers (memory of the current HIP
+ *     device); h_* are host pointers. The caller owns every pointer it
+ *     passes; the library never frees caller memory.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   - Return value: AGCN_OK (0) or one of the AGCN_ERR_* codes. On error,
+ *     agcn_last_error() describes it (thread-local). Argument checks run on
+ *     the host before any HIP call. No C++ exception crosses this boundary.
+ *   - Terminology: a "wave" is one 64-lane CDNA wavefront; a "virtual warp"
+ *     (vwarp) is the unit the paper calls a warp: one slice of one row's
+ *     nnz, covering all F columns. max_block_waves counts vwarps per block.
+ */
+#ifndef AGCN_H
+#define AGCN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum agcn_status {
+  AGCN_OK = 0,
+  AGCN_ERR_INVALID_ARGUMENT = 1, /* bad pointer, size, parameter or aliasing */
+  AGCN_ERR_INVALID_INPUT = 2,    /* CSR content invalid (see agcn_plan_create) */
+  AGCN_ERR_UNSUPPORTED = 3,      /* sizes beyond the int32 metadata format */
+  AGCN_ERR_OUT_OF_MEMORY = 4,    /* device allocation failed */
+  AGCN_ERR_HIP = 5               /* a HIP runtime call or launch failed */
+};
+
+/* Partition parameters (Alg. 1): W = max_block_waves vwarps per block, each
+ * vwarp holding at most Z = max_wave_nzs nnz; deg_bound = W * Z. Rows of
+ * degree > deg_bound are cut into chunks of hub_chunk_nnz nnz (the paper
+ * uses deg_bound; 0 selects deg_bound).
+ * Limits: 1 <= W <= 32; 1 <= Z; W * Z <= 4096; 0 <= hub_chunk_nnz <= 4096.
+ * flags must be 0 (reserved). */
+typedef struct agcn_plan_params {
+  int32_t max_block_waves;
+  int32_t max_wave_nzs;
+  int32_t hub_chunk_nnz;
+  uint32_t flags;
+} agcn_plan_params;
+
+/* Plan facts, for reporting and for sizing host export buffers. */
+typedef struct agcn_plan_stats {
+  int32_t n_rows;
+  int32_t n_cols;
+  int64_t nnz;
+  int64_t n_entries;       /* metadata entries = blocks of the partition */
+  int64_t hub_first_entry; /* index of the first hub-chunk entry (= n_entries if none) */
+  int64_t n_hub_chunks;    /* entries with deg > deg_bound */
+  int32_t n_hub_rows;      /* rows with degree > deg_bound */
+  int32_t hub_first_row;   /* sorted position of the first such row */
+  int32_t deg_bound;       /* W * Z */
+  int32_t hub_chunk_nnz;   /* effective H */
+  int32_t max_deg;
+  int32_t max_block_waves;
+  int32_t max_wave_nzs;
+  int32_t reserved;
+  size_t device_bytes;     /* device memory the plan holds */
+} agcn_plan_stats;
+
+typedef struct agcn_plan* agcn_plan_t;
+
+/* Fills *p with the library defaults (tuned for MI355X; the paper's own
+ * values are W = 12, Z = 32). */
+void agcn_default_params(agcn_plan_params* p);
+
+/* Degree sort + block-level partition on the device (Sec. III-C, Alg. 1-2).
+ *
+ * Inputs: d_rowptr[n_rows + 1], d_colidx[nnz], d_vals[nnz] on the current
+ * device; params NULL = defaults. The plan copies what it needs (sorted
+ * permutation, sorted CSR copy, metadata); the inputs may be freed once the
+ * call returns. Work is ordered on `stream`; the call synchronises that
+ * stream once (to read back the number of metadata entries).
+ *
+ * The CSR is validated on the device: rowptr[0] == 0, non-decreasing,
+ * rowptr[n_rows] == nnz, 0 <= colidx[e] < n_cols. A violation returns
+ * AGCN_ERR_INVALID_INPUT and no plan. Column indices need not be sorted and
+ * may repeat (repeated entries add up).
+ *
+ * Errors: INVALID_ARGUMENT (null out, negative sizes, null arrays with
+ * n_rows > 0 or nnz > 0, parameters outside the limits), UNSUPPORTED
+ * (nnz >= 2^31 or n_rows + nnz / H + 1 >= 2^31), OUT_OF_MEMORY, HIP.
+ * On any error *out is set to NULL. */
+int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t nnz,
+                     const int32_t* d_rowptr, const int32_t* d_colidx, const float* d_vals,
+                     const agcn_plan_params* params, void* stream);
+
+/* Device workspace agcn_spmm needs for feature width F: n_hub_chunks * F * 4
+ * bytes (partial rows of the hub chunks; 0 when the plan has no hub rows). */
+int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes);
+
+/* Y = A X for one F (Sec. III-D). Asynchronous on `stream`.
+ *
+ * d_X: n_cols rows of F floats, row stride ldx >= F (elements); d_Y: n_rows
+ * rows, stride ldy >= F. Every Y row is written exactly once (empty rows get
+ * zeros), so Y needs no clearing. X and Y must not overlap. d_ws: at least
+ * agcn_spmm_workspace_size(plan, F) bytes, may be NULL when that is 0.
+ * The 128-bit path runs when F, ldx and ldy are multiples of 4 and X, Y, ws
+ * are 16-byte aligned; otherwise a 32-bit path runs (same results up to
+ * float rounding order, both deterministic).
+ * Result: bitwise reproducible run to run; no atomics.
+ * The plan is read-only here: concurrent calls on different streams are
+ * safe when each has its own Y and ws. Must run on the plan's device.
+ * Errors: INVALID_ARGUMENT (null plan or pointers, F < 1, ld < F, overlap,
+ * missing workspace, wrong device), HIP. */
+int agcn_spmm(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+              int64_t ldy, void* d_ws, void* stream);
+
+/* agcn_spmm plus timing marks: records the caller's hipEvent_t handles (each
+ * may be NULL) on `stream` before the aggregation kernel (ev_begin), between
+ * it and the hub-row reduction (ev_mid), and after the reduction (ev_end).
+ * Same kernels, same launch shapes; used to time the aggregation kernel by
+ * itself. */
+int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+                    int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
+                    void* ev_end);
+
+/* Fills *out. Host-only, no HIP call. */
+int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* out);
+
+/* Copies the plan to host memory (synchronous).
+ * Any pointer may be NULL to skip that array. Sizes: h_perm[n_rows] (sorted
+ * position -> original row), h_rowptr_s[n_rows + 1], h_colidx_s[nnz],
+ * h_vals_s[nnz] (the CSR with rows in sorted order), h_meta[4 * n_entries]
+ * ({deg, loc, row, info} per entry: degree of the entry's rows; first nnz
+ * in the sorted CSR; first sorted row; for deg <= deg_bound
+ * warp_nzs << 16 | rows, else the chunk's nnz). */
+int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s,
+                     int32_t* h_colidx_s, float* h_vals_s, int32_t* h_meta);
+
+/* Frees the plan's device memory (synchronises the device first). NULL is
+ * ignored. No agcn_spmm on this plan may be in flight. */
+void agcn_plan_destroy(agcn_plan_t plan);
+
+/* Static text for a status code. */
+const char* agcn_status_string(int status);
+
+/* Description of the last error on this thread ("" if none). Valid until the
+ * next failing call on the same thread. */
+const char* agcn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AGCN_H */

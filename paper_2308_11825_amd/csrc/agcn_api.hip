@@ -1,0 +1,239 @@
+// C ABI of libagcn: argument checking, error reporting, plan lifetime.
+// Every check that can be made on the host runs before the first HIP call.
+#include <algorithm>
+#include <climits>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "agcn_internal.hpp"
+
+namespace agcn {
+
+namespace {
+thread_local std::string g_last_error;
+
+bool ranges_overlap(const void* a, size_t a_bytes, const void* b, size_t b_bytes) {
+  if (a_bytes == 0 || b_bytes == 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+  return a0 < b0 + b_bytes && b0 < a0 + a_bytes;
+}
+
+// Bytes spanned by `rows` rows of F floats with stride ld (0 if rows == 0);
+// false if it does not fit in size_t.
+bool span_bytes(int64_t rows, int64_t ld, int64_t F, size_t* out) {
+  if (rows <= 0) {
+    *out = 0;
+    return true;
+  }
+  if (ld > (INT64_MAX / 4 - F) / rows) return false;
+  *out = (size_t)(((rows - 1) * ld + F) * 4);
+  return true;
+}
+}  // namespace
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+int fail(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  (void)hipGetLastError();
+  g_last_error = std::string(what) + ": " + hipGetErrorName(e) + " (" + hipGetErrorString(e) + ")";
+  return AGCN_ERR_HIP;
+}
+
+}  // namespace agcn
+
+using agcn::fail;
+
+extern "C" {
+
+void agcn_default_params(agcn_plan_params* p) {
+  if (p == nullptr) return;
+  p->max_block_waves = 16;
+  p->max_wave_nzs = 32;
+  p->hub_chunk_nnz = 0;
+  p->flags = 0;
+}
+
+const char* agcn_status_string(int status) {
+  switch (status) {
+    case AGCN_OK: return "AGCN_OK";
+    case AGCN_ERR_INVALID_ARGUMENT: return "AGCN_ERR_INVALID_ARGUMENT";
+    case AGCN_ERR_INVALID_INPUT: return "AGCN_ERR_INVALID_INPUT";
+    case AGCN_ERR_UNSUPPORTED: return "AGCN_ERR_UNSUPPORTED";
+    case AGCN_ERR_OUT_OF_MEMORY: return "AGCN_ERR_OUT_OF_MEMORY";
+    case AGCN_ERR_HIP: return "AGCN_ERR_HIP";
+    default: return "AGCN_ERR_UNKNOWN";
+  }
+}
+
+const char* agcn_last_error(void) { return agcn::g_last_error.c_str(); }
+
+static void plan_free(agcn_plan* p) {
+  if (p == nullptr) return;
+  if (p->base != nullptr) (void)hipFree(p->base);
+  delete p;
+}
+
+int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t nnz,
+                     const int32_t* d_rowptr, const int32_t* d_colidx, const float* d_vals,
+                     const agcn_plan_params* params, void* stream) {
+  if (out == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "out is NULL");
+  *out = nullptr;
+  if (n_rows < 0 || n_cols < 0 || nnz < 0)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "n_rows, n_cols and nnz must be >= 0");
+  if (n_rows == 0 && nnz > 0)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "nnz > 0 with no rows");
+  if (nnz >= ((int64_t)1 << 31))
+    return fail(AGCN_ERR_UNSUPPORTED, "nnz >= 2^31 does not fit the int32 metadata format");
+  if (n_rows > 0 && d_rowptr == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "rowptr is NULL");
+  if (nnz > 0 && (d_colidx == nullptr || d_vals == nullptr))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "colidx or vals is NULL");
+  agcn_plan_params prm;
+  if (params == nullptr) agcn_default_params(&prm); else prm = *params;
+  if (prm.flags != 0) return fail(AGCN_ERR_INVALID_ARGUMENT, "flags must be 0");
+  if (prm.max_block_waves < 1 || prm.max_block_waves > agcn::kMaxBlockWaves)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "max_block_waves must be in [1, 32]");
+  if (prm.max_wave_nzs < 1 ||
+      (int64_t)prm.max_block_waves * prm.max_wave_nzs > agcn::kMaxEntryNnz)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "need max_wave_nzs >= 1 and W * Z <= 4096");
+  if (prm.hub_chunk_nnz < 0 || prm.hub_chunk_nnz > agcn::kMaxEntryNnz)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "hub_chunk_nnz must be in [0, 4096]");
+  const int32_t deg_bound = prm.max_block_waves * prm.max_wave_nzs;
+  const int32_t H = prm.hub_chunk_nnz > 0 ? prm.hub_chunk_nnz : deg_bound;
+  if (agcn::spmm_lds_bytes_max(prm.max_block_waves, std::max(deg_bound, H)) > 65536)
+    return fail(AGCN_ERR_INVALID_ARGUMENT,
+                "parameters need more than 64 KiB of LDS per workgroup (reduce W, Z or H)");
+  if ((int64_t)n_rows + nnz / H + 1 >= INT32_MAX)
+    return fail(AGCN_ERR_UNSUPPORTED, "too many metadata entries for int32 indexing");
+
+  int dev = 0;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return agcn::hip_fail(he, "hipGetDevice");
+
+  agcn_plan* p = new (std::nothrow) agcn_plan();
+  if (p == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "host allocation failed");
+  p->device = dev;
+  p->n_rows = n_rows;
+  p->n_cols = n_cols;
+  p->nnz = nnz;
+  p->W = prm.max_block_waves;
+  p->Z = prm.max_wave_nzs;
+  p->deg_bound = deg_bound;
+  p->H = H;
+  int rc;
+  try {
+    rc = agcn::build_plan(p, d_rowptr, d_colidx, d_vals, static_cast<hipStream_t>(stream));
+  } catch (const std::bad_alloc&) {
+    rc = fail(AGCN_ERR_OUT_OF_MEMORY, "host allocation failed");
+  } catch (...) {
+    rc = fail(AGCN_ERR_HIP, "unexpected exception while building the plan");
+  }
+  if (rc != AGCN_OK) {
+    // Let queued plan kernels finish before their memory is released.
+    (void)hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    plan_free(p);
+    return rc;
+  }
+  *out = p;
+  return AGCN_OK;
+}
+
+int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes) {
+  if (plan == nullptr || bytes == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "NULL argument");
+  if (F < 1) return fail(AGCN_ERR_INVALID_ARGUMENT, "F must be >= 1");
+  const int64_t chunks = plan->n_hub_rows > 0 ? (int64_t)plan->n_entries - plan->hub_first_entry : 0;
+  *bytes = (size_t)chunks * (size_t)F * sizeof(float);
+  return AGCN_OK;
+}
+
+int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+                    int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
+                    void* ev_end) {
+  if (plan == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "plan is NULL");
+  if (F < 1) return fail(AGCN_ERR_INVALID_ARGUMENT, "F must be >= 1");
+  if (ldx < F || ldy < F) return fail(AGCN_ERR_INVALID_ARGUMENT, "ldx and ldy must be >= F");
+  if (plan->n_rows > 0 && d_Y == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "Y is NULL");
+  if (plan->nnz > 0 && d_X == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "X is NULL");
+  size_t ws_need = 0;
+  agcn_spmm_workspace_size(plan, F, &ws_need);
+  if (ws_need > 0 && d_ws == nullptr)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "this plan has hub rows: a workspace is required");
+  size_t xb = 0, yb = 0;
+  if (!agcn::span_bytes(d_X ? plan->n_cols : 0, ldx, F, &xb) ||
+      !agcn::span_bytes(plan->n_rows, ldy, F, &yb))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "matrix extent overflows");
+  if (agcn::ranges_overlap(d_X, xb, d_Y, yb))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "X and Y overlap");
+  if (ws_need > 0 && (agcn::ranges_overlap(d_ws, ws_need, d_Y, yb) ||
+                      agcn::ranges_overlap(d_ws, ws_need, d_X, xb)))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "workspace overlaps X or Y");
+  int dev = -1;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return agcn::hip_fail(he, "hipGetDevice");
+  if (dev != plan->device)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "current device differs from the plan's device");
+  return agcn::run_spmm(plan, F, d_X, ldx, d_Y, ldy, static_cast<float*>(d_ws),
+                        static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(ev_begin),
+                        static_cast<hipEvent_t>(ev_mid), static_cast<hipEvent_t>(ev_end));
+}
+
+int agcn_spmm(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+              int64_t ldy, void* d_ws, void* stream) {
+  return agcn_spmm_timed(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, nullptr, nullptr, nullptr);
+}
+
+int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* s) {
+  if (plan == nullptr || s == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "NULL argument");
+  std::memset(s, 0, sizeof(*s));
+  s->n_rows = plan->n_rows;
+  s->n_cols = plan->n_cols;
+  s->nnz = plan->nnz;
+  s->n_entries = plan->n_entries;
+  s->hub_first_entry = plan->hub_first_entry;
+  s->n_hub_chunks = plan->n_hub_rows > 0 ? plan->n_entries - plan->hub_first_entry : 0;
+  s->n_hub_rows = plan->n_hub_rows;
+  s->hub_first_row = plan->hub_first_row;
+  s->deg_bound = plan->deg_bound;
+  s->hub_chunk_nnz = plan->H;
+  s->max_deg = plan->max_deg;
+  s->max_block_waves = plan->W;
+  s->max_wave_nzs = plan->Z;
+  s->device_bytes = plan->bytes;
+  return AGCN_OK;
+}
+
+int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s, int32_t* h_colidx_s,
+                     float* h_vals_s, int32_t* h_meta) {
+  if (plan == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "plan is NULL");
+  struct Item {
+    void* dst;
+    const void* src;
+    size_t bytes;
+  } items[] = {
+      {h_perm, plan->perm, (size_t)plan->n_rows * 4},
+      {h_rowptr_s, plan->rowptr_s, ((size_t)plan->n_rows + 1) * 4},
+      {h_colidx_s, plan->colidx_s, (size_t)plan->nnz * 4},
+      {h_vals_s, plan->vals_s, (size_t)plan->nnz * 4},
+      {h_meta, plan->meta, (size_t)plan->n_entries * 16},
+  };
+  int dev = -1;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return agcn::hip_fail(he, "hipGetDevice");
+  if (dev != plan->device)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "current device differs from the plan's device");
+  for (const Item& it : items) {
+    if (it.dst == nullptr || it.bytes == 0) continue;
+    he = hipMemcpy(it.dst, it.src, it.bytes, hipMemcpyDeviceToHost);
+    if (he != hipSuccess) return agcn::hip_fail(he, "hipMemcpy(export)");
+  }
+  return AGCN_OK;
+}
+
+void agcn_plan_destroy(agcn_plan_t plan) { plan_free(plan); }
+
+}  // extern "C"

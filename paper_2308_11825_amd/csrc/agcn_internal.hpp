@@ -1,0 +1,78 @@
+// Internal declarations shared by the libagcn sources (plan, SpMM, C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/agcn.h"
+
+namespace agcn {
+
+// Error flags the plan kernels raise on the device (OR-ed into one word).
+enum : uint32_t {
+  kErrRowptrStart = 1u << 0,   // rowptr[0] != 0
+  kErrRowptrOrder = 1u << 1,   // rowptr decreases
+  kErrRowptrEnd = 1u << 2,     // rowptr[n_rows] != nnz
+  kErrColumn = 1u << 3,        // a column index outside [0, n_cols)
+};
+
+// Facts the device computes while partitioning; read back once.
+struct PlanSummary {
+  int32_t n_entries;
+  int32_t hub_first_entry;
+  int32_t n_hub_rows;
+  int32_t hub_first_row;
+  int32_t max_deg;
+  uint32_t err;
+  int32_t pad[2];
+};
+
+// Largest number of (column, value) pairs one metadata entry stages in LDS.
+constexpr int kMaxEntryNnz = 4096;
+constexpr int kMaxBlockWaves = 32;
+// Feature columns one workgroup covers: 64 lanes x (4 or 1) floats.
+constexpr int kSliceLanes = 64;
+
+}  // namespace agcn
+
+struct agcn_plan {
+  int device = 0;
+  int32_t n_rows = 0, n_cols = 0;
+  int64_t nnz = 0;
+  int32_t W = 0, Z = 0, deg_bound = 0, H = 0;
+  int32_t n_entries = 0, hub_first_entry = 0, n_hub_rows = 0, hub_first_row = 0, max_deg = 0;
+  void* base = nullptr;  // single device allocation holding everything below
+  size_t bytes = 0;
+  int32_t* perm = nullptr;          // [n_rows]   sorted position -> original row
+  int32_t* rowptr_s = nullptr;      // [n_rows+1] sorted CSR
+  int32_t* colidx_s = nullptr;      // [nnz]
+  float* vals_s = nullptr;          // [nnz]
+  int4* meta = nullptr;             // [entries upper bound] {deg, loc, row, info}
+  int32_t* hub_chunk_off = nullptr; // [hub rows upper bound + 1] first chunk of each hub row
+};
+
+namespace agcn {
+
+// Thread-local error text (set by the failing call).
+void set_error(const std::string& msg);
+int fail(int status, const std::string& msg);
+int hip_fail(hipError_t e, const char* what);
+
+// Plan construction (agcn_plan.hip).
+int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
+               const float* d_vals, hipStream_t stream);
+
+// Execute (agcn_spmm.hip).
+int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,
+             float* ws, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_mid,
+             hipEvent_t ev_end);
+
+// Dynamic LDS bytes the SpMM kernel needs for a plan (worst case over F).
+size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz);
+
+inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace agcn

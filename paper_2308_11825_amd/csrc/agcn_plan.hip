@@ -1,0 +1,600 @@
+// Device-side preprocessing: degree sort and block-level partition
+// (Sec. III-C "Degree Sorting" and "Block-level Partition", Alg. 1 and Alg. 2).
+//
+// Pipeline (all on one stream, one host synchronisation at the end):
+//   k_init          clear the error word and the summary
+//   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer
+//   radix passes    stable LSD radix sort of row ids by degree, 8-bit digits:
+//                   k_radix_hist -> exclusive scan -> k_radix_scatter
+//   scan            rowptr_s = exclusive scan of the sorted degrees
+//   k_relayout      sorted CSR copy (column indices checked against n_cols)
+//   k_patterns      Alg. 1 table for d = 0..deg_bound
+//   k_class_start   first sorted row of each degree class 0..deg_bound+1
+//   k_seg_count     blocks per degree class / chunks per hub row
+//   scan            entry offsets of every segment
+//   k_meta_fill     one int4 {deg, loc, row, info} per entry, in Alg. 2's order
+//   k_hub_offsets   first chunk of each hub row + summary for the host
+//
+// Stability of the radix sort comes from giving each 64-lane wave a tile of
+// consecutive rows that it walks in order, ranking equal digits inside a
+// round with ballots; every count is an integer, so the result is exact.
+#include <algorithm>
+#include <climits>
+
+#include "agcn_internal.hpp"
+
+namespace agcn {
+namespace {
+
+constexpr int kThreads = 256;
+
+// Exclusive scan geometry.
+constexpr int kScanItems = 16;
+constexpr int kScanBlock = kThreads * kScanItems;  // 4096 elements per workgroup
+constexpr int kScanTopThreads = 1024;
+constexpr int kScanTopItems = 64;                   // <= 65536 partial sums
+constexpr int64_t kScanMaxN = (int64_t)kScanBlock * kScanTopThreads * kScanTopItems;
+
+// Radix sort geometry: one wave owns kRadixTile consecutive rows.
+constexpr int kRadixBins = 256;
+constexpr int kRadixItems = 32;
+constexpr int kRadixTile = 64 * kRadixItems;  // 2048
+constexpr int kRadixWaves = kThreads / 64;    // 4 tiles per workgroup
+
+// Relayout tile (sorted nnz positions per workgroup).
+constexpr int kRelayItems = 8;
+constexpr int kRelayTile = kThreads * kRelayItems;  // 2048
+
+constexpr uint32_t kErrInternal = 1u << 8;
+
+__device__ inline bool failed(const uint32_t* err) { return err[0] != 0; }
+
+__device__ inline int32_t wave_sum(int32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Inclusive scan over the 64 lanes of a wave.
+__device__ inline int32_t wave_inclusive_scan(int32_t v, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(v, o, 64);
+    if (lane >= o) v += y;
+  }
+  return v;
+}
+
+// Exclusive scan across a workgroup of T threads; *total receives the sum.
+template <int T>
+__device__ inline int32_t block_exclusive_scan(int32_t v, int32_t* total) {
+  __shared__ int32_t wsum[T / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int32_t inc = wave_inclusive_scan(v, lane);
+  if (lane == 63) wsum[w] = inc;
+  __syncthreads();
+  if (w == 0) {
+    const int32_t s = lane < T / 64 ? wsum[lane] : 0;
+    const int32_t si = wave_inclusive_scan(s, lane);
+    if (lane < T / 64) wsum[lane] = si;
+  }
+  __syncthreads();
+  *total = wsum[T / 64 - 1];
+  return (w > 0 ? wsum[w - 1] : 0) + inc - v;
+}
+
+// Lanes of the wave holding the same 8-bit digit (among valid lanes).
+__device__ inline uint64_t match_digit(uint32_t digit, bool valid) {
+  uint64_t m = __ballot(valid);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const bool bit = (digit >> b) & 1u;
+    const uint64_t bal = __ballot(bit);
+    m &= bit ? bal : ~bal;
+  }
+  return m;
+}
+
+// ---------------------------------------------------------------------------
+
+__global__ void k_init(uint32_t* err, PlanSummary* sum) {
+  if (threadIdx.x == 0) {
+    err[0] = 0;
+    sum->n_entries = 0;
+    sum->hub_first_entry = 0;
+    sum->n_hub_rows = 0;
+    sum->hub_first_row = 0;
+    sum->max_deg = 0;
+    sum->err = 0;
+  }
+}
+
+__global__ void k_set(int32_t* p, int32_t v) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) p[0] = v;
+}
+
+// Step (1) of the degree sort, plus the row-pointer checks.
+__global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
+                                                     const int32_t* __restrict__ rowptr,
+                                                     int32_t* __restrict__ deg, uint32_t* err) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n) return;
+  const int32_t a = rowptr[i], b = rowptr[i + 1];
+  uint32_t e = 0;
+  int32_t d = b - a;
+  if (a < 0 || b < a || (int64_t)b > nnz) {
+    e |= kErrRowptrOrder;
+    d = 0;
+  }
+  if (i == 0 && a != 0) e |= kErrRowptrStart;
+  if (i == n - 1 && (int64_t)b != nnz) e |= kErrRowptrEnd;
+  deg[i] = d;
+  if (e) atomicOr(err, e);
+}
+
+// Digit histogram of each wave tile; counts are stored digit-major so that one
+// exclusive scan yields every (digit, tile) start position.
+__global__ __launch_bounds__(kThreads) void k_radix_hist(int32_t n, const int32_t* __restrict__ keys,
+                                                         int shift, int32_t* __restrict__ counts,
+                                                         int32_t n_tiles, const uint32_t* err) {
+  if (failed(err)) return;
+  __shared__ int32_t cnt[kRadixWaves][kRadixBins];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t tile = (int64_t)blockIdx.x * kRadixWaves + wave;
+  if (tile >= n_tiles) return;  // uniform per wave; no workgroup barrier below
+  for (int d = lane; d < kRadixBins; d += 64) cnt[wave][d] = 0;
+  const int64_t base = tile * kRadixTile;
+  for (int j = 0; j < kRadixItems; ++j) {
+    const int64_t i = base + (int64_t)j * 64 + lane;
+    const bool valid = i < n;
+    const uint32_t digit = valid ? (((uint32_t)keys[i]) >> shift) & 0xFFu : 0u;
+    const uint64_t peers = match_digit(digit, valid);
+    // The lowest lane of each digit group adds the group's size (one writer per digit).
+    if (valid && __popcll(peers & __lanemask_lt()) == 0) cnt[wave][digit] += __popcll(peers);
+  }
+  for (int d = lane; d < kRadixBins; d += 64) counts[(int64_t)d * n_tiles + tile] = cnt[wave][d];
+}
+
+// Stable scatter: a row's new position is its (digit, tile) start plus the
+// number of earlier rows of the tile with the same digit.
+__global__ __launch_bounds__(kThreads) void k_radix_scatter(
+    int32_t n, const int32_t* __restrict__ keys_in, const int32_t* __restrict__ ids_in, int shift,
+    const int32_t* __restrict__ offsets, int32_t n_tiles, int32_t* __restrict__ keys_out,
+    int32_t* __restrict__ ids_out, const uint32_t* err) {
+  if (failed(err)) return;
+  __shared__ int32_t start[kRadixWaves][kRadixBins];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t tile = (int64_t)blockIdx.x * kRadixWaves + wave;
+  if (tile >= n_tiles) return;
+  for (int d = lane; d < kRadixBins; d += 64) start[wave][d] = offsets[(int64_t)d * n_tiles + tile];
+  const int64_t base = tile * kRadixTile;
+  for (int j = 0; j < kRadixItems; ++j) {
+    const int64_t i = base + (int64_t)j * 64 + lane;
+    const bool valid = i < n;
+    const int32_t key = valid ? keys_in[i] : 0;
+    const int32_t id = valid ? (ids_in ? ids_in[i] : (int32_t)i) : 0;
+    const uint32_t digit = (((uint32_t)key) >> shift) & 0xFFu;
+    const uint64_t peers = match_digit(digit, valid);
+    const int32_t rank = (int32_t)__popcll(peers & __lanemask_lt());
+    // All lanes read the digit's start before its single writer advances it
+    // (LDS operations of one wave complete in program order).
+    const int32_t pos = start[wave][digit] + rank;
+    if (valid) {
+      keys_out[pos] = key;
+      ids_out[pos] = id;
+    }
+    if (valid && rank == 0) start[wave][digit] += __popcll(peers);
+  }
+}
+
+// --- exclusive scan of int32 (three phases) ---------------------------------
+
+__global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t* __restrict__ in, int64_t n,
+                                                          int32_t* __restrict__ partials,
+                                                          const uint32_t* err) {
+  if (failed(err)) return;
+  __shared__ int32_t ws[kThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanBlock;
+  int32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const int64_t i = base + (int64_t)k * kThreads + threadIdx.x;
+    if (i < n) s += in[i];
+  }
+  s = wave_sum(s);
+  if ((threadIdx.x & 63) == 0) ws[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t t = 0;
+    for (int w = 0; w < kThreads / 64; ++w) t += ws[w];
+    partials[blockIdx.x] = t;
+  }
+}
+
+__global__ __launch_bounds__(kScanTopThreads) void k_scan_top(int32_t* __restrict__ partials,
+                                                              int32_t m, int32_t* total_out,
+                                                              const uint32_t* err) {
+  if (failed(err)) return;
+  const int64_t b0 = (int64_t)threadIdx.x * kScanTopItems;
+  int32_t s = 0;
+  for (int k = 0; k < kScanTopItems; ++k)
+    if (b0 + k < m) s += partials[b0 + k];
+  int32_t total;
+  int32_t run = block_exclusive_scan<kScanTopThreads>(s, &total);
+  for (int k = 0; k < kScanTopItems; ++k) {
+    if (b0 + k < m) {
+      const int32_t v = partials[b0 + k];
+      partials[b0 + k] = run;
+      run += v;
+    }
+  }
+  if (threadIdx.x == 0 && total_out) total_out[0] = total;
+}
+
+__global__ __launch_bounds__(kThreads) void k_scan_down(const int32_t* __restrict__ in, int64_t n,
+                                                        const int32_t* __restrict__ partials,
+                                                        int32_t* __restrict__ out,
+                                                        const uint32_t* err) {
+  if (failed(err)) return;
+  const int64_t i0 = (int64_t)blockIdx.x * kScanBlock + (int64_t)threadIdx.x * kScanItems;
+  int32_t v[kScanItems];
+  int32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    v[k] = (i0 + k < n) ? in[i0 + k] : 0;
+    s += v[k];
+  }
+  int32_t total;
+  int32_t run = block_exclusive_scan<kThreads>(s, &total) + partials[blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    if (i0 + k < n) out[i0 + k] = run;
+    run += v[k];
+  }
+}
+
+// --- relayout (step (3) of the degree sort) ----------------------------------
+
+// Largest r in [0, n) with rowptr_s[r] <= e (the row holding sorted nnz e).
+__device__ inline int32_t row_of(const int32_t* rowptr_s, int32_t n, int64_t e) {
+  int32_t a = 0, b = n - 1;
+  while (a < b) {
+    const int32_t mid = (int32_t)(((int64_t)a + b + 1) >> 1);
+    if (rowptr_s[mid] <= e) a = mid; else b = mid - 1;
+  }
+  return a;
+}
+
+// Each workgroup fills kRelayTile consecutive positions of the sorted CSR.
+// Degree-0 rows sort first, so every row that owns one of these positions
+// is non-empty and at most kRelayTile rows are involved.
+__global__ __launch_bounds__(kThreads) void k_relayout(
+    int32_t n, int64_t nnz, int32_t n_cols, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ colidx, const float* __restrict__ vals,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ rowptr_s,
+    int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, uint32_t* err) {
+  if (failed(err)) return;
+  __shared__ int32_t s_ptr[kRelayTile + 1];  // rowptr_s over the window rows (+1 end)
+  __shared__ int32_t s_src[kRelayTile];      // first nnz of each window row in the input CSR
+  __shared__ int32_t s_lo, s_hi;
+  const int64_t e0 = (int64_t)blockIdx.x * kRelayTile;
+  const int64_t e1 = e0 + kRelayTile < nnz ? e0 + kRelayTile : nnz;
+  if (threadIdx.x == 0) s_lo = row_of(rowptr_s, n, e0);
+  if (threadIdx.x == 1) s_hi = row_of(rowptr_s, n, e1 - 1);
+  __syncthreads();
+  const int32_t lo = s_lo;
+  const int32_t nw = s_hi - lo + 1;
+  if (nw > kRelayTile || nw < 1) {  // cannot happen for a sorted row order
+    if (threadIdx.x == 0) atomicOr(err, kErrInternal);
+    return;
+  }
+  for (int k = threadIdx.x; k <= nw; k += kThreads) s_ptr[k] = rowptr_s[lo + k];
+  for (int k = threadIdx.x; k < nw; k += kThreads) s_src[k] = rowptr[perm[lo + k]];
+  __syncthreads();
+  uint32_t bad = 0;
+#pragma unroll
+  for (int k = 0; k < kRelayItems; ++k) {
+    const int64_t e = e0 + (int64_t)k * kThreads + threadIdx.x;
+    if (e < e1) {
+      int32_t a = 0, b = nw - 1;
+      while (a < b) {
+        const int32_t mid = (a + b + 1) >> 1;
+        if (s_ptr[mid] <= e) a = mid; else b = mid - 1;
+      }
+      const int64_t src = (int64_t)s_src[a] + (e - s_ptr[a]);
+      const int32_t c = colidx[src];
+      const float v = vals[src];
+      if ((uint32_t)c >= (uint32_t)n_cols) bad = kErrColumn;
+      colidx_s[e] = c;
+      vals_s[e] = v;
+    }
+  }
+  if (bad) atomicOr(err, bad);
+}
+
+// --- partition ---------------------------------------------------------------
+
+// Alg. 1: for degree d, the smallest factor f of W with f * Z >= d gives
+// block_rows = W / f and warp_nzs = ceil(d / f). Stored as warp_nzs << 16 | rows.
+// Degree 0 (no nnz) gets W rows per block and warp_nzs 0.
+__global__ __launch_bounds__(kThreads) void k_patterns(int32_t W, int32_t Z, int32_t* pat) {
+  const int32_t d = blockIdx.x * kThreads + threadIdx.x;
+  if (d > W * Z) return;
+  if (d == 0) {
+    pat[0] = W;
+    return;
+  }
+  for (int32_t f = 1; f <= W; ++f) {
+    if (W % f == 0 && f * Z >= d) {
+      pat[d] = (((d + f - 1) / f) << 16) | (W / f);
+      return;
+    }
+  }
+}
+
+// cls[d] = first sorted row whose degree is >= d, for d in [0, DB + 1] (n if none).
+__global__ __launch_bounds__(kThreads) void k_class_start(int32_t n, const int32_t* __restrict__ deg_s,
+                                                          int32_t DB, int32_t* __restrict__ cls,
+                                                          const uint32_t* err) {
+  if (failed(err)) return;
+  const int64_t r = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (r > n) return;
+  const int32_t prev = r == 0 ? -1 : deg_s[r - 1];
+  const int32_t cur = r == n ? INT_MAX : deg_s[r];
+  const int32_t hi = cur < DB + 1 ? cur : DB + 1;
+  for (int32_t d = prev + 1; d <= hi; ++d) cls[d] = (int32_t)r;
+}
+
+// Segments: s <= DB is degree class s (ceil(count / block_rows) entries);
+// s > DB is hub row s - DB - 1 in sorted order (ceil(deg / H) chunk entries).
+__global__ __launch_bounds__(kThreads) void k_seg_count(int32_t n, const int32_t* __restrict__ deg_s,
+                                                        const int32_t* __restrict__ cls,
+                                                        const int32_t* __restrict__ pat, int32_t DB,
+                                                        int32_t H, int32_t S,
+                                                        int32_t* __restrict__ nb,
+                                                        const uint32_t* err) {
+  if (failed(err)) return;
+  const int64_t s = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (s >= S) return;
+  int64_t v = 0;
+  if (s <= DB) {
+    const int64_t cnt = cls[s + 1] - cls[s];
+    const int64_t br = pat[s] & 0xFFFF;
+    v = (cnt + br - 1) / br;
+  } else {
+    const int64_t r = (int64_t)cls[DB + 1] + (s - DB - 1);
+    if (r < n) v = ((int64_t)deg_s[r] + H - 1) / H;
+  }
+  nb[s] = (int32_t)v;
+}
+
+// Alg. 2's entries, each computed independently from its segment.
+__global__ __launch_bounds__(kThreads) void k_meta_fill(
+    const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ deg_s,
+    const int32_t* __restrict__ cls, const int32_t* __restrict__ pat,
+    const int32_t* __restrict__ seg_off, int32_t S, int32_t DB, int32_t H, int4* __restrict__ meta,
+    int64_t cap, const uint32_t* err) {
+  if (failed(err)) return;
+  const int64_t total = seg_off[S];
+  for (int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x; b < total && b < cap;
+       b += (int64_t)gridDim.x * kThreads) {
+    int32_t a = 0, c = S - 1;  // largest segment starting at or before b
+    while (a < c) {
+      const int32_t mid = (int32_t)(((int64_t)a + c + 1) >> 1);
+      if (seg_off[mid] <= b) a = mid; else c = mid - 1;
+    }
+    const int32_t j = (int32_t)(b - seg_off[a]);
+    int4 m;
+    if (a <= DB) {
+      const int32_t p = pat[a], br = p & 0xFFFF, wn = p >> 16;
+      const int32_t r0 = cls[a] + j * br;
+      const int32_t left = cls[a + 1] - r0;
+      const int32_t rows = left < br ? left : br;
+      m = make_int4(a, rowptr_s[r0], r0, (wn << 16) | rows);
+    } else {
+      const int32_t r = cls[DB + 1] + (a - DB - 1);
+      const int32_t d = deg_s[r];
+      const int32_t off = j * H;
+      const int32_t left = d - off;
+      m = make_int4(d, rowptr_s[r] + off, r, left < H ? left : H);
+    }
+    meta[b] = m;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_hub_offsets(
+    int32_t n, const int32_t* __restrict__ deg_s, const int32_t* __restrict__ cls,
+    const int32_t* __restrict__ seg_off, int32_t S, int32_t DB, int32_t hub_ub,
+    int32_t* __restrict__ hub_chunk_off, PlanSummary* sum, const uint32_t* err) {
+  const int64_t h = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const uint32_t e = err[0];
+  if (h == 0) sum->err = e;
+  if (e) return;
+  const int32_t first = cls[DB + 1];
+  const int32_t n_hub = n - first;
+  if (h <= n_hub && h <= hub_ub) hub_chunk_off[h] = seg_off[DB + 1 + h] - seg_off[DB + 1];
+  if (h == 0) {
+    sum->n_entries = seg_off[S];
+    sum->hub_first_entry = seg_off[DB + 1];
+    sum->n_hub_rows = n_hub;
+    sum->hub_first_row = first;
+    sum->max_deg = n > 0 ? deg_s[n - 1] : 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+
+inline unsigned grid_for(int64_t work, int per_block) {
+  return (unsigned)ceil_div64(work, per_block);
+}
+
+int check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? AGCN_OK : hip_fail(e, what);
+}
+
+// out[i] = sum of in[0..i) for i < n, and *total = sum of all (may alias out + n).
+int scan_exclusive(const int32_t* in, int64_t n, int32_t* out, int32_t* total, int32_t* partials,
+                   const uint32_t* err, hipStream_t st) {
+  if (n > kScanMaxN) return fail(AGCN_ERR_UNSUPPORTED, "scan longer than the supported maximum");
+  if (n == 0) {
+    if (total) k_set<<<1, 64, 0, st>>>(total, 0);
+    return check_launch("k_set");
+  }
+  const unsigned nb = grid_for(n, kScanBlock);
+  k_scan_reduce<<<nb, kThreads, 0, st>>>(in, n, partials, err);
+  k_scan_top<<<1, kScanTopThreads, 0, st>>>(partials, (int32_t)nb, total, err);
+  k_scan_down<<<nb, kThreads, 0, st>>>(in, n, partials, out, err);
+  return check_launch("scan");
+}
+
+struct Layout {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t at = off;
+    off += (bytes + 255) & ~size_t(255);
+    return at;
+  }
+};
+
+}  // namespace
+
+int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
+               const float* d_vals, hipStream_t st) {
+  const int64_t n = p->n_rows, nnz = p->nnz;
+  const int32_t W = p->W, Z = p->Z, DB = p->deg_bound, H = p->H;
+  const int64_t ent_ub = n + nnz / H + 1;         // every entry holds a row or a full chunk
+  const int64_t hub_ub = std::min<int64_t>(n, nnz / (DB + 1));
+  const int64_t S = (int64_t)DB + 1 + hub_ub;     // segments: degree classes + hub rows
+  const int64_t n_tiles = ceil_div64(n, kRadixTile);
+  const int64_t n_counts = n_tiles * kRadixBins;
+  const int64_t scan_max = std::max<int64_t>({n_counts, n + 1, S + 1});
+  const int64_t n_partials = ceil_div64(scan_max, kScanBlock) + 1;
+  if (ent_ub >= INT32_MAX || S + 1 >= INT32_MAX || n_counts > kScanMaxN)
+    return fail(AGCN_ERR_UNSUPPORTED, "graph too large for the int32 metadata format");
+
+  Layout L;
+  const size_t o_perm = L.take(4 * n);
+  const size_t o_rowptr_s = L.take(4 * (n + 1));
+  const size_t o_colidx_s = L.take(4 * nnz);
+  const size_t o_vals_s = L.take(4 * nnz);
+  const size_t o_meta = L.take(16 * ent_ub);
+  const size_t o_hub = L.take(4 * (hub_ub + 1));
+  // working buffers
+  const size_t o_deg = L.take(4 * n);
+  const size_t o_keys = L.take(4 * n);    // sorted degrees end here
+  const size_t o_keys2 = L.take(4 * n);
+  const size_t o_ids2 = L.take(4 * n);
+  const size_t o_counts = L.take(4 * n_counts);
+  const size_t o_partials = L.take(4 * n_partials);
+  const size_t o_pat = L.take(4 * (DB + 1));
+  const size_t o_cls = L.take(4 * (DB + 2));
+  const size_t o_nb = L.take(4 * S);
+  const size_t o_seg = L.take(4 * (S + 1));
+  const size_t o_err = L.take(64);
+  const size_t o_sum = L.take(sizeof(PlanSummary));
+
+  void* base = nullptr;
+  hipError_t he = hipMalloc(&base, L.off);
+  if (he != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(he == hipErrorOutOfMemory ? AGCN_ERR_OUT_OF_MEMORY : AGCN_ERR_HIP,
+                std::string("hipMalloc of ") + std::to_string(L.off) + " bytes failed: " +
+                    hipGetErrorString(he));
+  }
+  char* b = static_cast<char*>(base);
+  p->base = base;
+  p->bytes = L.off;
+  p->perm = reinterpret_cast<int32_t*>(b + o_perm);
+  p->rowptr_s = reinterpret_cast<int32_t*>(b + o_rowptr_s);
+  p->colidx_s = reinterpret_cast<int32_t*>(b + o_colidx_s);
+  p->vals_s = reinterpret_cast<float*>(b + o_vals_s);
+  p->meta = reinterpret_cast<int4*>(b + o_meta);
+  p->hub_chunk_off = reinterpret_cast<int32_t*>(b + o_hub);
+  int32_t* deg = reinterpret_cast<int32_t*>(b + o_deg);
+  int32_t* keys = reinterpret_cast<int32_t*>(b + o_keys);
+  int32_t* keys2 = reinterpret_cast<int32_t*>(b + o_keys2);
+  int32_t* ids2 = reinterpret_cast<int32_t*>(b + o_ids2);
+  int32_t* counts = reinterpret_cast<int32_t*>(b + o_counts);
+  int32_t* partials = reinterpret_cast<int32_t*>(b + o_partials);
+  int32_t* pat = reinterpret_cast<int32_t*>(b + o_pat);
+  int32_t* cls = reinterpret_cast<int32_t*>(b + o_cls);
+  int32_t* nb = reinterpret_cast<int32_t*>(b + o_nb);
+  int32_t* seg = reinterpret_cast<int32_t*>(b + o_seg);
+  uint32_t* err = reinterpret_cast<uint32_t*>(b + o_err);
+  PlanSummary* dsum = reinterpret_cast<PlanSummary*>(b + o_sum);
+
+  int rc;
+  k_init<<<1, 64, 0, st>>>(err, dsum);
+  if (n > 0) {
+    k_degree<<<grid_for(n, kThreads), kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err);
+    if ((rc = check_launch("k_degree"))) return rc;
+
+    // Stable LSD radix sort of row ids by degree. Degrees are at most nnz,
+    // so ceil(bits(nnz) / 8) passes order them completely. The pass schedule
+    // makes the last pass land in (keys, perm).
+    int bits = 0;
+    while (bits < 31 && (int64_t(1) << bits) <= nnz) ++bits;
+    const int passes = std::max(1, (bits + 7) / 8);
+    const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
+    const int32_t* kin = deg;
+    const int32_t* iin = nullptr;  // identity order on the first pass
+    for (int pass = 0; pass < passes; ++pass) {
+      const bool to_final = ((passes - 1 - pass) % 2) == 0;
+      int32_t* kout = to_final ? keys : keys2;
+      int32_t* iout = to_final ? p->perm : ids2;
+      const int shift = 8 * pass;
+      k_radix_hist<<<rgrid, kThreads, 0, st>>>((int32_t)n, kin, shift, counts, (int32_t)n_tiles, err);
+      if ((rc = check_launch("k_radix_hist"))) return rc;
+      if ((rc = scan_exclusive(counts, n_counts, counts, nullptr, partials, err, st))) return rc;
+      k_radix_scatter<<<rgrid, kThreads, 0, st>>>((int32_t)n, kin, iin, shift, counts,
+                                                  (int32_t)n_tiles, kout, iout, err);
+      if ((rc = check_launch("k_radix_scatter"))) return rc;
+      kin = kout;
+      iin = iout;
+    }
+  }
+  // rowptr_s = exclusive scan of the sorted degrees; rowptr_s[n] = nnz.
+  if ((rc = scan_exclusive(keys, n, p->rowptr_s, p->rowptr_s + n, partials, err, st))) return rc;
+  if (nnz > 0) {
+    k_relayout<<<grid_for(nnz, kRelayTile), kThreads, 0, st>>>(
+        (int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s, p->colidx_s,
+        p->vals_s, err);
+    if ((rc = check_launch("k_relayout"))) return rc;
+  }
+  k_patterns<<<grid_for((int64_t)DB + 1, kThreads), kThreads, 0, st>>>(W, Z, pat);
+  k_class_start<<<grid_for(n + 1, kThreads), kThreads, 0, st>>>((int32_t)n, keys, DB, cls, err);
+  k_seg_count<<<grid_for(S, kThreads), kThreads, 0, st>>>((int32_t)n, keys, cls, pat, DB, H,
+                                                         (int32_t)S, nb, err);
+  if ((rc = check_launch("partition counts"))) return rc;
+  if ((rc = scan_exclusive(nb, S, seg, seg + S, partials, err, st))) return rc;
+  const unsigned mgrid = (unsigned)std::min<int64_t>(grid_for(ent_ub, kThreads), 16384);
+  k_meta_fill<<<mgrid, kThreads, 0, st>>>(p->rowptr_s, keys, cls, pat, seg, (int32_t)S, DB, H,
+                                          p->meta, ent_ub, err);
+  k_hub_offsets<<<grid_for(hub_ub + 1, kThreads), kThreads, 0, st>>>(
+      (int32_t)n, keys, cls, seg, (int32_t)S, DB, (int32_t)hub_ub, p->hub_chunk_off, dsum, err);
+  if ((rc = check_launch("partition fill"))) return rc;
+
+  PlanSummary hs{};
+  he = hipMemcpyAsync(&hs, dsum, sizeof(hs), hipMemcpyDeviceToHost, st);
+  if (he != hipSuccess) return hip_fail(he, "hipMemcpyAsync(summary)");
+  he = hipStreamSynchronize(st);
+  if (he != hipSuccess) return hip_fail(he, "hipStreamSynchronize(plan)");
+  if (hs.err) {
+    std::string why;
+    if (hs.err & kErrRowptrStart) why += " rowptr[0] != 0;";
+    if (hs.err & kErrRowptrOrder) why += " rowptr decreases or leaves [0, nnz];";
+    if (hs.err & kErrRowptrEnd) why += " rowptr[n_rows] != nnz;";
+    if (hs.err & kErrColumn) why += " column index outside [0, n_cols);";
+    if (hs.err & kErrInternal) return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
+    return fail(AGCN_ERR_INVALID_INPUT, "invalid CSR:" + why);
+  }
+  p->n_entries = hs.n_entries;
+  p->hub_first_entry = hs.hub_first_entry;
+  p->n_hub_rows = hs.n_hub_rows;
+  p->hub_first_row = hs.hub_first_row;
+  p->max_deg = hs.max_deg;
+  return AGCN_OK;
+}
+
+}  // namespace agcn

@@ -1,0 +1,332 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle.
+
+* Plan (permutation, sorted CSR, metadata): bit-exact.
+* Y: |Y_gpu - Y_oracle| <= 1e-5 * S + 1e-7 per element, S = sum_e |a_e| |x|.
+* Determinism, row-permutation equivariance and the identity case: bit-exact.
+"""
+import numpy as np
+import pytest
+
+import graphgen
+import oracle
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2308_11825_amd as agcn  # noqa: E402
+
+DEV = "cuda:0"
+RTOL, ATOL = 1e-5, 1e-7
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _plan(g, **kw):
+    print(f"[plan] n={g.n_rows} nnz={g.nnz} {kw}", flush=True)
+    return agcn.Plan(_dev(g.rowptr), _dev(g.colidx), _dev(g.vals), n_cols=g.n_cols, **kw)
+
+
+def _params(plan):
+    return plan.stats.max_block_waves, plan.stats.max_wave_nzs, plan.stats.hub_chunk_nnz
+
+
+def assert_plan_matches_oracle(plan, g):
+    ex = plan.export()
+    W, Z, H = _params(plan)
+    ref = oracle.plan(g.rowptr, g.colidx, g.vals, W, Z, H)
+    assert np.array_equal(ex["perm"], ref["perm"]), "perm"
+    assert np.array_equal(ex["rowptr_s"], ref["rowptr_s"]), "rowptr_s"
+    assert np.array_equal(ex["colidx_s"], ref["colidx_s"]), "colidx_s"
+    assert np.array_equal(ex["vals_s"].view(np.uint32), ref["vals_s"].view(np.uint32)), "vals_s"
+    assert ex["meta"].shape == ref["meta"].shape, (ex["meta"].shape, ref["meta"].shape)
+    assert np.array_equal(ex["meta"], ref["meta"]), "meta"
+    s = plan.stats
+    d = np.diff(ref["rowptr_s"].astype(np.int64))
+    hub = d > s.deg_bound
+    assert s.n_hub_rows == int(hub.sum())
+    assert s.n_entries == len(ref["meta"])
+    assert s.max_deg == (int(d.max()) if d.size else 0)
+    return ex
+
+
+def assert_close(Yg, Y, S, what=""):
+    err = np.abs(Yg.astype(np.float64) - Y.astype(np.float64))
+    tol = RTOL * S + ATOL
+    bad = err > tol
+    if bad.any():
+        i = np.argwhere(bad)[0]
+        raise AssertionError(f"{what}: {int(bad.sum())} elements out of tolerance; first at {tuple(i)}: "
+                             f"gpu={Yg[tuple(i)]!r} oracle={Y[tuple(i)]!r} S={S[tuple(i)]!r}")
+
+
+def _mixed(seed, n, n_cols=None, hub_max=3000, dupes=False, empty_frac=0.05):
+    rng = np.random.default_rng(seed)
+    n_cols = n if n_cols is None else n_cols
+    deg = rng.choice([1, 2, 3, 4, 5, 7, 8, 9, 15, 16, 17, 31, 32, 33, 50, 64, 65, 100, 255, 256,
+                      257, 383, 384, 385, 511, 512, 513], size=n)
+    deg[rng.random(n) < empty_frac] = 0
+    hubs = rng.choice(n, size=max(2, n // 400), replace=False)
+    deg[hubs] = rng.integers(513, hub_max + 1, size=hubs.size)
+    if not dupes:
+        deg = np.minimum(deg, n_cols)
+    return graphgen.random_csr(n, n_cols, deg, seed=seed + 7, dupes=dupes)
+
+
+def _spmm_check(plan, g, F, X=None, seed=0):
+    if X is None:
+        X = np.random.default_rng(seed).standard_normal((g.n_cols, F)).astype(np.float32)
+    Y, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, n_cols=g.n_cols, want_scale=True)
+    Yg = plan.spmm(_dev(X)).cpu().numpy()
+    assert_close(Yg, Y, S, f"F={F}")
+    return Yg
+
+
+# ---------------------------------------------------------------------------
+# Plan parity
+# ---------------------------------------------------------------------------
+
+PARAM_SETS = [dict(), dict(max_block_waves=12, max_wave_nzs=32), dict(max_block_waves=8,
+              max_wave_nzs=64), dict(max_block_waves=16, max_wave_nzs=32, hub_chunk_nnz=1000),
+              dict(max_block_waves=2, max_wave_nzs=2), dict(max_block_waves=6, max_wave_nzs=3)]
+
+
+@pytest.mark.parametrize("kw", PARAM_SETS)
+@pytest.mark.parametrize("seed", [0, 1])
+def test_plan_bit_exact_random(kw, seed):
+    g = _mixed(seed, n=9000 + 1777 * seed, dupes=bool(seed))
+    plan = _plan(g, **kw)
+    assert_plan_matches_oracle(plan, g)
+    plan.destroy()
+
+
+@pytest.mark.parametrize("case", ["one_row", "all_empty", "deg_eq_bound", "deg_multiple_bound",
+                                  "deg_bound_plus_one", "single_hub", "no_nnz_cols", "rect"])
+def test_plan_and_spmm_edge_cases(case):
+    W, Z = 4, 8
+    DB = W * Z
+    n_cols = None
+    if case == "one_row":
+        deg = [5]
+    elif case == "all_empty":
+        deg = [0] * 37
+    elif case == "deg_eq_bound":
+        deg = [DB] * 11 + [1] * 3
+    elif case == "deg_multiple_bound":
+        deg = [3 * DB] * 3 + [2] * 5
+    elif case == "deg_bound_plus_one":
+        deg = [DB + 1] * 4 + [DB - 1] * 4
+    elif case == "single_hub":
+        deg = [0] * 3 + [1] * 100 + [5000]
+    elif case == "no_nnz_cols":
+        deg = [0, 0, 0]
+        n_cols = 0
+    else:  # rectangular: more columns than rows
+        deg = [3, 40, 0, 7, 33]
+        n_cols = 6000
+    n = len(deg)
+    nc = n_cols if n_cols is not None else max(n, max(deg) + 1 if deg else 1)
+    g = graphgen.random_csr(n, nc, np.array(deg), seed=3, dupes=True)
+    plan = _plan(g, max_block_waves=W, max_wave_nzs=Z)
+    assert_plan_matches_oracle(plan, g)
+    for F in (1, 4, 16, 17):
+        if nc == 0:
+            X = np.zeros((0, F), np.float32)
+            Yg = plan.spmm(_dev(X)).cpu().numpy()
+            assert np.all(Yg == 0)
+        else:
+            _spmm_check(plan, g, F)
+    plan.destroy()
+
+
+def test_empty_matrix():
+    g = graphgen.Graph("empty", 0, 0, np.zeros(1, np.int32), np.zeros(0, np.int32),
+                       np.zeros(0, np.float32))
+    plan = _plan(g)
+    assert plan.stats.n_entries == 0
+    Y = plan.spmm(torch.zeros((0, 8), device=DEV))
+    assert Y.shape == (0, 8)
+    plan.destroy()
+
+
+# ---------------------------------------------------------------------------
+# SpMM parity across F and layouts
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def mixed_plan():
+    g = _mixed(11, n=12000, hub_max=6000)
+    plan = _plan(g)
+    yield g, plan
+    plan.destroy()
+
+
+@pytest.mark.parametrize("F", [1, 3, 4, 8, 16, 17, 32, 64, 96, 128, 256, 257, 320, 512])
+def test_spmm_matches_oracle(mixed_plan, F):
+    g, plan = mixed_plan
+    _spmm_check(plan, g, F, seed=F)
+
+
+def test_spmm_unaligned_and_strided(mixed_plan):
+    g, plan = mixed_plan
+    rng = np.random.default_rng(5)
+    F = 64
+    X = rng.standard_normal((g.n_cols, F)).astype(np.float32)
+    Y, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, want_scale=True)
+    # X starting one float past an aligned address: the 32-bit path.
+    buf = torch.empty(g.n_cols * F + 1, dtype=torch.float32, device=DEV)
+    Xu = buf[1:].view(g.n_cols, F)
+    Xu.copy_(_dev(X))
+    assert Xu.data_ptr() % 16 != 0
+    assert_close(plan.spmm(Xu).cpu().numpy(), Y, S, "unaligned X")
+    # Row strides larger than F for both X and Y.
+    Xs = torch.zeros((g.n_cols, F + 12), dtype=torch.float32, device=DEV)
+    Xs[:, :F] = _dev(X)
+    Ys = torch.full((g.n_rows, F + 8), 7.0, dtype=torch.float32, device=DEV)
+    plan.spmm(Xs[:, :F], out=Ys[:, :F])
+    assert_close(Ys[:, :F].cpu().numpy(), Y, S, "strided")
+    assert torch.all(Ys[:, F:] == 7.0)      # padding untouched
+    # ldy not a multiple of 4 -> 32-bit path
+    Ys2 = torch.empty((g.n_rows, F + 1), dtype=torch.float32, device=DEV)
+    plan.spmm(_dev(X), out=Ys2[:, :F])
+    assert_close(Ys2[:, :F].cpu().numpy(), Y, S, "odd ldy")
+
+
+def test_spmm_deterministic_and_column_slicing(mixed_plan):
+    g, plan = mixed_plan
+    X = np.random.default_rng(9).standard_normal((g.n_cols, 128)).astype(np.float32)
+    Xd = _dev(X)
+    Y1 = plan.spmm(Xd).cpu().numpy()
+    Y2 = plan.spmm(Xd).cpu().numpy()
+    assert np.array_equal(Y1.view(np.uint32), Y2.view(np.uint32))
+    Y16 = plan.spmm(_dev(X[:, :16])).cpu().numpy()
+    _, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X[:, :16], want_scale=True)
+    assert_close(Y16, Y1[:, :16], 2 * S, "column slice")
+
+
+def test_identity_is_exact():
+    n, F = 5000, 36
+    g = graphgen.identity_csr(n)
+    plan = _plan(g)
+    X = np.random.default_rng(2).standard_normal((n, F)).astype(np.float32)
+    Yg = plan.spmm(_dev(X)).cpu().numpy()
+    assert np.array_equal(Yg.view(np.uint32), X.view(np.uint32))
+    plan.destroy()
+
+
+def test_row_permutation_equivariance_bit_exact():
+    g = _mixed(21, n=6000)
+    p = np.random.default_rng(22).permutation(g.n_rows)
+    gp = graphgen.permute_rows(g, p)
+    X = _dev(np.random.default_rng(23).standard_normal((g.n_cols, 48)).astype(np.float32))
+    pa, pb = _plan(g), _plan(gp)
+    Ya = pa.spmm(X).cpu().numpy()
+    Yb = pb.spmm(X).cpu().numpy()
+    assert np.array_equal(Yb.view(np.uint32), Ya[p].view(np.uint32))
+    pa.destroy()
+    pb.destroy()
+
+
+def test_ones_gives_row_sums(mixed_plan):
+    g, plan = mixed_plan
+    X = np.ones((g.n_cols, 4), np.float32)
+    Y, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, want_scale=True)
+    assert_close(plan.spmm(_dev(X)).cpu().numpy(), Y, S, "ones")
+
+
+def test_plan_reused_across_streams(mixed_plan):
+    g, plan = mixed_plan
+    X = _dev(np.random.default_rng(4).standard_normal((g.n_cols, 32)).astype(np.float32))
+    ref = plan.spmm(X).cpu().numpy()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        ws = torch.empty(max(1, plan.workspace_bytes(32) // 4), device=DEV)
+        Y = plan.spmm(X, ws=ws if plan.workspace_bytes(32) else None, stream=s)
+    s.synchronize()
+    assert np.array_equal(Y.cpu().numpy(), ref)
+
+
+# ---------------------------------------------------------------------------
+# Input validation on the device and host-side errors with a live plan
+# ---------------------------------------------------------------------------
+
+def test_invalid_csr_rejected_on_device():
+    g = graphgen.random_csr(100, 100, np.full(100, 3), seed=1)
+    bad = g.colidx.copy()
+    bad[57] = 100
+    with pytest.raises(agcn.AgcnError) as ei:
+        agcn.Plan(_dev(g.rowptr), _dev(bad), _dev(g.vals), n_cols=100)
+    assert ei.value.status == agcn.AGCN_ERR_INVALID_INPUT and "column" in str(ei.value)
+    rp = g.rowptr.copy()
+    rp[40] = rp[41] + 1
+    with pytest.raises(agcn.AgcnError) as ei:
+        agcn.Plan(_dev(rp), _dev(g.colidx), _dev(g.vals), n_cols=100)
+    assert ei.value.status == agcn.AGCN_ERR_INVALID_INPUT
+    rp = g.rowptr.copy()
+    rp[-1] -= 1
+    with pytest.raises(agcn.AgcnError) as ei:
+        agcn.Plan(_dev(rp), _dev(g.colidx), _dev(g.vals), n_cols=100)
+    assert ei.value.status == agcn.AGCN_ERR_INVALID_INPUT
+
+
+def test_spmm_argument_errors(mixed_plan):
+    g, plan = mixed_plan
+    X = torch.zeros((g.n_cols, 16), device=DEV)
+    Y = torch.zeros((g.n_rows, 16), device=DEV)
+    h = plan.handle
+    ws = plan.workspace(16)
+    wsp = ws.data_ptr() if ws is not None else None
+    for args, status in [((h, 0, X.data_ptr(), 16, Y.data_ptr(), 16, wsp), 1),
+                         ((h, 16, X.data_ptr(), 8, Y.data_ptr(), 16, wsp), 1),
+                         ((h, 16, X.data_ptr(), 16, X.data_ptr(), 16, wsp), 1),
+                         ((h, 16, X.data_ptr(), 16, None, 16, wsp), 1)]:
+        with pytest.raises(agcn.AgcnError) as ei:
+            agcn.agcn_spmm(*args)
+        assert ei.value.status == status
+    if plan.stats.n_hub_chunks:
+        with pytest.raises(agcn.AgcnError):
+            agcn.agcn_spmm(h, 16, X.data_ptr(), 16, Y.data_ptr(), 16, None)
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads (default parameters, the launch configuration the
+# benchmark times): plan bit-exact, Y on sampled rows.
+# ---------------------------------------------------------------------------
+
+_GRAPHS = {}
+
+
+def _workload(name):
+    if name not in _GRAPHS:
+        _GRAPHS.clear()
+        _GRAPHS[name] = graphgen.make(name, verbose=True)
+    return _GRAPHS[name]
+
+
+def _sample_rows(g, plan, k=3000, seed=0):
+    rng = np.random.default_rng(seed)
+    d = g.degrees
+    rows = [rng.choice(g.n_rows, size=min(k, g.n_rows), replace=False), [0, g.n_rows - 1]]
+    hub = np.nonzero(d > plan.stats.deg_bound)[0]
+    if hub.size:
+        rows.append(rng.choice(hub, size=min(300, hub.size), replace=False))
+    rows.append(np.argsort(d)[-20:])
+    return np.unique(np.concatenate(rows)).astype(np.int32)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", list(graphgen.CONFIGS))
+def test_workload_parity(name):
+    g = _workload(name)
+    plan = _plan(g)
+    assert_plan_matches_oracle(plan, g)
+    rows = _sample_rows(g, plan)
+    for F in graphgen.CONFIGS[name]["F"]:
+        X = graphgen.workload_features(name, g, F)
+        Yg = plan.spmm(_dev(X)).cpu().numpy()
+        Yr, Sr = oracle.spmm_rows(g.rowptr, g.colidx, g.vals, X, rows)
+        assert_close(Yg[rows], Yr, Sr, f"{name} F={F}")
+        assert np.all(np.isfinite(Yg))
+        print(f"[parity] {name} F={F} ok ({rows.size} rows checked)", flush=True)
+    plan.destroy()
