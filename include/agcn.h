@@ -150,9 +150,16 @@ int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* out);
 int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s,
                      int32_t* h_colidx_s, float* h_vals_s, int32_t* h_meta);
 
-/* Frees the plan's device memory (synchronises the device first). NULL is
- * ignored. No agcn_spmm on this plan may be in flight. */
+/* Releases the plan. Synchronises the plan's device first, so work still
+ * queued on any stream finishes before the memory is reused. The device
+ * block is kept in a per-device cache (one block per device) that the next
+ * agcn_plan_create on that device reuses when it fits; see
+ * agcn_release_cached_memory. NULL is ignored. */
 void agcn_plan_destroy(agcn_plan_t plan);
+
+/* Frees the device memory cached by destroyed plans, on every device. Plans
+ * that are still alive are not affected. */
+void agcn_release_cached_memory(void);
 
 /* Static text for a status code. */
 const char* agcn_status_string(int status);

@@ -17,7 +17,8 @@ import os
 __all__ = [
     "LIB_PATH", "AgcnError", "load_library", "agcn_default_params", "agcn_plan_create",
     "agcn_spmm_workspace_size", "agcn_spmm", "agcn_spmm_timed", "agcn_plan_info",
-    "agcn_plan_export", "agcn_plan_destroy", "agcn_status_string", "agcn_last_error", "Plan",
+    "agcn_plan_export", "agcn_plan_destroy", "agcn_status_string", "agcn_last_error",
+    "agcn_release_cached_memory", "Plan",
     "PlanParams", "PlanStats", "EXPORTED_SYMBOLS",
 ]
 
@@ -27,7 +28,7 @@ LIB_PATH = os.path.join(_HERE, "libagcn.so")
 EXPORTED_SYMBOLS = [
     "agcn_default_params", "agcn_plan_create", "agcn_spmm_workspace_size", "agcn_spmm",
     "agcn_spmm_timed", "agcn_plan_info", "agcn_plan_export", "agcn_plan_destroy",
-    "agcn_status_string", "agcn_last_error",
+    "agcn_status_string", "agcn_last_error", "agcn_release_cached_memory",
 ]
 
 AGCN_OK = 0
@@ -121,6 +122,8 @@ def load_library(path: str | None = None):
     lib.agcn_plan_export.restype = ctypes.c_int
     lib.agcn_plan_destroy.argtypes = [_vp]
     lib.agcn_plan_destroy.restype = None
+    lib.agcn_release_cached_memory.argtypes = []
+    lib.agcn_release_cached_memory.restype = None
     lib.agcn_status_string.argtypes = [ctypes.c_int]
     lib.agcn_status_string.restype = ctypes.c_char_p
     lib.agcn_last_error.argtypes = []
@@ -180,6 +183,10 @@ def agcn_plan_export(plan, h_perm=None, h_rowptr_s=None, h_colidx_s=None, h_vals
 
 def agcn_plan_destroy(plan):
     load_library().agcn_plan_destroy(plan)
+
+
+def agcn_release_cached_memory():
+    load_library().agcn_release_cached_memory()
 
 
 def agcn_status_string(status) -> str:

@@ -3,6 +3,8 @@
 #include <algorithm>
 #include <climits>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -45,6 +47,86 @@ int hip_fail(hipError_t e, const char* what) {
   return AGCN_ERR_HIP;
 }
 
+// --- plan memory cache ------------------------------------------------------
+// Creating and destroying plans of similar size (a new graph per batch, or the
+// same graph re-planned) would otherwise pay a hipMalloc and a hipFree --
+// which synchronises the device -- each time. A destroyed plan's block stays
+// cached, one block per device, and the next plan on that device reuses it
+// when it fits without wasting more than half of it.
+namespace {
+struct CachedBlock {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_cache_mu;
+std::map<int, CachedBlock> g_cache;
+
+int with_device(int device, int* prev) {
+  hipError_t e = hipGetDevice(prev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (*prev != device && (e = hipSetDevice(device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+  return AGCN_OK;
+}
+}  // namespace
+
+int device_alloc(int device, size_t bytes, void** out, size_t* got) {
+  {
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    auto it = g_cache.find(device);
+    if (it != g_cache.end() && it->second.ptr != nullptr && it->second.bytes >= bytes &&
+        it->second.bytes / 2 <= bytes) {
+      *out = it->second.ptr;
+      *got = it->second.bytes;
+      it->second = CachedBlock{};
+      return AGCN_OK;
+    }
+  }
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, bytes);
+  if (e == hipErrorOutOfMemory) {
+    // Give the cached block back to the device and try once more.
+    (void)hipGetLastError();
+    CachedBlock old;
+    {
+      std::lock_guard<std::mutex> lk(g_cache_mu);
+      old = g_cache[device];
+      g_cache[device] = CachedBlock{};
+    }
+    if (old.ptr) (void)hipFree(old.ptr);
+    e = hipMalloc(&p, bytes);
+  }
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(e == hipErrorOutOfMemory ? AGCN_ERR_OUT_OF_MEMORY : AGCN_ERR_HIP,
+                std::string("hipMalloc of ") + std::to_string(bytes) + " bytes failed: " +
+                    hipGetErrorString(e));
+  }
+  *out = p;
+  *got = bytes;
+  return AGCN_OK;
+}
+
+void device_release(int device, void* ptr, size_t bytes) {
+  if (ptr == nullptr) return;
+  int prev = 0;
+  if (with_device(device, &prev) != AGCN_OK) return;
+  // Kernels of this plan may still run on any stream: wait for all of them.
+  (void)hipDeviceSynchronize();
+  CachedBlock evict;
+  {
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    CachedBlock& slot = g_cache[device];
+    if (slot.ptr == nullptr || slot.bytes <= bytes) {
+      evict = slot;
+      slot = CachedBlock{ptr, bytes};
+    } else {
+      evict = CachedBlock{ptr, bytes};
+    }
+  }
+  if (evict.ptr) (void)hipFree(evict.ptr);
+  if (prev != device) (void)hipSetDevice(prev);
+}
+
 }  // namespace agcn
 
 using agcn::fail;
@@ -75,8 +157,23 @@ const char* agcn_last_error(void) { return agcn::g_last_error.c_str(); }
 
 static void plan_free(agcn_plan* p) {
   if (p == nullptr) return;
-  if (p->base != nullptr) (void)hipFree(p->base);
+  agcn::device_release(p->device, p->base, p->bytes);
   delete p;
+}
+
+void agcn_release_cached_memory(void) {
+  std::map<int, agcn::CachedBlock> blocks;
+  {
+    std::lock_guard<std::mutex> lk(agcn::g_cache_mu);
+    blocks.swap(agcn::g_cache);
+  }
+  for (auto& kv : blocks) {
+    if (kv.second.ptr == nullptr) continue;
+    int prev = 0;
+    if (agcn::with_device(kv.first, &prev) != AGCN_OK) continue;
+    (void)hipFree(kv.second.ptr);
+    if (prev != kv.first) (void)hipSetDevice(prev);
+  }
 }
 
 int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t nnz,

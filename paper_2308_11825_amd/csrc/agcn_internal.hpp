@@ -73,6 +73,12 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
 // Dynamic LDS bytes the SpMM kernel needs for a plan (worst case over F).
 size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz);
 
+// Plan memory. device_alloc may hand back the block a destroyed plan left in
+// the per-device cache (*got receives its size, >= bytes); device_release
+// synchronises the device and keeps the block cached (one per device).
+int device_alloc(int device, size_t bytes, void** out, size_t* got);
+void device_release(int device, void* ptr, size_t bytes);
+
 inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 }  // namespace agcn

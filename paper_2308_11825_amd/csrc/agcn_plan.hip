@@ -3,9 +3,12 @@
 //
 // Pipeline (all on one stream, one host synchronisation at the end):
 //   k_init          clear the error word and the summary
-//   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer
+//   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
+//                   maximum degree (integer atomic max)
 //   radix passes    stable LSD radix sort of row ids by degree, 8-bit digits:
-//                   k_radix_hist -> exclusive scan -> k_radix_scatter
+//                   k_radix_hist -> exclusive scan -> k_radix_scatter. A pass
+//                   whose digit is zero for every key (its shift is above the
+//                   maximum degree) reduces to a copy, decided on the device.
 //   scan            rowptr_s = exclusive scan of the sorted degrees
 //   k_relayout      sorted CSR copy (column indices checked against n_cols)
 //   k_patterns      Alg. 1 table for d = 0..deg_bound
@@ -34,6 +37,8 @@ constexpr int kScanBlock = kThreads * kScanItems;  // 4096 elements per workgrou
 constexpr int kScanTopThreads = 1024;
 constexpr int kScanTopItems = 64;                   // <= 65536 partial sums
 constexpr int64_t kScanMaxN = (int64_t)kScanBlock * kScanTopThreads * kScanTopItems;
+constexpr int kScanSingleItems = 32;  // one workgroup scans up to 32768 values
+constexpr int64_t kScanSingleMax = (int64_t)kScanTopThreads * kScanSingleItems;
 
 // Radix sort geometry: one wave owns kRadixTile consecutive rows.
 constexpr int kRadixBins = 256;
@@ -48,6 +53,18 @@ constexpr int kRelayTile = kThreads * kRelayItems;  // 2048
 constexpr uint32_t kErrInternal = 1u << 8;
 
 __device__ inline bool failed(const uint32_t* err) { return err[0] != 0; }
+
+// A radix pass (and its scan) is skipped when no key has bits at or above
+// `shift`; `gate` holds the maximum key. Pass 0 is never skipped.
+__device__ inline bool pass_skipped(const int32_t* gate, int shift) {
+  return gate != nullptr && shift > 0 && (gate[0] >> shift) == 0;
+}
+
+__device__ inline int32_t wave_max(int32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  return v;
+}
 
 __device__ inline int32_t wave_sum(int32_t v) {
 #pragma unroll
@@ -97,9 +114,10 @@ __device__ inline uint64_t match_digit(uint32_t digit, bool valid) {
 
 // ---------------------------------------------------------------------------
 
-__global__ void k_init(uint32_t* err, PlanSummary* sum) {
+__global__ void k_init(uint32_t* err, int32_t* dmax, PlanSummary* sum) {
   if (threadIdx.x == 0) {
     err[0] = 0;
+    dmax[0] = 0;
     sum->n_entries = 0;
     sum->hub_first_entry = 0;
     sum->n_hub_rows = 0;
@@ -113,31 +131,38 @@ __global__ void k_set(int32_t* p, int32_t v) {
   if (threadIdx.x == 0 && blockIdx.x == 0) p[0] = v;
 }
 
-// Step (1) of the degree sort, plus the row-pointer checks.
+// Step (1) of the degree sort, plus the row-pointer checks and the maximum
+// degree (each wave contributes its maximum with one integer atomic).
 __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
                                                      const int32_t* __restrict__ rowptr,
-                                                     int32_t* __restrict__ deg, uint32_t* err) {
+                                                     int32_t* __restrict__ deg, uint32_t* err,
+                                                     int32_t* dmax) {
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (i >= n) return;
-  const int32_t a = rowptr[i], b = rowptr[i + 1];
   uint32_t e = 0;
-  int32_t d = b - a;
-  if (a < 0 || b < a || (int64_t)b > nnz) {
-    e |= kErrRowptrOrder;
-    d = 0;
+  int32_t d = 0;
+  if (i < n) {
+    const int32_t a = rowptr[i], b = rowptr[i + 1];
+    d = b - a;
+    if (a < 0 || b < a || (int64_t)b > nnz) {
+      e |= kErrRowptrOrder;
+      d = 0;
+    }
+    if (i == 0 && a != 0) e |= kErrRowptrStart;
+    if (i == n - 1 && (int64_t)b != nnz) e |= kErrRowptrEnd;
+    deg[i] = d;
   }
-  if (i == 0 && a != 0) e |= kErrRowptrStart;
-  if (i == n - 1 && (int64_t)b != nnz) e |= kErrRowptrEnd;
-  deg[i] = d;
   if (e) atomicOr(err, e);
+  const int32_t m = wave_max(d);
+  if ((threadIdx.x & 63) == 0 && m > 0) atomicMax(dmax, m);
 }
 
 // Digit histogram of each wave tile; counts are stored digit-major so that one
 // exclusive scan yields every (digit, tile) start position.
 __global__ __launch_bounds__(kThreads) void k_radix_hist(int32_t n, const int32_t* __restrict__ keys,
                                                          int shift, int32_t* __restrict__ counts,
-                                                         int32_t n_tiles, const uint32_t* err) {
-  if (failed(err)) return;
+                                                         int32_t n_tiles, const uint32_t* err,
+                                                         const int32_t* dmax) {
+  if (failed(err) || pass_skipped(dmax, shift)) return;
   __shared__ int32_t cnt[kRadixWaves][kRadixBins];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t tile = (int64_t)blockIdx.x * kRadixWaves + wave;
@@ -160,12 +185,22 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(int32_t n, const int32_
 __global__ __launch_bounds__(kThreads) void k_radix_scatter(
     int32_t n, const int32_t* __restrict__ keys_in, const int32_t* __restrict__ ids_in, int shift,
     const int32_t* __restrict__ offsets, int32_t n_tiles, int32_t* __restrict__ keys_out,
-    int32_t* __restrict__ ids_out, const uint32_t* err) {
+    int32_t* __restrict__ ids_out, const uint32_t* err, const int32_t* dmax) {
   if (failed(err)) return;
   __shared__ int32_t start[kRadixWaves][kRadixBins];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t tile = (int64_t)blockIdx.x * kRadixWaves + wave;
   if (tile >= n_tiles) return;
+  if (pass_skipped(dmax, shift)) {  // every digit is zero: the stable order is unchanged
+    for (int j = 0; j < kRadixItems; ++j) {
+      const int64_t i = tile * kRadixTile + (int64_t)j * 64 + lane;
+      if (i < n) {
+        keys_out[i] = keys_in[i];
+        ids_out[i] = ids_in ? ids_in[i] : (int32_t)i;
+      }
+    }
+    return;
+  }
   for (int d = lane; d < kRadixBins; d += 64) start[wave][d] = offsets[(int64_t)d * n_tiles + tile];
   const int64_t base = tile * kRadixTile;
   for (int j = 0; j < kRadixItems; ++j) {
@@ -191,8 +226,9 @@ __global__ __launch_bounds__(kThreads) void k_radix_scatter(
 
 __global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t* __restrict__ in, int64_t n,
                                                           int32_t* __restrict__ partials,
-                                                          const uint32_t* err) {
-  if (failed(err)) return;
+                                                          const uint32_t* err, const int32_t* gate,
+                                                          int gate_shift) {
+  if (failed(err) || pass_skipped(gate, gate_shift)) return;
   __shared__ int32_t ws[kThreads / 64];
   const int64_t base = (int64_t)blockIdx.x * kScanBlock;
   int32_t s = 0;
@@ -213,8 +249,9 @@ __global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t* __restr
 
 __global__ __launch_bounds__(kScanTopThreads) void k_scan_top(int32_t* __restrict__ partials,
                                                               int32_t m, int32_t* total_out,
-                                                              const uint32_t* err) {
-  if (failed(err)) return;
+                                                              const uint32_t* err,
+                                                              const int32_t* gate, int gate_shift) {
+  if (failed(err) || pass_skipped(gate, gate_shift)) return;
   const int64_t b0 = (int64_t)threadIdx.x * kScanTopItems;
   int32_t s = 0;
   for (int k = 0; k < kScanTopItems; ++k)
@@ -234,8 +271,9 @@ __global__ __launch_bounds__(kScanTopThreads) void k_scan_top(int32_t* __restric
 __global__ __launch_bounds__(kThreads) void k_scan_down(const int32_t* __restrict__ in, int64_t n,
                                                         const int32_t* __restrict__ partials,
                                                         int32_t* __restrict__ out,
-                                                        const uint32_t* err) {
-  if (failed(err)) return;
+                                                        const uint32_t* err, const int32_t* gate,
+                                                        int gate_shift) {
+  if (failed(err) || pass_skipped(gate, gate_shift)) return;
   const int64_t i0 = (int64_t)blockIdx.x * kScanBlock + (int64_t)threadIdx.x * kScanItems;
   int32_t v[kScanItems];
   int32_t s = 0;
@@ -251,6 +289,29 @@ __global__ __launch_bounds__(kThreads) void k_scan_down(const int32_t* __restric
     if (i0 + k < n) out[i0 + k] = run;
     run += v[k];
   }
+}
+
+// One workgroup scans the whole array (n <= kScanSingleMax).
+__global__ __launch_bounds__(kScanTopThreads) void k_scan_single(
+    const int32_t* __restrict__ in, int32_t n, int32_t* __restrict__ out, int32_t* total_out,
+    const uint32_t* err, const int32_t* gate, int gate_shift) {
+  if (failed(err) || pass_skipped(gate, gate_shift)) return;
+  const int32_t i0 = threadIdx.x * kScanSingleItems;
+  int32_t v[kScanSingleItems];
+  int32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanSingleItems; ++k) {
+    v[k] = i0 + k < n ? in[i0 + k] : 0;
+    s += v[k];
+  }
+  int32_t total;
+  int32_t run = block_exclusive_scan<kScanTopThreads>(s, &total);
+#pragma unroll
+  for (int k = 0; k < kScanSingleItems; ++k) {
+    if (i0 + k < n) out[i0 + k] = run;
+    run += v[k];
+  }
+  if (threadIdx.x == 0 && total_out) total_out[0] = total;
 }
 
 // --- relayout (step (3) of the degree sort) ----------------------------------
@@ -434,17 +495,24 @@ int check_launch(const char* what) {
 }
 
 // out[i] = sum of in[0..i) for i < n, and *total = sum of all (may alias out + n).
+// In place (out == in) is allowed. With `gate`, the scan is skipped on the
+// device when the radix pass at `gate_shift` is.
 int scan_exclusive(const int32_t* in, int64_t n, int32_t* out, int32_t* total, int32_t* partials,
-                   const uint32_t* err, hipStream_t st) {
+                   const uint32_t* err, hipStream_t st, const int32_t* gate = nullptr,
+                   int gate_shift = 0) {
   if (n > kScanMaxN) return fail(AGCN_ERR_UNSUPPORTED, "scan longer than the supported maximum");
   if (n == 0) {
     if (total) k_set<<<1, 64, 0, st>>>(total, 0);
     return check_launch("k_set");
   }
+  if (n <= kScanSingleMax) {
+    k_scan_single<<<1, kScanTopThreads, 0, st>>>(in, (int32_t)n, out, total, err, gate, gate_shift);
+    return check_launch("k_scan_single");
+  }
   const unsigned nb = grid_for(n, kScanBlock);
-  k_scan_reduce<<<nb, kThreads, 0, st>>>(in, n, partials, err);
-  k_scan_top<<<1, kScanTopThreads, 0, st>>>(partials, (int32_t)nb, total, err);
-  k_scan_down<<<nb, kThreads, 0, st>>>(in, n, partials, out, err);
+  k_scan_reduce<<<nb, kThreads, 0, st>>>(in, n, partials, err, gate, gate_shift);
+  k_scan_top<<<1, kScanTopThreads, 0, st>>>(partials, (int32_t)nb, total, err, gate, gate_shift);
+  k_scan_down<<<nb, kThreads, 0, st>>>(in, n, partials, out, err, gate, gate_shift);
   return check_launch("scan");
 }
 
@@ -492,19 +560,16 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   const size_t o_nb = L.take(4 * S);
   const size_t o_seg = L.take(4 * (S + 1));
   const size_t o_err = L.take(64);
+  const size_t o_dmax = L.take(64);
   const size_t o_sum = L.take(sizeof(PlanSummary));
 
   void* base = nullptr;
-  hipError_t he = hipMalloc(&base, L.off);
-  if (he != hipSuccess) {
-    (void)hipGetLastError();
-    return fail(he == hipErrorOutOfMemory ? AGCN_ERR_OUT_OF_MEMORY : AGCN_ERR_HIP,
-                std::string("hipMalloc of ") + std::to_string(L.off) + " bytes failed: " +
-                    hipGetErrorString(he));
-  }
+  size_t got = 0;
+  int rc = device_alloc(p->device, L.off, &base, &got);
+  if (rc) return rc;
   char* b = static_cast<char*>(base);
   p->base = base;
-  p->bytes = L.off;
+  p->bytes = got;
   p->perm = reinterpret_cast<int32_t*>(b + o_perm);
   p->rowptr_s = reinterpret_cast<int32_t*>(b + o_rowptr_s);
   p->colidx_s = reinterpret_cast<int32_t*>(b + o_colidx_s);
@@ -522,12 +587,12 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   int32_t* nb = reinterpret_cast<int32_t*>(b + o_nb);
   int32_t* seg = reinterpret_cast<int32_t*>(b + o_seg);
   uint32_t* err = reinterpret_cast<uint32_t*>(b + o_err);
+  int32_t* dmax = reinterpret_cast<int32_t*>(b + o_dmax);
   PlanSummary* dsum = reinterpret_cast<PlanSummary*>(b + o_sum);
 
-  int rc;
-  k_init<<<1, 64, 0, st>>>(err, dsum);
+  k_init<<<1, 64, 0, st>>>(err, dmax, dsum);
   if (n > 0) {
-    k_degree<<<grid_for(n, kThreads), kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err);
+    k_degree<<<grid_for(n, kThreads), kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err, dmax);
     if ((rc = check_launch("k_degree"))) return rc;
 
     // Stable LSD radix sort of row ids by degree. Degrees are at most nnz,
@@ -544,11 +609,13 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
       int32_t* kout = to_final ? keys : keys2;
       int32_t* iout = to_final ? p->perm : ids2;
       const int shift = 8 * pass;
-      k_radix_hist<<<rgrid, kThreads, 0, st>>>((int32_t)n, kin, shift, counts, (int32_t)n_tiles, err);
+      k_radix_hist<<<rgrid, kThreads, 0, st>>>((int32_t)n, kin, shift, counts, (int32_t)n_tiles, err,
+                                               dmax);
       if ((rc = check_launch("k_radix_hist"))) return rc;
-      if ((rc = scan_exclusive(counts, n_counts, counts, nullptr, partials, err, st))) return rc;
+      if ((rc = scan_exclusive(counts, n_counts, counts, nullptr, partials, err, st, dmax, shift)))
+        return rc;
       k_radix_scatter<<<rgrid, kThreads, 0, st>>>((int32_t)n, kin, iin, shift, counts,
-                                                  (int32_t)n_tiles, kout, iout, err);
+                                                  (int32_t)n_tiles, kout, iout, err, dmax);
       if ((rc = check_launch("k_radix_scatter"))) return rc;
       kin = kout;
       iin = iout;
@@ -576,7 +643,7 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   if ((rc = check_launch("partition fill"))) return rc;
 
   PlanSummary hs{};
-  he = hipMemcpyAsync(&hs, dsum, sizeof(hs), hipMemcpyDeviceToHost, st);
+  hipError_t he = hipMemcpyAsync(&hs, dsum, sizeof(hs), hipMemcpyDeviceToHost, st);
   if (he != hipSuccess) return hip_fail(he, "hipMemcpyAsync(summary)");
   he = hipStreamSynchronize(st);
   if (he != hipSuccess) return hip_fail(he, "hipStreamSynchronize(plan)");

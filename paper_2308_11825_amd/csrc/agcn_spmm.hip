@@ -1,33 +1,39 @@
 // Execute: Y = A X over the block-level partition (Sec. III-C, III-D).
 //
-// k_spmm: one workgroup per metadata entry and per slice of <= 64 lanes of
-// the feature dimension (256 columns on the 128-bit path, 64 on the 32-bit
-// path; a slice exists only when F exceeds that width).
+// k_spmm: one workgroup per (metadata entry, column slice). A column slice is
+// 32 floats -- one 128-byte line of an X row -- unless F is smaller. The grid
+// is (entries, slices) and workgroups are dispatched x-fastest, so the whole
+// GPU sweeps the entries for slice 0, then slice 1, ...: at any moment the
+// L2 of every XCD holds only 128-byte pieces of X rows, which lets it keep
+// 8x more rows than whole 1-KiB rows (F = 256) and raises its hit rate on the
+// power-law column reuse. Slices narrower than a line would fetch unused
+// halves, so the slice never drops below 128 bytes.
 //   1. The entry {deg, loc, row, info} is read once (uniform, scalar load).
-//   2. The entry's column indices and values -- contiguous in the sorted
-//      CSR -- are staged into LDS with coalesced non-temporal loads. The LDS
-//      index is padded by one word per 32 so the vwarps of a wave, which read
-//      slices a fixed stride apart, hit different banks.
+//   2. Its column indices and values -- contiguous in the sorted CSR -- are
+//      staged into LDS with non-temporal loads, 4 pairs per thread in flight.
+//      The LDS index is padded by one word per 32 so the vwarps of a wave,
+//      which read slices a fixed stride apart, fall in different banks.
 //   3. Virtual warps (the paper's warps): a row of degree d is covered by
-//      ceil(d / warp_nzs) consecutive vwarps of warp_nzs nnz; each vwarp owns
-//      L lanes laid across the columns, one float4 per lane (the combined
-//      warp of Sec. III-D, built from 64-lane waves: several vwarps share a
-//      wave when F < 256). Workgroup lanes are mapped to (vwarp, lane) in
-//      `rounds` passes when W * L exceeds the workgroup size.
-//   4. Each lane gathers X rows (16-byte loads, 4 independent loads in
-//      flight per lane) and accumulates with fp32 FMA in nnz order.
-//   5. Rows held by a single vwarp store straight to Y (non-temporal). Rows
-//      split over several vwarps sum their partials from LDS in vwarp order;
-//      hub chunks (deg > deg_bound) sum all W slices in order and write one
-//      partial row to the workspace. No atomics: the result is bitwise
-//      reproducible and does not depend on the row's position in the order.
-// k_hub_reduce: one workgroup per hub row; G groups of lanes each add a
-//   contiguous run of the row's chunk partials, then a fixed pairwise tree
-//   combines the G group sums and the row is written once.
+//      ceil(d / warp_nzs) consecutive vwarps of warp_nzs nnz. Each vwarp owns
+//      L lanes laid across the slice's columns, one float4 per lane (the
+//      paper's combined warp, built from 64-lane waves: 64 / L vwarps share a
+//      wave). Workgroup threads map to (vwarp, lane) in `rounds` passes when
+//      W * L exceeds 1024.
+//   4. Each lane gathers X rows with 16-byte loads, 8 in flight, and
+//      accumulates with fp32 FMA in nnz order.
+//   5. Rows held by one vwarp store straight to Y (non-temporal). Rows split
+//      over several vwarps add their partials from LDS in vwarp order; hub
+//      chunks (deg > deg_bound) add all W slices in order and write one
+//      partial row to the workspace. No atomics: results are bitwise
+//      reproducible and independent of a row's position in the sorted order.
+// k_hub_reduce: one workgroup per (hub row, column slice); G lane groups each
+//   add a contiguous run of the row's chunk partials, then a fixed pairwise
+//   tree combines the G sums and the row is written once.
 //
 // Entries are launched heaviest first (metadata is in ascending degree order).
 #include <algorithm>
 #include <climits>
+#include <cstdlib>
 
 #include "agcn_internal.hpp"
 
@@ -47,7 +53,18 @@ struct VecOf<1> {
   using T = float;
 };
 
+constexpr int kDefaultSliceCols = 32;  // one 128-byte line per X row per pass
+constexpr int kStageUnroll = 4;
+constexpr int kGatherUnroll = 8;
+
 __device__ inline int pad_idx(int i) { return i + (i >> 5); }
+
+// Partial-sum slots: one padding slot per 8 float4 (per 32 floats) keeps
+// rows that are a multiple of 128 bytes apart in different banks.
+template <int VW>
+__device__ __host__ inline int part_idx(int i) {
+  return VW == 4 ? i + (i >> 3) : i + (i >> 5);
+}
 
 __device__ inline f4 fma_v(float a, f4 x, f4 acc) {
   f4 r;
@@ -59,49 +76,44 @@ __device__ inline f4 fma_v(float a, f4 x, f4 acc) {
 }
 __device__ inline float fma_v(float a, float x, float acc) { return __builtin_fmaf(a, x, acc); }
 
-template <typename V>
-__device__ inline V zero_v() {
-  return V(0.0f);
-}
-
 // acc = sum over j in [s0, s0 + len) of val[j] * X[col[j], lane], in order.
+// Groups of kGatherUnroll loads are issued before the first is consumed; the
+// tail of a group is predicated, so short slices still overlap their loads.
 template <int VW>
 __device__ inline typename VecOf<VW>::T gather_row(const int32_t* s_col, const float* s_val,
                                                    int s0, int len,
                                                    const typename VecOf<VW>::T* __restrict__ Xv,
                                                    int64_t ldv, int32_t lane_col) {
   using V = typename VecOf<VW>::T;
-  V acc = zero_v<V>();
-  int j = 0;
-  for (; j + 4 <= len; j += 4) {
-    const int p0 = pad_idx(s0 + j), p1 = pad_idx(s0 + j + 1);
-    const int p2 = pad_idx(s0 + j + 2), p3 = pad_idx(s0 + j + 3);
-    const int32_t c0 = s_col[p0], c1 = s_col[p1], c2 = s_col[p2], c3 = s_col[p3];
-    const float a0 = s_val[p0], a1 = s_val[p1], a2 = s_val[p2], a3 = s_val[p3];
-    const V x0 = Xv[(int64_t)c0 * ldv + lane_col];
-    const V x1 = Xv[(int64_t)c1 * ldv + lane_col];
-    const V x2 = Xv[(int64_t)c2 * ldv + lane_col];
-    const V x3 = Xv[(int64_t)c3 * ldv + lane_col];
-    acc = fma_v(a0, x0, acc);
-    acc = fma_v(a1, x1, acc);
-    acc = fma_v(a2, x2, acc);
-    acc = fma_v(a3, x3, acc);
-  }
-  for (; j < len; ++j) {
-    const int pj = pad_idx(s0 + j);
-    acc = fma_v(s_val[pj], Xv[(int64_t)s_col[pj] * ldv + lane_col], acc);
+  V acc = V(0.0f);
+  for (int j = 0; j < len; j += kGatherUnroll) {
+    V x[kGatherUnroll];
+    float a[kGatherUnroll];
+#pragma unroll
+    for (int u = 0; u < kGatherUnroll; ++u) {
+      if (j + u < len) {
+        const int p = pad_idx(s0 + j + u);
+        a[u] = s_val[p];
+        x[u] = Xv[(int64_t)s_col[p] * ldv + lane_col];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kGatherUnroll; ++u)
+      if (j + u < len) acc = fma_v(a[u], x[u], acc);
   }
   return acc;
 }
 
-template <int VW>
+// LT > 0: lanes per vwarp fixed at compile time; LT == 0: taken from L.
+template <int VW, int LT>
 __global__ __launch_bounds__(1024) void k_spmm(
     const int4* __restrict__ meta, int32_t n_entries, int32_t entry_base, int32_t hub_first_entry,
     int32_t deg_bound, int32_t W, const int32_t* __restrict__ colidx_s,
     const float* __restrict__ vals_s, const int32_t* __restrict__ perm, const float* __restrict__ X,
     int64_t ldx, float* __restrict__ Y, int64_t ldy, float* __restrict__ ws, int32_t F,
-    int32_t col_base, int32_t L, int32_t rounds, int32_t cap_pad) {
+    int32_t col_base, int32_t slice_cols, int32_t L_rt, int32_t rounds, int32_t cap_pad) {
   using V = typename VecOf<VW>::T;
+  const int L = LT > 0 ? LT : L_rt;
   extern __shared__ float smem[];
   int32_t* s_col = reinterpret_cast<int32_t*>(smem);
   float* s_val = smem + cap_pad;
@@ -109,16 +121,32 @@ __global__ __launch_bounds__(1024) void k_spmm(
 
   const int T = blockDim.x;
   const int32_t b = n_entries - 1 - (entry_base + (int32_t)blockIdx.x);
-  const int32_t col0 = col_base + (int32_t)blockIdx.y * kSliceLanes * VW;
+  const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
   const int4 m = meta[b];
   const int32_t deg = m.x, loc = m.y, row = m.z, info = m.w;
   const bool hub = deg > deg_bound;
   const int32_t rows = info & 0xFFFF;
   const int32_t n_e = hub ? info : rows * deg;
 
-  for (int i = threadIdx.x; i < n_e; i += T) {
-    s_col[pad_idx(i)] = __builtin_nontemporal_load(colidx_s + loc + i);
-    s_val[pad_idx(i)] = __builtin_nontemporal_load(vals_s + loc + i);
+  for (int i0 = 0; i0 < n_e; i0 += T * kStageUnroll) {
+    int32_t c[kStageUnroll];
+    float v[kStageUnroll];
+#pragma unroll
+    for (int u = 0; u < kStageUnroll; ++u) {
+      const int i = i0 + u * T + threadIdx.x;
+      if (i < n_e) {
+        c[u] = __builtin_nontemporal_load(colidx_s + loc + i);
+        v[u] = __builtin_nontemporal_load(vals_s + loc + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kStageUnroll; ++u) {
+      const int i = i0 + u * T + threadIdx.x;
+      if (i < n_e) {
+        s_col[pad_idx(i)] = c[u];
+        s_val[pad_idx(i)] = v[u];
+      }
+    }
   }
   __syncthreads();
 
@@ -140,7 +168,7 @@ __global__ __launch_bounds__(1024) void k_spmm(
           V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[row + rl] * ldy + col0);
           __builtin_nontemporal_store(acc, yr + l);
         } else {
-          s_part[v * L + l] = acc;
+          s_part[part_idx<VW>(v * L + l)] = acc;
         }
       }
     }
@@ -150,8 +178,8 @@ __global__ __launch_bounds__(1024) void k_spmm(
         const int vt = threadIdx.x + k * T;
         const int r = vt / L, l = vt - r * L;
         if (r < rows) {
-          V sum = s_part[(r * wpr) * L + l];
-          for (int q = 1; q < wpr; ++q) sum += s_part[(r * wpr + q) * L + l];
+          V sum = s_part[part_idx<VW>((r * wpr) * L + l)];
+          for (int q = 1; q < wpr; ++q) sum += s_part[part_idx<VW>((r * wpr + q) * L + l)];
           V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[row + r] * ldy + col0);
           __builtin_nontemporal_store(sum, yr + l);
         }
@@ -166,15 +194,15 @@ __global__ __launch_bounds__(1024) void k_spmm(
         const int s0 = v * sl;
         const int left = n_e - s0;
         const int len = left < 0 ? 0 : (left < sl ? left : sl);
-        s_part[v * L + l] = gather_row<VW>(s_col, s_val, s0, len, Xv, ldxv, l);
+        s_part[part_idx<VW>(v * L + l)] = gather_row<VW>(s_col, s_val, s0, len, Xv, ldxv, l);
       }
     }
     __syncthreads();
     for (int k = 0; k < rounds; ++k) {
       const int l = threadIdx.x + k * T;
       if (l < L) {
-        V sum = s_part[l];
-        for (int v = 1; v < W; ++v) sum += s_part[v * L + l];
+        V sum = s_part[part_idx<VW>(l)];
+        for (int v = 1; v < W; ++v) sum += s_part[part_idx<VW>(v * L + l)];
         V* wr = reinterpret_cast<V*>(ws + (int64_t)(b - hub_first_entry) * F + col0);
         wr[l] = sum;
       }
@@ -188,18 +216,19 @@ __global__ __launch_bounds__(1024) void k_hub_reduce(const int32_t* __restrict__
                                                      const int32_t* __restrict__ perm,
                                                      const float* __restrict__ ws, int32_t F,
                                                      float* __restrict__ Y, int64_t ldy,
-                                                     int32_t col_base, int32_t L, int32_t G) {
+                                                     int32_t col_base, int32_t slice_cols,
+                                                     int32_t L, int32_t G) {
   using V = typename VecOf<VW>::T;
   extern __shared__ float smem[];
   V* s_acc = reinterpret_cast<V*>(smem);  // [G][L]
   const int32_t h = blockIdx.x;
-  const int32_t col0 = col_base + (int32_t)blockIdx.y * kSliceLanes * VW;
+  const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
   const int32_t c0 = hub_chunk_off[h], c1 = hub_chunk_off[h + 1];
   const int32_t nc = c1 - c0;
   const int g = threadIdx.x / L, l = threadIdx.x - g * L;
   const int32_t q = (nc + G - 1) / G;
   if (g < G) {
-    V acc = zero_v<V>();
+    V acc = V(0.0f);
     const int32_t a = c0 + g * q;
     const int32_t e = a + q < c1 ? a + q : c1;
     for (int32_t c = a; c < e; ++c)
@@ -225,42 +254,95 @@ inline int stage_words(int32_t max_entry_nnz) {
   return round_up(last + (last >> 5) + 1, 4);
 }
 
+// Floats of partial-sum storage for W vwarps of L lanes.
+inline int part_floats(int VW, int W, int L) {
+  const int n = W * L;
+  return VW * (VW == 4 ? n + (n >> 3) + 1 : n + (n >> 5) + 1);
+}
+
+// Column-slice width: 32 floats (one 128-byte line) by default. The variable
+// AGCN_SLICE_COLS (a multiple of 4, 4..256) overrides it for measurements.
+int slice_cols_setting() {
+  static const int v = [] {
+    const char* s = std::getenv("AGCN_SLICE_COLS");
+    const int x = s ? std::atoi(s) : kDefaultSliceCols;
+    return (x >= 4 && x <= 256 && x % 4 == 0) ? x : kDefaultSliceCols;
+  }();
+  return v;
+}
+
+struct SpmmArgs {
+  const agcn_plan* p;
+  int32_t F;
+  const float* X;
+  int64_t ldx;
+  float* Y;
+  int64_t ldy;
+  float* ws;
+  hipStream_t st;
+};
+
+template <int VW, int LT>
+void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols) {
+  const agcn_plan* p = a.p;
+  const int cap_pad = stage_words(std::max(p->deg_bound, p->H));
+  const int want = p->W * L;
+  const int T = std::min(1024, round_up(want, 64));
+  const int rounds = (want + T - 1) / T;
+  const size_t lds = (size_t)2 * cap_pad * 4 + (size_t)part_floats(VW, p->W, L) * 4;
+  const int64_t max_grid = (int64_t)(UINT32_MAX / (uint32_t)T);
+  for (int64_t e0 = 0; e0 < p->n_entries; e0 += max_grid) {
+    const int64_t cnt = std::min<int64_t>(max_grid, p->n_entries - e0);
+    dim3 grid((unsigned)cnt, (unsigned)n_slices);
+    k_spmm<VW, LT><<<grid, T, lds, a.st>>>(p->meta, p->n_entries, (int32_t)e0, p->hub_first_entry,
+                                           p->deg_bound, p->W, p->colidx_s, p->vals_s, p->perm,
+                                           a.X, a.ldx, a.Y, a.ldy, a.ws, a.F, col_base, slice_cols,
+                                           L, rounds, cap_pad);
+  }
+}
+
 template <int VW>
-int launch_slices(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y,
-                  int64_t ldy, float* ws, hipStream_t st, bool hub_phase) {
-  const int slice_cols = kSliceLanes * VW;
-  const int n_full = F / slice_cols;
-  const int tail_cols = F - n_full * slice_cols;
-  const int cap = std::max(p->deg_bound, p->H);
-  const int cap_pad = stage_words(cap);
+void dispatch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols) {
+  switch (L) {
+    case 1: return launch_spmm<VW, 1>(a, L, n_slices, col_base, slice_cols);
+    case 2: return launch_spmm<VW, 2>(a, L, n_slices, col_base, slice_cols);
+    case 4: return launch_spmm<VW, 4>(a, L, n_slices, col_base, slice_cols);
+    case 8: return launch_spmm<VW, 8>(a, L, n_slices, col_base, slice_cols);
+    case 16: return launch_spmm<VW, 16>(a, L, n_slices, col_base, slice_cols);
+    case 32: return launch_spmm<VW, 32>(a, L, n_slices, col_base, slice_cols);
+    case 64: return launch_spmm<VW, 64>(a, L, n_slices, col_base, slice_cols);
+    default: return launch_spmm<VW, 0>(a, L, n_slices, col_base, slice_cols);
+  }
+}
+
+template <int VW>
+void launch_hub(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols) {
+  const agcn_plan* p = a.p;
+  int G = 1;
+  while (G < 16 && 2 * G * L <= 1024) G *= 2;
+  const int T = round_up(G * L, 64);
+  const size_t lds = (size_t)G * L * VW * 4;
+  dim3 grid((unsigned)p->n_hub_rows, (unsigned)n_slices);
+  k_hub_reduce<VW><<<grid, T, lds, a.st>>>(p->hub_chunk_off, p->hub_first_row, p->perm, a.ws, a.F,
+                                           a.Y, a.ldy, col_base, slice_cols, L, G);
+}
+
+// Runs one phase (aggregation or hub reduction) over all column slices: the
+// full slices in one launch, a narrower last slice in a second one.
+template <int VW>
+int run_phase(const SpmmArgs& a, bool hub_phase) {
+  const int sc_max = VW == 4 ? slice_cols_setting() : std::min(64, slice_cols_setting());
+  const int sc = std::min(a.F, sc_max);
+  const int n_full = a.F / sc;
+  const int tail = a.F - n_full * sc;
   for (int part = 0; part < 2; ++part) {
-    const int n_slices = part == 0 ? n_full : (tail_cols > 0 ? 1 : 0);
+    const int n_slices = part == 0 ? n_full : (tail > 0 ? 1 : 0);
     if (n_slices == 0) continue;
-    const int cols = part == 0 ? slice_cols : tail_cols;
+    const int cols = part == 0 ? sc : tail;
     const int L = cols / VW;
-    const int col_base = part == 0 ? 0 : n_full * slice_cols;
-    if (!hub_phase) {
-      const int want = p->W * L;
-      const int T = std::min(1024, round_up(want, 64));
-      const int rounds = (want + T - 1) / T;
-      const size_t lds = (size_t)2 * cap_pad * 4 + (size_t)p->W * L * VW * 4;
-      const int64_t max_grid = (int64_t)(UINT32_MAX / (uint32_t)T);
-      for (int64_t e0 = 0; e0 < p->n_entries; e0 += max_grid) {
-        const int64_t cnt = std::min<int64_t>(max_grid, p->n_entries - e0);
-        dim3 grid((unsigned)cnt, (unsigned)n_slices);
-        k_spmm<VW><<<grid, T, lds, st>>>(p->meta, p->n_entries, (int32_t)e0, p->hub_first_entry,
-                                         p->deg_bound, p->W, p->colidx_s, p->vals_s, p->perm, X,
-                                         ldx, Y, ldy, ws, F, col_base, L, rounds, cap_pad);
-      }
-    } else {
-      int G = 1;
-      while (G < 16 && 2 * G * L <= 1024) G *= 2;
-      const int T = round_up(G * L, 64);
-      const size_t lds = (size_t)G * L * VW * 4;
-      dim3 grid((unsigned)p->n_hub_rows, (unsigned)n_slices);
-      k_hub_reduce<VW><<<grid, T, lds, st>>>(p->hub_chunk_off, p->hub_first_row, p->perm, ws, F,
-                                             Y, ldy, col_base, L, G);
-    }
+    const int col_base = part == 0 ? 0 : n_full * sc;
+    if (hub_phase) launch_hub<VW>(a, L, n_slices, col_base, sc);
+    else dispatch_spmm<VW>(a, L, n_slices, col_base, sc);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, hub_phase ? "k_hub_reduce launch" : "k_spmm launch");
   }
@@ -272,7 +354,8 @@ inline bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 
 }  // namespace
 
 size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz) {
-  return (size_t)2 * stage_words(max_entry_nnz) * 4 + (size_t)W * kSliceLanes * 4 * 4;
+  // Worst case over slice widths: 64 lanes of float4 per vwarp.
+  return (size_t)2 * stage_words(max_entry_nnz) * 4 + (size_t)part_floats(4, W, 64) * 4;
 }
 
 int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,
@@ -280,18 +363,15 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
              hipEvent_t ev_end) {
   const bool vec = (F % 4 == 0) && (ldx % 4 == 0) && (ldy % 4 == 0) && aligned16(X) &&
                    aligned16(Y) && (ws == nullptr || aligned16(ws));
+  const SpmmArgs a{p, F, X, ldx, Y, ldy, ws, st};
   hipError_t e;
   if (ev_begin && (e = hipEventRecord(ev_begin, st)) != hipSuccess)
     return hip_fail(e, "hipEventRecord");
   int rc = AGCN_OK;
-  if (p->n_entries > 0)
-    rc = vec ? launch_slices<4>(p, F, X, ldx, Y, ldy, ws, st, false)
-             : launch_slices<1>(p, F, X, ldx, Y, ldy, ws, st, false);
+  if (p->n_entries > 0) rc = vec ? run_phase<4>(a, false) : run_phase<1>(a, false);
   if (rc) return rc;
   if (ev_mid && (e = hipEventRecord(ev_mid, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if (p->n_hub_rows > 0)
-    rc = vec ? launch_slices<4>(p, F, X, ldx, Y, ldy, ws, st, true)
-             : launch_slices<1>(p, F, X, ldx, Y, ldy, ws, st, true);
+  if (p->n_hub_rows > 0) rc = vec ? run_phase<4>(a, true) : run_phase<1>(a, true);
   if (rc) return rc;
   if (ev_end && (e = hipEventRecord(ev_end, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   return AGCN_OK;

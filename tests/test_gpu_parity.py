@@ -330,3 +330,21 @@ def test_workload_parity(name):
         assert np.all(np.isfinite(Yg))
         print(f"[parity] {name} F={F} ok ({rows.size} rows checked)", flush=True)
     plan.destroy()
+
+
+def test_plan_memory_reused_across_plans():
+    """A destroyed plan's device block is reused by the next plan; stale
+    contents must not leak into the new plan."""
+    g1 = _mixed(31, n=8000)
+    g2 = _mixed(32, n=7900)
+    p1 = _plan(g1)
+    assert_plan_matches_oracle(p1, g1)
+    p1.destroy()
+    p2 = _plan(g2)
+    assert_plan_matches_oracle(p2, g2)
+    _spmm_check(p2, g2, 64)
+    p2.destroy()
+    agcn.agcn_release_cached_memory()
+    p3 = _plan(g1)
+    assert_plan_matches_oracle(p3, g1)
+    p3.destroy()
