@@ -2,16 +2,18 @@
 // (Sec. III-C "Degree Sorting" and "Block-level Partition", Alg. 1 and Alg. 2).
 //
 // Pipeline (all on one stream, one host synchronisation at the end):
-//   k_init          clear the error word and the summary
+//   k_init          clear the error word, the maximum degree and the summary
 //   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
-//                   maximum degree (integer atomic max)
+//                   per-workgroup maximum degree
+//   k_dmax          maximum degree (one workgroup); copied to pinned host
+//                   memory while radix pass 0 runs, so the host launches only
+//                   the passes the maximum degree needs
 //   radix passes    stable LSD radix sort of row ids by degree, 8-bit digits:
-//                   k_radix_hist -> exclusive scan -> k_radix_scatter. A pass
-//                   whose digit is zero for every key (its shift is above the
-//                   maximum degree) reduces to a copy, decided on the device.
+//                   k_radix_hist -> exclusive scan -> k_radix_scatter. Buffers
+//                   alternate so that the last pass writes the final
+//                   (keys, perm) pair.
 //   scan            rowptr_s = exclusive scan of the sorted degrees
 //   k_relayout      sorted CSR copy (column indices checked against n_cols)
-//   k_patterns      Alg. 1 table for d = 0..deg_bound
 //   k_class_start   first sorted row of each degree class 0..deg_bound+1
 //   k_seg_count     blocks per degree class / chunks per hub row
 //   scan            entry offsets of every segment
@@ -23,6 +25,7 @@
 // round with ballots; every count is an integer, so the result is exact.
 #include <algorithm>
 #include <climits>
+#include <map>
 
 #include "agcn_internal.hpp"
 
@@ -37,13 +40,15 @@ constexpr int kScanBlock = kThreads * kScanItems;  // 4096 elements per workgrou
 constexpr int kScanTopThreads = 1024;
 constexpr int kScanTopItems = 64;                   // <= 65536 partial sums
 constexpr int64_t kScanMaxN = (int64_t)kScanBlock * kScanTopThreads * kScanTopItems;
-constexpr int kScanSingleItems = 32;  // one workgroup scans up to 32768 values
-constexpr int64_t kScanSingleMax = (int64_t)kScanTopThreads * kScanSingleItems;
+constexpr int kScanChunkItems = 8;                  // single-workgroup scan: 8192 per chunk
+constexpr int kScanChunk = kScanTopThreads * kScanChunkItems;
+constexpr int64_t kScanSingleMax = 2 * kScanChunk;  // up to two chunks in one workgroup
+constexpr int64_t kScanTwoPassMaxBlocks = 1024;     // reduce + down, partial prefix inline
 
 // Radix sort geometry: one wave owns kRadixTile consecutive rows.
 constexpr int kRadixBins = 256;
-constexpr int kRadixItems = 32;
-constexpr int kRadixTile = 64 * kRadixItems;  // 2048
+constexpr int kRadixItems = 8;
+constexpr int kRadixTile = 64 * kRadixItems;  // 512
 constexpr int kRadixWaves = kThreads / 64;    // 4 tiles per workgroup
 
 // Relayout tile (sorted nnz positions per workgroup).
@@ -54,21 +59,26 @@ constexpr uint32_t kErrInternal = 1u << 8;
 
 __device__ inline bool failed(const uint32_t* err) { return err[0] != 0; }
 
-// A radix pass (and its scan) is skipped when no key has bits at or above
-// `shift`; `gate` holds the maximum key. Pass 0 is never skipped.
-__device__ inline bool pass_skipped(const int32_t* gate, int shift) {
-  return gate != nullptr && shift > 0 && (gate[0] >> shift) == 0;
+// Radix passes the maximum degree needs (at least one).
+__device__ inline int passes_needed(int32_t dmax) {
+  const int bits = dmax > 0 ? 32 - __clz(dmax) : 0;
+  return bits > 8 ? (bits + 7) / 8 : 1;
 }
 
-__device__ inline int32_t wave_max(int32_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
-  return v;
+// A gated scan belongs to radix pass `pass` and is skipped with it.
+__device__ inline bool gate_closed(const int32_t* dmax, int pass) {
+  return dmax != nullptr && pass >= passes_needed(dmax[0]);
 }
 
 __device__ inline int32_t wave_sum(int32_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ inline int32_t wave_max(int32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
   return v;
 }
 
@@ -83,6 +93,7 @@ __device__ inline int32_t wave_inclusive_scan(int32_t v, int lane) {
 }
 
 // Exclusive scan across a workgroup of T threads; *total receives the sum.
+// Ends with a barrier, so it may be called again right away.
 template <int T>
 __device__ inline int32_t block_exclusive_scan(int32_t v, int32_t* total) {
   __shared__ int32_t wsum[T / 64];
@@ -97,7 +108,9 @@ __device__ inline int32_t block_exclusive_scan(int32_t v, int32_t* total) {
   }
   __syncthreads();
   *total = wsum[T / 64 - 1];
-  return (w > 0 ? wsum[w - 1] : 0) + inc - v;
+  const int32_t r = (w > 0 ? wsum[w - 1] : 0) + inc - v;
+  __syncthreads();
+  return r;
 }
 
 // Lanes of the wave holding the same 8-bit digit (among valid lanes).
@@ -110,6 +123,16 @@ __device__ inline uint64_t match_digit(uint32_t digit, bool valid) {
     m &= bit ? bal : ~bal;
   }
   return m;
+}
+
+// Alg. 1 for one degree: the smallest factor f of W with f * Z >= d gives
+// block_rows = W / f and warp_nzs = ceil(d / f); returned as
+// warp_nzs << 16 | block_rows. Degree 0 gets W rows and warp_nzs 0.
+__device__ inline int32_t pattern_of(int32_t d, int32_t W, int32_t Z) {
+  if (d == 0) return W;
+  for (int32_t f = 1; f <= W; ++f)
+    if (W % f == 0 && f * Z >= d) return (((d + f - 1) / f) << 16) | (W / f);
+  return 0;  // d > W * Z: not a degree class
 }
 
 // ---------------------------------------------------------------------------
@@ -132,11 +155,12 @@ __global__ void k_set(int32_t* p, int32_t v) {
 }
 
 // Step (1) of the degree sort, plus the row-pointer checks and the maximum
-// degree (each wave contributes its maximum with one integer atomic).
+// degree of each workgroup.
 __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
                                                      const int32_t* __restrict__ rowptr,
                                                      int32_t* __restrict__ deg, uint32_t* err,
-                                                     int32_t* dmax) {
+                                                     int32_t* __restrict__ block_max) {
+  __shared__ int32_t s_max[kThreads / 64];
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   uint32_t e = 0;
   int32_t d = 0;
@@ -153,26 +177,67 @@ __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
   }
   if (e) atomicOr(err, e);
   const int32_t m = wave_max(d);
-  if ((threadIdx.x & 63) == 0 && m > 0) atomicMax(dmax, m);
+  if ((threadIdx.x & 63) == 0) s_max[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t t = 0;
+    for (int w = 0; w < kThreads / 64; ++w) t = max(t, s_max[w]);
+    block_max[blockIdx.x] = t;
+  }
 }
+
+// Maximum of the per-workgroup maxima (one workgroup of kScanTopThreads).
+__global__ __launch_bounds__(kScanTopThreads) void k_dmax(const int32_t* __restrict__ block_max,
+                                                          int32_t nb, int32_t* dmax) {
+  __shared__ int32_t s_max[kScanTopThreads / 64];
+  int32_t m = 0;
+  for (int32_t i = threadIdx.x; i < nb; i += kScanTopThreads) m = max(m, block_max[i]);
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) s_max[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t t = 0;
+    for (int w = 0; w < kScanTopThreads / 64; ++w) t = max(t, s_max[w]);
+    dmax[0] = t;
+  }
+}
+
+// Buffers of the radix passes: pass p (if it runs) writes slot (need - 1 - p) % 2
+// of (keys, ids), slot 0 being the final (keys, perm); pass 0 reads the
+// degrees in row order.
+struct RadixBufs {
+  const int32_t* deg;
+  int32_t* keys[2];
+  int32_t* ids[2];
+};
 
 // Digit histogram of each wave tile; counts are stored digit-major so that one
 // exclusive scan yields every (digit, tile) start position.
-__global__ __launch_bounds__(kThreads) void k_radix_hist(int32_t n, const int32_t* __restrict__ keys,
-                                                         int shift, int32_t* __restrict__ counts,
+__global__ __launch_bounds__(kThreads) void k_radix_hist(int32_t n, RadixBufs bufs, int pass,
+                                                         int32_t* __restrict__ counts,
                                                          int32_t n_tiles, const uint32_t* err,
                                                          const int32_t* dmax) {
-  if (failed(err) || pass_skipped(dmax, shift)) return;
+  if (failed(err)) return;
+  const int need = passes_needed(dmax[0]);
+  if (pass >= need) return;
+  const int32_t* keys = pass == 0 ? bufs.deg : bufs.keys[(need - pass) & 1];
+  const int shift = 8 * pass;
   __shared__ int32_t cnt[kRadixWaves][kRadixBins];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t tile = (int64_t)blockIdx.x * kRadixWaves + wave;
   if (tile >= n_tiles) return;  // uniform per wave; no workgroup barrier below
   for (int d = lane; d < kRadixBins; d += 64) cnt[wave][d] = 0;
   const int64_t base = tile * kRadixTile;
+  int32_t k[kRadixItems];
+#pragma unroll
   for (int j = 0; j < kRadixItems; ++j) {
     const int64_t i = base + (int64_t)j * 64 + lane;
-    const bool valid = i < n;
-    const uint32_t digit = valid ? (((uint32_t)keys[i]) >> shift) & 0xFFu : 0u;
+    k[j] = i < n ? keys[i] : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < kRadixItems; ++j) {
+    const bool valid = base + (int64_t)j * 64 + lane < n;
+    const uint32_t digit = (((uint32_t)k[j]) >> shift) & 0xFFu;
     const uint64_t peers = match_digit(digit, valid);
     // The lowest lane of each digit group adds the group's size (one writer per digit).
     if (valid && __popcll(peers & __lanemask_lt()) == 0) cnt[wave][digit] += __popcll(peers);
@@ -182,53 +247,57 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(int32_t n, const int32_
 
 // Stable scatter: a row's new position is its (digit, tile) start plus the
 // number of earlier rows of the tile with the same digit.
-__global__ __launch_bounds__(kThreads) void k_radix_scatter(
-    int32_t n, const int32_t* __restrict__ keys_in, const int32_t* __restrict__ ids_in, int shift,
-    const int32_t* __restrict__ offsets, int32_t n_tiles, int32_t* __restrict__ keys_out,
-    int32_t* __restrict__ ids_out, const uint32_t* err, const int32_t* dmax) {
+__global__ __launch_bounds__(kThreads) void k_radix_scatter(int32_t n, RadixBufs bufs, int pass,
+                                                            const int32_t* __restrict__ offsets,
+                                                            int32_t n_tiles, const uint32_t* err,
+                                                            const int32_t* dmax) {
   if (failed(err)) return;
+  const int need = passes_needed(dmax[0]);
+  if (pass >= need) return;
+  const int out = (need - 1 - pass) & 1;
+  const int32_t* keys_in = pass == 0 ? bufs.deg : bufs.keys[out ^ 1];
+  const int32_t* ids_in = pass == 0 ? nullptr : bufs.ids[out ^ 1];
+  int32_t* __restrict__ keys_out = bufs.keys[out];
+  int32_t* __restrict__ ids_out = bufs.ids[out];
+  const int shift = 8 * pass;
   __shared__ int32_t start[kRadixWaves][kRadixBins];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t tile = (int64_t)blockIdx.x * kRadixWaves + wave;
   if (tile >= n_tiles) return;
-  if (pass_skipped(dmax, shift)) {  // every digit is zero: the stable order is unchanged
-    for (int j = 0; j < kRadixItems; ++j) {
-      const int64_t i = tile * kRadixTile + (int64_t)j * 64 + lane;
-      if (i < n) {
-        keys_out[i] = keys_in[i];
-        ids_out[i] = ids_in ? ids_in[i] : (int32_t)i;
-      }
-    }
-    return;
-  }
   for (int d = lane; d < kRadixBins; d += 64) start[wave][d] = offsets[(int64_t)d * n_tiles + tile];
   const int64_t base = tile * kRadixTile;
+  int32_t k[kRadixItems], id[kRadixItems];
+#pragma unroll
   for (int j = 0; j < kRadixItems; ++j) {
     const int64_t i = base + (int64_t)j * 64 + lane;
-    const bool valid = i < n;
-    const int32_t key = valid ? keys_in[i] : 0;
-    const int32_t id = valid ? (ids_in ? ids_in[i] : (int32_t)i) : 0;
-    const uint32_t digit = (((uint32_t)key) >> shift) & 0xFFu;
+    k[j] = i < n ? keys_in[i] : 0;
+    id[j] = i < n ? (ids_in ? ids_in[i] : (int32_t)i) : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < kRadixItems; ++j) {
+    const bool valid = base + (int64_t)j * 64 + lane < n;
+    const uint32_t digit = (((uint32_t)k[j]) >> shift) & 0xFFu;
     const uint64_t peers = match_digit(digit, valid);
     const int32_t rank = (int32_t)__popcll(peers & __lanemask_lt());
     // All lanes read the digit's start before its single writer advances it
     // (LDS operations of one wave complete in program order).
     const int32_t pos = start[wave][digit] + rank;
     if (valid) {
-      keys_out[pos] = key;
-      ids_out[pos] = id;
+      keys_out[pos] = k[j];
+      ids_out[pos] = id[j];
     }
     if (valid && rank == 0) start[wave][digit] += __popcll(peers);
   }
 }
 
-// --- exclusive scan of int32 (three phases) ---------------------------------
+// --- exclusive scan of int32 -------------------------------------------------
 
+// Phase 1: one total per block of kScanBlock values.
 __global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t* __restrict__ in, int64_t n,
                                                           int32_t* __restrict__ partials,
                                                           const uint32_t* err, const int32_t* gate,
-                                                          int gate_shift) {
-  if (failed(err) || pass_skipped(gate, gate_shift)) return;
+                                                          int gate_pass) {
+  if (failed(err) || gate_closed(gate, gate_pass)) return;
   __shared__ int32_t ws[kThreads / 64];
   const int64_t base = (int64_t)blockIdx.x * kScanBlock;
   int32_t s = 0;
@@ -247,11 +316,12 @@ __global__ __launch_bounds__(kThreads) void k_scan_reduce(const int32_t* __restr
   }
 }
 
+// Phase 2 (many blocks only): exclusive scan of the block totals in place.
 __global__ __launch_bounds__(kScanTopThreads) void k_scan_top(int32_t* __restrict__ partials,
                                                               int32_t m, int32_t* total_out,
                                                               const uint32_t* err,
-                                                              const int32_t* gate, int gate_shift) {
-  if (failed(err) || pass_skipped(gate, gate_shift)) return;
+                                                              const int32_t* gate, int gate_pass) {
+  if (failed(err) || gate_closed(gate, gate_pass)) return;
   const int64_t b0 = (int64_t)threadIdx.x * kScanTopItems;
   int32_t s = 0;
   for (int k = 0; k < kScanTopItems; ++k)
@@ -268,67 +338,136 @@ __global__ __launch_bounds__(kScanTopThreads) void k_scan_top(int32_t* __restric
   if (threadIdx.x == 0 && total_out) total_out[0] = total;
 }
 
+// Last phase. With `inline_prefix` the block adds up the totals of the blocks
+// before it itself (partials hold raw totals; few blocks), and the last block
+// writes the grand total; otherwise partials already hold exclusive offsets.
 __global__ __launch_bounds__(kThreads) void k_scan_down(const int32_t* __restrict__ in, int64_t n,
                                                         const int32_t* __restrict__ partials,
-                                                        int32_t* __restrict__ out,
-                                                        const uint32_t* err, const int32_t* gate,
-                                                        int gate_shift) {
-  if (failed(err) || pass_skipped(gate, gate_shift)) return;
-  const int64_t i0 = (int64_t)blockIdx.x * kScanBlock + (int64_t)threadIdx.x * kScanItems;
+                                                        int32_t* __restrict__ out, int32_t* total_out,
+                                                        int inline_prefix, const uint32_t* err,
+                                                        const int32_t* gate, int gate_pass) {
+  if (failed(err) || gate_closed(gate, gate_pass)) return;
+  __shared__ int32_t s_base;
+  if (inline_prefix) {
+    if (threadIdx.x < 64) {
+      int32_t s = 0;
+      for (int b = threadIdx.x; b < (int)blockIdx.x; b += 64) s += partials[b];
+      s = wave_sum(s);
+      if (threadIdx.x == 0) s_base = s;
+    }
+  } else if (threadIdx.x == 0) {
+    s_base = partials[blockIdx.x];
+  }
+  // Coalesced load into registers, thread-contiguous ownership through LDS.
+  __shared__ int32_t tile[kScanBlock + kScanBlock / 32];
+  const int64_t base = (int64_t)blockIdx.x * kScanBlock;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const int j = k * kThreads + threadIdx.x;
+    const int64_t i = base + j;
+    tile[j + (j >> 5)] = i < n ? in[i] : 0;
+  }
+  __syncthreads();
   int32_t v[kScanItems];
   int32_t s = 0;
 #pragma unroll
   for (int k = 0; k < kScanItems; ++k) {
-    v[k] = (i0 + k < n) ? in[i0 + k] : 0;
+    const int j = threadIdx.x * kScanItems + k;
+    v[k] = tile[j + (j >> 5)];
     s += v[k];
   }
   int32_t total;
-  int32_t run = block_exclusive_scan<kThreads>(s, &total) + partials[blockIdx.x];
+  int32_t run = block_exclusive_scan<kThreads>(s, &total) + s_base;
 #pragma unroll
   for (int k = 0; k < kScanItems; ++k) {
-    if (i0 + k < n) out[i0 + k] = run;
+    const int j = threadIdx.x * kScanItems + k;
+    tile[j + (j >> 5)] = run;
     run += v[k];
   }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    const int j = k * kThreads + threadIdx.x;
+    const int64_t i = base + j;
+    if (i < n) out[i] = tile[j + (j >> 5)];
+  }
+  if (inline_prefix && total_out && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0)
+    total_out[0] = s_base + total;
 }
 
-// One workgroup scans the whole array (n <= kScanSingleMax).
+// One workgroup scans the whole array in chunks (n <= kScanSingleMax).
 __global__ __launch_bounds__(kScanTopThreads) void k_scan_single(
     const int32_t* __restrict__ in, int32_t n, int32_t* __restrict__ out, int32_t* total_out,
-    const uint32_t* err, const int32_t* gate, int gate_shift) {
-  if (failed(err) || pass_skipped(gate, gate_shift)) return;
-  const int32_t i0 = threadIdx.x * kScanSingleItems;
-  int32_t v[kScanSingleItems];
-  int32_t s = 0;
+    const uint32_t* err, const int32_t* gate, int gate_pass) {
+  if (failed(err) || gate_closed(gate, gate_pass)) return;
+  __shared__ int32_t tile[kScanChunk + kScanChunk / 32];
+  int32_t carry = 0;
+  for (int32_t c0 = 0; c0 < n; c0 += kScanChunk) {
 #pragma unroll
-  for (int k = 0; k < kScanSingleItems; ++k) {
-    v[k] = i0 + k < n ? in[i0 + k] : 0;
-    s += v[k];
-  }
-  int32_t total;
-  int32_t run = block_exclusive_scan<kScanTopThreads>(s, &total);
+    for (int k = 0; k < kScanChunkItems; ++k) {
+      const int j = k * kScanTopThreads + threadIdx.x;
+      tile[j + (j >> 5)] = c0 + j < n ? in[c0 + j] : 0;
+    }
+    __syncthreads();
+    int32_t v[kScanChunkItems];
+    int32_t s = 0;
 #pragma unroll
-  for (int k = 0; k < kScanSingleItems; ++k) {
-    if (i0 + k < n) out[i0 + k] = run;
-    run += v[k];
+    for (int k = 0; k < kScanChunkItems; ++k) {
+      const int j = threadIdx.x * kScanChunkItems + k;
+      v[k] = tile[j + (j >> 5)];
+      s += v[k];
+    }
+    int32_t total;
+    int32_t run = block_exclusive_scan<kScanTopThreads>(s, &total) + carry;
+#pragma unroll
+    for (int k = 0; k < kScanChunkItems; ++k) {
+      const int j = threadIdx.x * kScanChunkItems + k;
+      tile[j + (j >> 5)] = run;
+      run += v[k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kScanChunkItems; ++k) {
+      const int j = k * kScanTopThreads + threadIdx.x;
+      if (c0 + j < n) out[c0 + j] = tile[j + (j >> 5)];
+    }
+    carry += total;
+    __syncthreads();
   }
-  if (threadIdx.x == 0 && total_out) total_out[0] = total;
+  if (threadIdx.x == 0 && total_out) total_out[0] = carry;
 }
 
 // --- relayout (step (3) of the degree sort) ----------------------------------
 
-// Largest r in [0, n) with rowptr_s[r] <= e (the row holding sorted nnz e).
-__device__ inline int32_t row_of(const int32_t* rowptr_s, int32_t n, int64_t e) {
-  int32_t a = 0, b = n - 1;
-  while (a < b) {
-    const int32_t mid = (int32_t)(((int64_t)a + b + 1) >> 1);
-    if (rowptr_s[mid] <= e) a = mid; else b = mid - 1;
+// Largest r in [0, n) with rowptr_s[r] <= e (the row holding sorted nnz e),
+// found by one whole wave: each step probes 64 evenly spaced rows and keeps
+// the interval between the last probe <= e and the next, so a search over
+// n rows takes about log64(n) dependent loads. Call with all 64 lanes.
+__device__ inline int32_t wave_row_of(const int32_t* rowptr_s, int32_t n, int64_t e, int lane) {
+  int32_t a = 0, b = n - 1;  // invariant: rowptr_s[a] <= e, answer in [a, b]
+  while (b > a) {
+    const int64_t span = (int64_t)b - a;
+    const int32_t probe = a + (int32_t)((span * (lane + 1) + 63) / 64);  // in (a, b]
+    const bool le = rowptr_s[probe] <= e;
+    const uint64_t mask = __ballot(le);
+    // Probes increase with the lane and rowptr_s is non-decreasing, so the
+    // lanes with rowptr_s[probe] <= e form a prefix.
+    const int k = __popcll(mask);  // number of probes <= e
+    const int32_t na = k > 0 ? __shfl(probe, k - 1, 64) : a;
+    const int32_t nb = k < 64 ? __shfl(probe, k, 64) - 1 : b;
+    a = na;
+    b = nb;
   }
   return a;
 }
 
+__device__ inline int rpad(int i) { return i + (i >> 5); }
+
 // Each workgroup fills kRelayTile consecutive positions of the sorted CSR.
-// Degree-0 rows sort first, so every row that owns one of these positions
-// is non-empty and at most kRelayTile rows are involved.
+// Degree-0 rows sort first, so every row owning one of these positions is
+// non-empty and at most kRelayTile rows (the "window") are involved. Each
+// window row marks its first position; an inclusive max-scan of the marks
+// then gives every position its row in O(1).
 __global__ __launch_bounds__(kThreads) void k_relayout(
     int32_t n, int64_t nnz, int32_t n_cols, const int32_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, const float* __restrict__ vals,
@@ -337,11 +476,19 @@ __global__ __launch_bounds__(kThreads) void k_relayout(
   if (failed(err)) return;
   __shared__ int32_t s_ptr[kRelayTile + 1];  // rowptr_s over the window rows (+1 end)
   __shared__ int32_t s_src[kRelayTile];      // first nnz of each window row in the input CSR
+  __shared__ int32_t s_row[kRelayTile + kRelayTile / 32];  // window row of each position
+  __shared__ int32_t s_wmax[kThreads / 64];
   __shared__ int32_t s_lo, s_hi;
   const int64_t e0 = (int64_t)blockIdx.x * kRelayTile;
   const int64_t e1 = e0 + kRelayTile < nnz ? e0 + kRelayTile : nnz;
-  if (threadIdx.x == 0) s_lo = row_of(rowptr_s, n, e0);
-  if (threadIdx.x == 1) s_hi = row_of(rowptr_s, n, e1 - 1);
+  if (threadIdx.x < 64) {
+    const int32_t r = wave_row_of(rowptr_s, n, e0, threadIdx.x);
+    if (threadIdx.x == 0) s_lo = r;
+  } else if (threadIdx.x < 128) {
+    const int32_t r = wave_row_of(rowptr_s, n, e1 - 1, threadIdx.x - 64);
+    if (threadIdx.x == 64) s_hi = r;
+  }
+  for (int k = threadIdx.x; k < kRelayTile; k += kThreads) s_row[rpad(k)] = 0;
   __syncthreads();
   const int32_t lo = s_lo;
   const int32_t nw = s_hi - lo + 1;
@@ -352,46 +499,52 @@ __global__ __launch_bounds__(kThreads) void k_relayout(
   for (int k = threadIdx.x; k <= nw; k += kThreads) s_ptr[k] = rowptr_s[lo + k];
   for (int k = threadIdx.x; k < nw; k += kThreads) s_src[k] = rowptr[perm[lo + k]];
   __syncthreads();
+  // Window rows 1..nw-1 start strictly inside the tile.
+  for (int w = 1 + threadIdx.x; w < nw; w += kThreads) s_row[rpad((int)(s_ptr[w] - e0))] = w;
+  __syncthreads();
+  // Inclusive max-scan of the marks; thread t owns positions 8t .. 8t+7.
+  int32_t v[kRelayItems];
+  int32_t m = 0;
+#pragma unroll
+  for (int k = 0; k < kRelayItems; ++k) {
+    m = max(m, s_row[rpad(threadIdx.x * kRelayItems + k)]);
+    v[k] = m;
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int32_t inc = m;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc = max(inc, y);
+  }
+  if (lane == 63) s_wmax[wv] = inc;
+  int32_t before = __shfl_up(inc, 1, 64);
+  if (lane == 0) before = 0;
+  __syncthreads();
+  for (int w = 0; w < wv; ++w) before = max(before, s_wmax[w]);
+#pragma unroll
+  for (int k = 0; k < kRelayItems; ++k)
+    s_row[rpad(threadIdx.x * kRelayItems + k)] = max(before, v[k]);
+  __syncthreads();
   uint32_t bad = 0;
 #pragma unroll
   for (int k = 0; k < kRelayItems; ++k) {
-    const int64_t e = e0 + (int64_t)k * kThreads + threadIdx.x;
+    const int j = k * kThreads + threadIdx.x;
+    const int64_t e = e0 + j;
     if (e < e1) {
-      int32_t a = 0, b = nw - 1;
-      while (a < b) {
-        const int32_t mid = (a + b + 1) >> 1;
-        if (s_ptr[mid] <= e) a = mid; else b = mid - 1;
-      }
-      const int64_t src = (int64_t)s_src[a] + (e - s_ptr[a]);
+      const int32_t w = s_row[rpad(j)];
+      const int64_t src = (int64_t)s_src[w] + (e - s_ptr[w]);
       const int32_t c = colidx[src];
-      const float v = vals[src];
+      const float val = vals[src];
       if ((uint32_t)c >= (uint32_t)n_cols) bad = kErrColumn;
       colidx_s[e] = c;
-      vals_s[e] = v;
+      vals_s[e] = val;
     }
   }
   if (bad) atomicOr(err, bad);
 }
 
 // --- partition ---------------------------------------------------------------
-
-// Alg. 1: for degree d, the smallest factor f of W with f * Z >= d gives
-// block_rows = W / f and warp_nzs = ceil(d / f). Stored as warp_nzs << 16 | rows.
-// Degree 0 (no nnz) gets W rows per block and warp_nzs 0.
-__global__ __launch_bounds__(kThreads) void k_patterns(int32_t W, int32_t Z, int32_t* pat) {
-  const int32_t d = blockIdx.x * kThreads + threadIdx.x;
-  if (d > W * Z) return;
-  if (d == 0) {
-    pat[0] = W;
-    return;
-  }
-  for (int32_t f = 1; f <= W; ++f) {
-    if (W % f == 0 && f * Z >= d) {
-      pat[d] = (((d + f - 1) / f) << 16) | (W / f);
-      return;
-    }
-  }
-}
 
 // cls[d] = first sorted row whose degree is >= d, for d in [0, DB + 1] (n if none).
 __global__ __launch_bounds__(kThreads) void k_class_start(int32_t n, const int32_t* __restrict__ deg_s,
@@ -409,9 +562,8 @@ __global__ __launch_bounds__(kThreads) void k_class_start(int32_t n, const int32
 // Segments: s <= DB is degree class s (ceil(count / block_rows) entries);
 // s > DB is hub row s - DB - 1 in sorted order (ceil(deg / H) chunk entries).
 __global__ __launch_bounds__(kThreads) void k_seg_count(int32_t n, const int32_t* __restrict__ deg_s,
-                                                        const int32_t* __restrict__ cls,
-                                                        const int32_t* __restrict__ pat, int32_t DB,
-                                                        int32_t H, int32_t S,
+                                                        const int32_t* __restrict__ cls, int32_t W,
+                                                        int32_t Z, int32_t DB, int32_t H, int32_t S,
                                                         int32_t* __restrict__ nb,
                                                         const uint32_t* err) {
   if (failed(err)) return;
@@ -420,8 +572,10 @@ __global__ __launch_bounds__(kThreads) void k_seg_count(int32_t n, const int32_t
   int64_t v = 0;
   if (s <= DB) {
     const int64_t cnt = cls[s + 1] - cls[s];
-    const int64_t br = pat[s] & 0xFFFF;
-    v = (cnt + br - 1) / br;
+    if (cnt > 0) {
+      const int64_t br = pattern_of((int32_t)s, W, Z) & 0xFFFF;
+      v = (cnt + br - 1) / br;
+    }
   } else {
     const int64_t r = (int64_t)cls[DB + 1] + (s - DB - 1);
     if (r < n) v = ((int64_t)deg_s[r] + H - 1) / H;
@@ -432,9 +586,8 @@ __global__ __launch_bounds__(kThreads) void k_seg_count(int32_t n, const int32_t
 // Alg. 2's entries, each computed independently from its segment.
 __global__ __launch_bounds__(kThreads) void k_meta_fill(
     const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ deg_s,
-    const int32_t* __restrict__ cls, const int32_t* __restrict__ pat,
-    const int32_t* __restrict__ seg_off, int32_t S, int32_t DB, int32_t H, int4* __restrict__ meta,
-    int64_t cap, const uint32_t* err) {
+    const int32_t* __restrict__ cls, const int32_t* __restrict__ seg_off, int32_t S, int32_t W,
+    int32_t Z, int32_t DB, int32_t H, int4* __restrict__ meta, int64_t cap, const uint32_t* err) {
   if (failed(err)) return;
   const int64_t total = seg_off[S];
   for (int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x; b < total && b < cap;
@@ -447,7 +600,7 @@ __global__ __launch_bounds__(kThreads) void k_meta_fill(
     const int32_t j = (int32_t)(b - seg_off[a]);
     int4 m;
     if (a <= DB) {
-      const int32_t p = pat[a], br = p & 0xFFFF, wn = p >> 16;
+      const int32_t p = pattern_of(a, W, Z), br = p & 0xFFFF, wn = p >> 16;
       const int32_t r0 = cls[a] + j * br;
       const int32_t left = cls[a + 1] - r0;
       const int32_t rows = left < br ? left : br;
@@ -495,25 +648,60 @@ int check_launch(const char* what) {
 }
 
 // out[i] = sum of in[0..i) for i < n, and *total = sum of all (may alias out + n).
-// In place (out == in) is allowed. With `gate`, the scan is skipped on the
-// device when the radix pass at `gate_shift` is.
+// In place (out == in) is allowed. With `gate`, the scan belongs to radix
+// pass `gate_pass` and is skipped on the device when that pass is.
 int scan_exclusive(const int32_t* in, int64_t n, int32_t* out, int32_t* total, int32_t* partials,
                    const uint32_t* err, hipStream_t st, const int32_t* gate = nullptr,
-                   int gate_shift = 0) {
+                   int gate_pass = 0) {
   if (n > kScanMaxN) return fail(AGCN_ERR_UNSUPPORTED, "scan longer than the supported maximum");
   if (n == 0) {
     if (total) k_set<<<1, 64, 0, st>>>(total, 0);
     return check_launch("k_set");
   }
   if (n <= kScanSingleMax) {
-    k_scan_single<<<1, kScanTopThreads, 0, st>>>(in, (int32_t)n, out, total, err, gate, gate_shift);
+    k_scan_single<<<1, kScanTopThreads, 0, st>>>(in, (int32_t)n, out, total, err, gate, gate_pass);
     return check_launch("k_scan_single");
   }
   const unsigned nb = grid_for(n, kScanBlock);
-  k_scan_reduce<<<nb, kThreads, 0, st>>>(in, n, partials, err, gate, gate_shift);
-  k_scan_top<<<1, kScanTopThreads, 0, st>>>(partials, (int32_t)nb, total, err, gate, gate_shift);
-  k_scan_down<<<nb, kThreads, 0, st>>>(in, n, partials, out, err, gate, gate_shift);
+  k_scan_reduce<<<nb, kThreads, 0, st>>>(in, n, partials, err, gate, gate_pass);
+  if (nb <= kScanTwoPassMaxBlocks) {
+    k_scan_down<<<nb, kThreads, 0, st>>>(in, n, partials, out, total, 1, err, gate, gate_pass);
+  } else {
+    k_scan_top<<<1, kScanTopThreads, 0, st>>>(partials, (int32_t)nb, total, err, gate, gate_pass);
+    k_scan_down<<<nb, kThreads, 0, st>>>(in, n, partials, out, nullptr, 0, err, gate, gate_pass);
+  }
   return check_launch("scan");
+}
+
+// Per-thread pinned host buffer for the plan's read-backs, allocated on the
+// first plan built by the thread and kept for the life of the process.
+PlanSummary* pinned_summary() {
+  thread_local PlanSummary* buf = nullptr;
+  if (buf == nullptr) {
+    void* q = nullptr;
+    if (hipHostMalloc(&q, sizeof(PlanSummary), hipHostMallocDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    buf = static_cast<PlanSummary*>(q);
+  }
+  return buf;
+}
+
+// Per-thread, per-device event marking the maximum-degree read-back.
+hipEvent_t plan_event() {
+  thread_local std::map<int, hipEvent_t> events;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  auto it = events.find(dev);
+  if (it != events.end()) return it->second;
+  hipEvent_t e = nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  events[dev] = e;
+  return e;
 }
 
 struct Layout {
@@ -555,12 +743,13 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   const size_t o_ids2 = L.take(4 * n);
   const size_t o_counts = L.take(4 * n_counts);
   const size_t o_partials = L.take(4 * n_partials);
-  const size_t o_pat = L.take(4 * (DB + 1));
   const size_t o_cls = L.take(4 * (DB + 2));
   const size_t o_nb = L.take(4 * S);
   const size_t o_seg = L.take(4 * (S + 1));
   const size_t o_err = L.take(64);
   const size_t o_dmax = L.take(64);
+  const int64_t n_deg_blocks = ceil_div64(n, kThreads);
+  const size_t o_bmax = L.take(4 * (n_deg_blocks + 1));
   const size_t o_sum = L.take(sizeof(PlanSummary));
 
   void* base = nullptr;
@@ -582,43 +771,51 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   int32_t* ids2 = reinterpret_cast<int32_t*>(b + o_ids2);
   int32_t* counts = reinterpret_cast<int32_t*>(b + o_counts);
   int32_t* partials = reinterpret_cast<int32_t*>(b + o_partials);
-  int32_t* pat = reinterpret_cast<int32_t*>(b + o_pat);
   int32_t* cls = reinterpret_cast<int32_t*>(b + o_cls);
   int32_t* nb = reinterpret_cast<int32_t*>(b + o_nb);
   int32_t* seg = reinterpret_cast<int32_t*>(b + o_seg);
   uint32_t* err = reinterpret_cast<uint32_t*>(b + o_err);
   int32_t* dmax = reinterpret_cast<int32_t*>(b + o_dmax);
+  int32_t* bmax = reinterpret_cast<int32_t*>(b + o_bmax);
   PlanSummary* dsum = reinterpret_cast<PlanSummary*>(b + o_sum);
 
+  PlanSummary* hs = pinned_summary();
+  if (hs == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "pinned host buffer allocation failed");
+  hipError_t he;
   k_init<<<1, 64, 0, st>>>(err, dmax, dsum);
   if (n > 0) {
-    k_degree<<<grid_for(n, kThreads), kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err, dmax);
+    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err,
+                                                         bmax);
+    k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, (int32_t)n_deg_blocks, dmax);
     if ((rc = check_launch("k_degree"))) return rc;
+    // The maximum degree goes to the host while radix pass 0 (always needed)
+    // runs; the host then launches exactly the passes it needs.
+    he = hipMemcpyAsync(&hs->max_deg, dmax, sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    if (he != hipSuccess) return hip_fail(he, "hipMemcpyAsync(max degree)");
+    hipEvent_t ev = plan_event();
+    if (ev == nullptr || (he = hipEventRecord(ev, st)) != hipSuccess)
+      return hip_fail(ev ? he : hipErrorOutOfMemory, "hipEventRecord(plan)");
 
-    // Stable LSD radix sort of row ids by degree. Degrees are at most nnz,
-    // so ceil(bits(nnz) / 8) passes order them completely. The pass schedule
-    // makes the last pass land in (keys, perm).
-    int bits = 0;
-    while (bits < 31 && (int64_t(1) << bits) <= nnz) ++bits;
-    const int passes = std::max(1, (bits + 7) / 8);
+    // Stable LSD radix sort of row ids by degree, 8-bit digits.
     const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
-    const int32_t* kin = deg;
-    const int32_t* iin = nullptr;  // identity order on the first pass
+    const RadixBufs bufs{deg, {keys, keys2}, {p->perm, ids2}};
+    int passes = 1;
     for (int pass = 0; pass < passes; ++pass) {
-      const bool to_final = ((passes - 1 - pass) % 2) == 0;
-      int32_t* kout = to_final ? keys : keys2;
-      int32_t* iout = to_final ? p->perm : ids2;
-      const int shift = 8 * pass;
-      k_radix_hist<<<rgrid, kThreads, 0, st>>>((int32_t)n, kin, shift, counts, (int32_t)n_tiles, err,
+      k_radix_hist<<<rgrid, kThreads, 0, st>>>((int32_t)n, bufs, pass, counts, (int32_t)n_tiles, err,
                                                dmax);
       if ((rc = check_launch("k_radix_hist"))) return rc;
-      if ((rc = scan_exclusive(counts, n_counts, counts, nullptr, partials, err, st, dmax, shift)))
+      if ((rc = scan_exclusive(counts, n_counts, counts, nullptr, partials, err, st, dmax, pass)))
         return rc;
-      k_radix_scatter<<<rgrid, kThreads, 0, st>>>((int32_t)n, kin, iin, shift, counts,
-                                                  (int32_t)n_tiles, kout, iout, err, dmax);
+      k_radix_scatter<<<rgrid, kThreads, 0, st>>>((int32_t)n, bufs, pass, counts, (int32_t)n_tiles,
+                                                  err, dmax);
       if ((rc = check_launch("k_radix_scatter"))) return rc;
-      kin = kout;
-      iin = iout;
+      if (pass == 0) {
+        if ((he = hipEventSynchronize(ev)) != hipSuccess) return hip_fail(he, "hipEventSynchronize");
+        const int32_t md = hs->max_deg;
+        int bits = 0;
+        while (bits < 31 && (int64_t(1) << bits) <= md) ++bits;
+        passes = std::max(1, (bits + 7) / 8);
+      }
     }
   }
   // rowptr_s = exclusive scan of the sorted degrees; rowptr_s[n] = nnz.
@@ -629,38 +826,36 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
         p->vals_s, err);
     if ((rc = check_launch("k_relayout"))) return rc;
   }
-  k_patterns<<<grid_for((int64_t)DB + 1, kThreads), kThreads, 0, st>>>(W, Z, pat);
   k_class_start<<<grid_for(n + 1, kThreads), kThreads, 0, st>>>((int32_t)n, keys, DB, cls, err);
-  k_seg_count<<<grid_for(S, kThreads), kThreads, 0, st>>>((int32_t)n, keys, cls, pat, DB, H,
+  k_seg_count<<<grid_for(S, kThreads), kThreads, 0, st>>>((int32_t)n, keys, cls, W, Z, DB, H,
                                                          (int32_t)S, nb, err);
   if ((rc = check_launch("partition counts"))) return rc;
   if ((rc = scan_exclusive(nb, S, seg, seg + S, partials, err, st))) return rc;
   const unsigned mgrid = (unsigned)std::min<int64_t>(grid_for(ent_ub, kThreads), 16384);
-  k_meta_fill<<<mgrid, kThreads, 0, st>>>(p->rowptr_s, keys, cls, pat, seg, (int32_t)S, DB, H,
+  k_meta_fill<<<mgrid, kThreads, 0, st>>>(p->rowptr_s, keys, cls, seg, (int32_t)S, W, Z, DB, H,
                                           p->meta, ent_ub, err);
   k_hub_offsets<<<grid_for(hub_ub + 1, kThreads), kThreads, 0, st>>>(
       (int32_t)n, keys, cls, seg, (int32_t)S, DB, (int32_t)hub_ub, p->hub_chunk_off, dsum, err);
   if ((rc = check_launch("partition fill"))) return rc;
 
-  PlanSummary hs{};
-  hipError_t he = hipMemcpyAsync(&hs, dsum, sizeof(hs), hipMemcpyDeviceToHost, st);
+  he = hipMemcpyAsync(hs, dsum, sizeof(PlanSummary), hipMemcpyDeviceToHost, st);
   if (he != hipSuccess) return hip_fail(he, "hipMemcpyAsync(summary)");
   he = hipStreamSynchronize(st);
   if (he != hipSuccess) return hip_fail(he, "hipStreamSynchronize(plan)");
-  if (hs.err) {
+  if (hs->err) {
     std::string why;
-    if (hs.err & kErrRowptrStart) why += " rowptr[0] != 0;";
-    if (hs.err & kErrRowptrOrder) why += " rowptr decreases or leaves [0, nnz];";
-    if (hs.err & kErrRowptrEnd) why += " rowptr[n_rows] != nnz;";
-    if (hs.err & kErrColumn) why += " column index outside [0, n_cols);";
-    if (hs.err & kErrInternal) return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
+    if (hs->err & kErrRowptrStart) why += " rowptr[0] != 0;";
+    if (hs->err & kErrRowptrOrder) why += " rowptr decreases or leaves [0, nnz];";
+    if (hs->err & kErrRowptrEnd) why += " rowptr[n_rows] != nnz;";
+    if (hs->err & kErrColumn) why += " column index outside [0, n_cols);";
+    if (hs->err & kErrInternal) return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
     return fail(AGCN_ERR_INVALID_INPUT, "invalid CSR:" + why);
   }
-  p->n_entries = hs.n_entries;
-  p->hub_first_entry = hs.hub_first_entry;
-  p->n_hub_rows = hs.n_hub_rows;
-  p->hub_first_row = hs.hub_first_row;
-  p->max_deg = hs.max_deg;
+  p->n_entries = hs->n_entries;
+  p->hub_first_entry = hs->hub_first_entry;
+  p->n_hub_rows = hs->n_hub_rows;
+  p->hub_first_row = hs->hub_first_row;
+  p->max_deg = hs->max_deg;
   return AGCN_OK;
 }
 
