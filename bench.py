@@ -112,7 +112,7 @@ def main():
     ap.add_argument("--Z", type=int, default=None)
     ap.add_argument("--H", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-frac", type=float, default=0.2)
+    ap.add_argument("--cpu-frac", type=float, default=0.4)
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run a plain device copy of 1 GiB (counter calibration)")
     args = ap.parse_args()
