@@ -158,6 +158,7 @@ const char* agcn_last_error(void) { return agcn::g_last_error.c_str(); }
 static void plan_free(agcn_plan* p) {
   if (p == nullptr) return;
   agcn::device_release(p->device, p->base, p->bytes);
+  if (p->ready != nullptr) (void)hipEventDestroy(p->ready);
   delete p;
 }
 

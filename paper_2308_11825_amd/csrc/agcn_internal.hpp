@@ -52,6 +52,8 @@ struct agcn_plan {
   float* vals_s = nullptr;          // [nnz]
   int4* meta = nullptr;             // [entries upper bound] {deg, loc, row, info}
   int32_t* hub_chunk_off = nullptr; // [hub rows upper bound + 1] first chunk of each hub row
+  int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
+  hipEvent_t ready = nullptr;       // recorded after the launch order is built
 };
 
 namespace agcn {

@@ -19,12 +19,17 @@
 //   scan            entry offsets of every segment
 //   k_meta_fill     one int4 {deg, loc, row, info} per entry, in Alg. 2's order
 //   k_hub_offsets   first chunk of each hub row + summary for the host
+//   (host sync)     entry counts read back
+//   launch order    hub-chunk entries sorted by a 16-bit key of their first
+//                   column (two radix passes, when hub rows are long), then
+//                   the other entries heaviest first; an event marks it ready
 //
 // Stability of the radix sort comes from giving each 64-lane wave a tile of
 // consecutive rows that it walks in order, ranking equal digits inside a
 // round with ballots; every count is an integer, so the result is exact.
 #include <algorithm>
 #include <climits>
+#include <cstdlib>
 #include <map>
 
 #include "agcn_internal.hpp"
@@ -56,6 +61,9 @@ constexpr int kRelayItems = 8;
 constexpr int kRelayTile = kThreads * kRelayItems;  // 2048
 
 constexpr uint32_t kErrInternal = 1u << 8;
+
+// Launch-order sort of hub chunks: minimum mean chunks per hub row.
+constexpr int kOrderMinChunks = 8;
 
 __device__ inline bool failed(const uint32_t* err) { return err[0] != 0; }
 
@@ -636,6 +644,38 @@ __global__ __launch_bounds__(kThreads) void k_hub_offsets(
   }
 }
 
+// --- launch order -----------------------------------------------------------
+
+// Key of hub chunk i: its first column scaled to 16 bits. Chunks of a row
+// with sorted columns cover narrow column ranges, so ordering chunks by this
+// key makes chunks that run side by side gather neighbouring X rows.
+__global__ __launch_bounds__(kThreads) void k_hub_keys(const int4* __restrict__ meta,
+                                                       const int32_t* __restrict__ colidx_s,
+                                                       int32_t hub_first, int32_t n_chunks,
+                                                       int32_t n_cols, int32_t* __restrict__ keys,
+                                                       int32_t* gate) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i == 0) gate[0] = 0xFFFF;  // two 8-bit passes
+  if (i >= n_chunks) return;
+  const int32_t c = colidx_s[meta[hub_first + i].y];
+  keys[i] = (int32_t)(((int64_t)c << 16) / n_cols);
+}
+
+// order[i] = entry launched by workgroup i: the n_chunks hub entries first
+// (sorted ids, or in reverse entry order without them), then the remaining
+// entries from the heaviest down.
+__global__ __launch_bounds__(kThreads) void k_order_fill(int32_t* __restrict__ order,
+                                                         int32_t n_entries, int32_t hub_first,
+                                                         int32_t n_chunks,
+                                                         const int32_t* __restrict__ sorted_ids) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n_entries) return;
+  if (i < n_chunks)
+    order[i] = sorted_ids ? hub_first + sorted_ids[i] : n_entries - 1 - (int32_t)i;
+  else
+    order[i] = hub_first - 1 - (int32_t)(i - n_chunks);
+}
+
 // ---------------------------------------------------------------------------
 
 inline unsigned grid_for(int64_t work, int per_block) {
@@ -671,6 +711,16 @@ int scan_exclusive(const int32_t* in, int64_t n, int32_t* out, int32_t* total, i
     k_scan_down<<<nb, kThreads, 0, st>>>(in, n, partials, out, nullptr, 0, err, gate, gate_pass);
   }
   return check_launch("scan");
+}
+
+// Hub-chunk launch order by column (AGCN_HUB_ORDER=0 keeps the plain
+// heaviest-first order, for measurements).
+bool hub_order_setting() {
+  static const bool v = [] {
+    const char* s = std::getenv("AGCN_HUB_ORDER");
+    return s == nullptr || std::atoi(s) != 0;
+  }();
+  return v;
 }
 
 // Per-thread pinned host buffer for the plan's read-backs, allocated on the
@@ -722,8 +772,9 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   const int64_t ent_ub = n + nnz / H + 1;         // every entry holds a row or a full chunk
   const int64_t hub_ub = std::min<int64_t>(n, nnz / (DB + 1));
   const int64_t S = (int64_t)DB + 1 + hub_ub;     // segments: degree classes + hub rows
+  const int64_t chunk_ub = nnz / H + hub_ub + 1;   // hub-chunk entries
   const int64_t n_tiles = ceil_div64(n, kRadixTile);
-  const int64_t n_counts = n_tiles * kRadixBins;
+  const int64_t n_counts = ceil_div64(std::max<int64_t>(n, chunk_ub), kRadixTile) * kRadixBins;
   const int64_t scan_max = std::max<int64_t>({n_counts, n + 1, S + 1});
   const int64_t n_partials = ceil_div64(scan_max, kScanBlock) + 1;
   if (ent_ub >= INT32_MAX || S + 1 >= INT32_MAX || n_counts > kScanMaxN)
@@ -736,6 +787,7 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   const size_t o_vals_s = L.take(4 * nnz);
   const size_t o_meta = L.take(16 * ent_ub);
   const size_t o_hub = L.take(4 * (hub_ub + 1));
+  const size_t o_order = L.take(4 * ent_ub);
   // working buffers
   const size_t o_deg = L.take(4 * n);
   const size_t o_keys = L.take(4 * n);    // sorted degrees end here
@@ -750,6 +802,8 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   const size_t o_dmax = L.take(64);
   const int64_t n_deg_blocks = ceil_div64(n, kThreads);
   const size_t o_bmax = L.take(4 * (n_deg_blocks + 1));
+  const size_t o_hsort = L.take(4 * 5 * chunk_ub);  // keys in, 2 x keys, 2 x ids
+  const size_t o_hgate = L.take(64);
   const size_t o_sum = L.take(sizeof(PlanSummary));
 
   void* base = nullptr;
@@ -765,6 +819,7 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   p->vals_s = reinterpret_cast<float*>(b + o_vals_s);
   p->meta = reinterpret_cast<int4*>(b + o_meta);
   p->hub_chunk_off = reinterpret_cast<int32_t*>(b + o_hub);
+  p->order = reinterpret_cast<int32_t*>(b + o_order);
   int32_t* deg = reinterpret_cast<int32_t*>(b + o_deg);
   int32_t* keys = reinterpret_cast<int32_t*>(b + o_keys);
   int32_t* keys2 = reinterpret_cast<int32_t*>(b + o_keys2);
@@ -777,6 +832,8 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   uint32_t* err = reinterpret_cast<uint32_t*>(b + o_err);
   int32_t* dmax = reinterpret_cast<int32_t*>(b + o_dmax);
   int32_t* bmax = reinterpret_cast<int32_t*>(b + o_bmax);
+  int32_t* hsort = reinterpret_cast<int32_t*>(b + o_hsort);
+  int32_t* hgate = reinterpret_cast<int32_t*>(b + o_hgate);
   PlanSummary* dsum = reinterpret_cast<PlanSummary*>(b + o_sum);
 
   PlanSummary* hs = pinned_summary();
@@ -856,6 +913,40 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   p->n_hub_rows = hs->n_hub_rows;
   p->hub_first_row = hs->hub_first_row;
   p->max_deg = hs->max_deg;
+
+  // Launch order for the SpMM (does not change any result, only which
+  // entries run side by side). Queued after the synchronisation; agcn_spmm
+  // waits for the event recorded below.
+  const int32_t n_chunks = p->n_hub_rows > 0 ? p->n_entries - p->hub_first_entry : 0;
+  const int32_t* sorted_ids = nullptr;
+  // Only long rows have chunks with narrow column ranges: sort when the hub
+  // rows average at least kOrderMinChunks chunks (otherwise each chunk spans
+  // most columns and the sort costs more than it saves).
+  if (n_chunks > 0 && hub_order_setting() &&
+      (int64_t)n_chunks >= (int64_t)kOrderMinChunks * p->n_hub_rows) {
+    const int64_t ct = ceil_div64(n_chunks, kRadixTile);
+    int32_t* hk_in = hsort;
+    const RadixBufs hb{hk_in, {hsort + chunk_ub, hsort + 2 * chunk_ub},
+                       {hsort + 3 * chunk_ub, hsort + 4 * chunk_ub}};
+    k_hub_keys<<<grid_for(n_chunks, kThreads), kThreads, 0, st>>>(
+        p->meta, p->colidx_s, p->hub_first_entry, n_chunks, p->n_cols, hk_in, hgate);
+    const unsigned hgrid = grid_for(ct, kRadixWaves);
+    for (int pass = 0; pass < 2; ++pass) {
+      k_radix_hist<<<hgrid, kThreads, 0, st>>>(n_chunks, hb, pass, counts, (int32_t)ct, err, hgate);
+      if ((rc = scan_exclusive(counts, ct * kRadixBins, counts, nullptr, partials, err, st)))
+        return rc;
+      k_radix_scatter<<<hgrid, kThreads, 0, st>>>(n_chunks, hb, pass, counts, (int32_t)ct, err,
+                                                  hgate);
+    }
+    sorted_ids = hb.ids[0];
+  }
+  if (p->n_entries > 0)
+    k_order_fill<<<grid_for(p->n_entries, kThreads), kThreads, 0, st>>>(
+        p->order, p->n_entries, p->hub_first_entry, n_chunks, sorted_ids);
+  if ((rc = check_launch("launch order"))) return rc;
+  if ((he = hipEventCreateWithFlags(&p->ready, hipEventDisableTiming)) != hipSuccess)
+    return hip_fail(he, "hipEventCreate(plan ready)");
+  if ((he = hipEventRecord(p->ready, st)) != hipSuccess) return hip_fail(he, "hipEventRecord(plan ready)");
   return AGCN_OK;
 }
 

@@ -30,7 +30,10 @@
 //   add a contiguous run of the row's chunk partials, then a fixed pairwise
 //   tree combines the G sums and the row is written once.
 //
-// Entries are launched heaviest first (metadata is in ascending degree order).
+// Launch order (built by the plan): hub-chunk entries sorted by the first
+// column they gather, so chunks running side by side read neighbouring X rows
+// and share them in L2; then the other entries heaviest first (the metadata
+// is in ascending degree order).
 #include <algorithm>
 #include <climits>
 #include <cstdlib>
@@ -107,7 +110,8 @@ __device__ inline typename VecOf<VW>::T gather_row(const int32_t* s_col, const f
 // LT > 0: lanes per vwarp fixed at compile time; LT == 0: taken from L.
 template <int VW, int LT>
 __global__ __launch_bounds__(1024) void k_spmm(
-    const int4* __restrict__ meta, int32_t n_entries, int32_t entry_base, int32_t hub_first_entry,
+    const int4* __restrict__ meta, const int32_t* __restrict__ order, int32_t entry_base,
+    int32_t hub_first_entry,
     int32_t deg_bound, int32_t W, const int32_t* __restrict__ colidx_s,
     const float* __restrict__ vals_s, const int32_t* __restrict__ perm, const float* __restrict__ X,
     int64_t ldx, float* __restrict__ Y, int64_t ldy, float* __restrict__ ws, int32_t F,
@@ -120,7 +124,7 @@ __global__ __launch_bounds__(1024) void k_spmm(
   V* s_part = reinterpret_cast<V*>(smem + 2 * cap_pad);
 
   const int T = blockDim.x;
-  const int32_t b = n_entries - 1 - (entry_base + (int32_t)blockIdx.x);
+  const int32_t b = order[entry_base + (int32_t)blockIdx.x];
   const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
   const int4 m = meta[b];
   const int32_t deg = m.x, loc = m.y, row = m.z, info = m.w;
@@ -294,7 +298,7 @@ void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice
   for (int64_t e0 = 0; e0 < p->n_entries; e0 += max_grid) {
     const int64_t cnt = std::min<int64_t>(max_grid, p->n_entries - e0);
     dim3 grid((unsigned)cnt, (unsigned)n_slices);
-    k_spmm<VW, LT><<<grid, T, lds, a.st>>>(p->meta, p->n_entries, (int32_t)e0, p->hub_first_entry,
+    k_spmm<VW, LT><<<grid, T, lds, a.st>>>(p->meta, p->order, (int32_t)e0, p->hub_first_entry,
                                            p->deg_bound, p->W, p->colidx_s, p->vals_s, p->perm,
                                            a.X, a.ldx, a.Y, a.ldy, a.ws, a.F, col_base, slice_cols,
                                            L, rounds, cap_pad);
@@ -365,6 +369,10 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
                    aligned16(Y) && (ws == nullptr || aligned16(ws));
   const SpmmArgs a{p, F, X, ldx, Y, ldy, ws, st};
   hipError_t e;
+  // The plan's last kernels (the launch order) were queued on the plan's
+  // stream after its host synchronisation; order this stream after them.
+  if (p->ready && (e = hipStreamWaitEvent(st, p->ready, 0)) != hipSuccess)
+    return hip_fail(e, "hipStreamWaitEvent(plan ready)");
   if (ev_begin && (e = hipEventRecord(ev_begin, st)) != hipSuccess)
     return hip_fail(e, "hipEventRecord");
   int rc = AGCN_OK;
