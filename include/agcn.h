@@ -128,11 +128,11 @@ int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes);
 int agcn_spmm(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
               int64_t ldy, void* d_ws, void* stream);
 
-/* agcn_spmm plus timing marks: records the caller's hipEvent_t handles (each
- * may be NULL) on `stream` before the aggregation kernel (ev_begin), between
- * it and the hub-row reduction (ev_mid), and after the reduction (ev_end).
- * Same kernels, same launch shapes; used to time the aggregation kernel by
- * itself. */
+/* agcn_spmm plus timing marks on the caller's hipEvent_t handles (each may be
+ * NULL): ev_begin is recorded when the aggregation kernel starts and ev_mid
+ * when it ends (attached to the kernel's own launch, so no marker packet sits
+ * between kernels), ev_end after the hub-row reduction. Same kernels, same
+ * launch shapes; used to time the aggregation kernel by itself. */
 int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
                     int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
                     void* ev_end);

@@ -2,7 +2,10 @@
 // (Sec. III-C "Degree Sorting" and "Block-level Partition", Alg. 1 and Alg. 2).
 //
 // Pipeline (all on one stream, one host synchronisation at the end):
-//   k_init          clear the error word, the maximum degree and the summary
+//   k_init          clear the error word and the maximum degree
+// The two read-backs (maximum degree, summary) are written by the kernels
+// straight into pinned, host-coherent memory; the host reads them after an
+// event or stream synchronisation, with no copy launched.
 //   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
 //                   per-workgroup maximum degree
 //   k_dmax          maximum degree (one workgroup); copied to pinned host
@@ -145,16 +148,10 @@ __device__ inline int32_t pattern_of(int32_t d, int32_t W, int32_t Z) {
 
 // ---------------------------------------------------------------------------
 
-__global__ void k_init(uint32_t* err, int32_t* dmax, PlanSummary* sum) {
+__global__ void k_init(uint32_t* err, int32_t* dmax) {
   if (threadIdx.x == 0) {
     err[0] = 0;
     dmax[0] = 0;
-    sum->n_entries = 0;
-    sum->hub_first_entry = 0;
-    sum->n_hub_rows = 0;
-    sum->hub_first_row = 0;
-    sum->max_deg = 0;
-    sum->err = 0;
   }
 }
 
@@ -196,7 +193,8 @@ __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
 
 // Maximum of the per-workgroup maxima (one workgroup of kScanTopThreads).
 __global__ __launch_bounds__(kScanTopThreads) void k_dmax(const int32_t* __restrict__ block_max,
-                                                          int32_t nb, int32_t* dmax) {
+                                                          int32_t nb, int32_t* dmax,
+                                                          PlanSummary* host_sum) {
   __shared__ int32_t s_max[kScanTopThreads / 64];
   int32_t m = 0;
   for (int32_t i = threadIdx.x; i < nb; i += kScanTopThreads) m = max(m, block_max[i]);
@@ -207,6 +205,8 @@ __global__ __launch_bounds__(kScanTopThreads) void k_dmax(const int32_t* __restr
     int32_t t = 0;
     for (int w = 0; w < kScanTopThreads / 64; ++w) t = max(t, s_max[w]);
     dmax[0] = t;
+    host_sum->max_deg = t;
+    __threadfence_system();
   }
 }
 
@@ -630,7 +630,10 @@ __global__ __launch_bounds__(kThreads) void k_hub_offsets(
     int32_t* __restrict__ hub_chunk_off, PlanSummary* sum, const uint32_t* err) {
   const int64_t h = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const uint32_t e = err[0];
-  if (h == 0) sum->err = e;
+  if (h == 0) {
+    sum->err = e;
+    if (e) __threadfence_system();
+  }
   if (e) return;
   const int32_t first = cls[DB + 1];
   const int32_t n_hub = n - first;
@@ -641,6 +644,7 @@ __global__ __launch_bounds__(kThreads) void k_hub_offsets(
     sum->n_hub_rows = n_hub;
     sum->hub_first_row = first;
     sum->max_deg = n > 0 ? deg_s[n - 1] : 0;
+    __threadfence_system();
   }
 }
 
@@ -723,18 +727,29 @@ bool hub_order_setting() {
   return v;
 }
 
-// Per-thread pinned host buffer for the plan's read-backs, allocated on the
-// first plan built by the thread and kept for the life of the process.
-PlanSummary* pinned_summary() {
+// Per-thread pinned, host-coherent buffer for the plan's read-backs (the
+// kernels write it directly), allocated on the first plan built by the thread
+// and kept for the life of the process. *dev receives its device address.
+PlanSummary* pinned_summary(PlanSummary** dev) {
   thread_local PlanSummary* buf = nullptr;
+  thread_local PlanSummary* dbuf = nullptr;
   if (buf == nullptr) {
     void* q = nullptr;
-    if (hipHostMalloc(&q, sizeof(PlanSummary), hipHostMallocDefault) != hipSuccess) {
+    if (hipHostMalloc(&q, sizeof(PlanSummary), hipHostMallocMapped | hipHostMallocCoherent) !=
+        hipSuccess) {
       (void)hipGetLastError();
       return nullptr;
     }
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, q, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      (void)hipHostFree(q);
+      return nullptr;
+    }
     buf = static_cast<PlanSummary*>(q);
+    dbuf = static_cast<PlanSummary*>(d);
   }
+  *dev = dbuf;
   return buf;
 }
 
@@ -804,7 +819,6 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   const size_t o_bmax = L.take(4 * (n_deg_blocks + 1));
   const size_t o_hsort = L.take(4 * 5 * chunk_ub);  // keys in, 2 x keys, 2 x ids
   const size_t o_hgate = L.take(64);
-  const size_t o_sum = L.take(sizeof(PlanSummary));
 
   void* base = nullptr;
   size_t got = 0;
@@ -834,21 +848,20 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
   int32_t* bmax = reinterpret_cast<int32_t*>(b + o_bmax);
   int32_t* hsort = reinterpret_cast<int32_t*>(b + o_hsort);
   int32_t* hgate = reinterpret_cast<int32_t*>(b + o_hgate);
-  PlanSummary* dsum = reinterpret_cast<PlanSummary*>(b + o_sum);
 
-  PlanSummary* hs = pinned_summary();
+  PlanSummary* dsum = nullptr;
+  PlanSummary* hs = pinned_summary(&dsum);
   if (hs == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "pinned host buffer allocation failed");
+  *hs = PlanSummary{};  // no kernel of this thread's previous plan is still running
   hipError_t he;
-  k_init<<<1, 64, 0, st>>>(err, dmax, dsum);
+  k_init<<<1, 64, 0, st>>>(err, dmax);
   if (n > 0) {
     k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err,
                                                          bmax);
-    k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, (int32_t)n_deg_blocks, dmax);
+    k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, (int32_t)n_deg_blocks, dmax, dsum);
     if ((rc = check_launch("k_degree"))) return rc;
-    // The maximum degree goes to the host while radix pass 0 (always needed)
+    // The maximum degree reaches the host while radix pass 0 (always needed)
     // runs; the host then launches exactly the passes it needs.
-    he = hipMemcpyAsync(&hs->max_deg, dmax, sizeof(int32_t), hipMemcpyDeviceToHost, st);
-    if (he != hipSuccess) return hip_fail(he, "hipMemcpyAsync(max degree)");
     hipEvent_t ev = plan_event();
     if (ev == nullptr || (he = hipEventRecord(ev, st)) != hipSuccess)
       return hip_fail(ev ? he : hipErrorOutOfMemory, "hipEventRecord(plan)");
@@ -895,8 +908,6 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
       (int32_t)n, keys, cls, seg, (int32_t)S, DB, (int32_t)hub_ub, p->hub_chunk_off, dsum, err);
   if ((rc = check_launch("partition fill"))) return rc;
 
-  he = hipMemcpyAsync(hs, dsum, sizeof(PlanSummary), hipMemcpyDeviceToHost, st);
-  if (he != hipSuccess) return hip_fail(he, "hipMemcpyAsync(summary)");
   he = hipStreamSynchronize(st);
   if (he != hipSuccess) return hip_fail(he, "hipStreamSynchronize(plan)");
   if (hs->err) {

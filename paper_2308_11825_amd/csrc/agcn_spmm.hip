@@ -38,6 +38,8 @@
 #include <climits>
 #include <cstdlib>
 
+#include <hip/hip_ext.h>
+
 #include "agcn_internal.hpp"
 
 namespace agcn {
@@ -286,8 +288,17 @@ struct SpmmArgs {
   hipStream_t st;
 };
 
+// Timing marks for k_spmm: the first launch records `start` when it begins
+// and the last records `stop` when it ends (hipExtLaunchKernel), so no
+// separate marker packets sit between the kernels.
+struct Marks {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
 template <int VW, int LT>
-void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols) {
+void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols,
+                 Marks& mk, bool last_part) {
   const agcn_plan* p = a.p;
   const int cap_pad = stage_words(std::max(p->deg_bound, p->H));
   const int want = p->W * L;
@@ -298,24 +309,34 @@ void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice
   for (int64_t e0 = 0; e0 < p->n_entries; e0 += max_grid) {
     const int64_t cnt = std::min<int64_t>(max_grid, p->n_entries - e0);
     dim3 grid((unsigned)cnt, (unsigned)n_slices);
-    k_spmm<VW, LT><<<grid, T, lds, a.st>>>(p->meta, p->order, (int32_t)e0, p->hub_first_entry,
-                                           p->deg_bound, p->W, p->colidx_s, p->vals_s, p->perm,
-                                           a.X, a.ldx, a.Y, a.ldy, a.ws, a.F, col_base, slice_cols,
-                                           L, rounds, cap_pad);
+    const hipEvent_t stop = (last_part && e0 + cnt >= p->n_entries) ? mk.stop : nullptr;
+    if (mk.start || stop) {
+      hipExtLaunchKernelGGL(k_spmm<VW, LT>, grid, dim3(T), (uint32_t)lds, a.st, mk.start, stop, 0,
+                            p->meta, p->order, (int32_t)e0, p->hub_first_entry, p->deg_bound, p->W,
+                            p->colidx_s, p->vals_s, p->perm, a.X, a.ldx, a.Y, a.ldy, a.ws, a.F,
+                            col_base, slice_cols, L, rounds, cap_pad);
+      mk.start = nullptr;
+    } else {
+      k_spmm<VW, LT><<<grid, T, lds, a.st>>>(p->meta, p->order, (int32_t)e0, p->hub_first_entry,
+                                             p->deg_bound, p->W, p->colidx_s, p->vals_s, p->perm,
+                                             a.X, a.ldx, a.Y, a.ldy, a.ws, a.F, col_base,
+                                             slice_cols, L, rounds, cap_pad);
+    }
   }
 }
 
 template <int VW>
-void dispatch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols) {
+void dispatch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols, Marks& mk,
+                   bool last_part) {
   switch (L) {
-    case 1: return launch_spmm<VW, 1>(a, L, n_slices, col_base, slice_cols);
-    case 2: return launch_spmm<VW, 2>(a, L, n_slices, col_base, slice_cols);
-    case 4: return launch_spmm<VW, 4>(a, L, n_slices, col_base, slice_cols);
-    case 8: return launch_spmm<VW, 8>(a, L, n_slices, col_base, slice_cols);
-    case 16: return launch_spmm<VW, 16>(a, L, n_slices, col_base, slice_cols);
-    case 32: return launch_spmm<VW, 32>(a, L, n_slices, col_base, slice_cols);
-    case 64: return launch_spmm<VW, 64>(a, L, n_slices, col_base, slice_cols);
-    default: return launch_spmm<VW, 0>(a, L, n_slices, col_base, slice_cols);
+    case 1: return launch_spmm<VW, 1>(a, L, n_slices, col_base, slice_cols, mk, last_part);
+    case 2: return launch_spmm<VW, 2>(a, L, n_slices, col_base, slice_cols, mk, last_part);
+    case 4: return launch_spmm<VW, 4>(a, L, n_slices, col_base, slice_cols, mk, last_part);
+    case 8: return launch_spmm<VW, 8>(a, L, n_slices, col_base, slice_cols, mk, last_part);
+    case 16: return launch_spmm<VW, 16>(a, L, n_slices, col_base, slice_cols, mk, last_part);
+    case 32: return launch_spmm<VW, 32>(a, L, n_slices, col_base, slice_cols, mk, last_part);
+    case 64: return launch_spmm<VW, 64>(a, L, n_slices, col_base, slice_cols, mk, last_part);
+    default: return launch_spmm<VW, 0>(a, L, n_slices, col_base, slice_cols, mk, last_part);
   }
 }
 
@@ -334,7 +355,7 @@ void launch_hub(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_
 // Runs one phase (aggregation or hub reduction) over all column slices: the
 // full slices in one launch, a narrower last slice in a second one.
 template <int VW>
-int run_phase(const SpmmArgs& a, bool hub_phase) {
+int run_phase(const SpmmArgs& a, bool hub_phase, Marks& mk) {
   const int sc_max = VW == 4 ? slice_cols_setting() : std::min(64, slice_cols_setting());
   const int sc = std::min(a.F, sc_max);
   const int n_full = a.F / sc;
@@ -345,8 +366,9 @@ int run_phase(const SpmmArgs& a, bool hub_phase) {
     const int cols = part == 0 ? sc : tail;
     const int L = cols / VW;
     const int col_base = part == 0 ? 0 : n_full * sc;
+    const bool last_part = part == 1 || tail == 0;
     if (hub_phase) launch_hub<VW>(a, L, n_slices, col_base, sc);
-    else dispatch_spmm<VW>(a, L, n_slices, col_base, sc);
+    else dispatch_spmm<VW>(a, L, n_slices, col_base, sc, mk, last_part);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, hub_phase ? "k_hub_reduce launch" : "k_spmm launch");
   }
@@ -373,13 +395,16 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
   // stream after its host synchronisation; order this stream after them.
   if (p->ready && (e = hipStreamWaitEvent(st, p->ready, 0)) != hipSuccess)
     return hip_fail(e, "hipStreamWaitEvent(plan ready)");
-  if (ev_begin && (e = hipEventRecord(ev_begin, st)) != hipSuccess)
-    return hip_fail(e, "hipEventRecord");
+  Marks mk{ev_begin, ev_mid};
   int rc = AGCN_OK;
-  if (p->n_entries > 0) rc = vec ? run_phase<4>(a, false) : run_phase<1>(a, false);
+  if (p->n_entries > 0) rc = vec ? run_phase<4>(a, false, mk) : run_phase<1>(a, false, mk);
   if (rc) return rc;
-  if (ev_mid && (e = hipEventRecord(ev_mid, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if (p->n_hub_rows > 0) rc = vec ? run_phase<4>(a, true) : run_phase<1>(a, true);
+  if (p->n_entries == 0) {  // nothing launched: keep the marks meaningful
+    if (ev_begin && (e = hipEventRecord(ev_begin, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if (ev_mid && (e = hipEventRecord(ev_mid, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  Marks none{};
+  if (p->n_hub_rows > 0) rc = vec ? run_phase<4>(a, true, none) : run_phase<1>(a, true, none);
   if (rc) return rc;
   if (ev_end && (e = hipEventRecord(ev_end, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   return AGCN_OK;

@@ -348,3 +348,23 @@ def test_plan_memory_reused_across_plans():
     p3 = _plan(g1)
     assert_plan_matches_oracle(p3, g1)
     p3.destroy()
+
+
+def test_long_hub_rows_column_ordered_launch():
+    """Hub rows of tens of thousands of nnz (many chunks each) take the
+    column-ordered launch path; Y must still match the oracle everywhere."""
+    rng = np.random.default_rng(41)
+    n = 60000
+    deg = rng.integers(1, 9, size=n)
+    hubs = rng.choice(n, size=24, replace=False)
+    deg[hubs] = rng.integers(20000, 50001, size=hubs.size)
+    g = graphgen.random_csr(n, n, deg, seed=42)
+    plan = _plan(g)
+    st = plan.stats
+    assert st.n_hub_chunks >= 8 * st.n_hub_rows      # the sorted-order path is taken
+    assert_plan_matches_oracle(plan, g)
+    for F in (16, 64, 100):
+        Yg = _spmm_check(plan, g, F, seed=F)
+    X = _dev(np.random.default_rng(1).standard_normal((n, 64)).astype(np.float32))
+    assert np.array_equal(plan.spmm(X).cpu().numpy(), plan.spmm(X).cpu().numpy())
+    plan.destroy()
