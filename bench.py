@@ -12,8 +12,12 @@ Extra keys: per-F execute timings, plan time, the roofline of the dominant
 kernel (measured with HIP events recorded by the library around that kernel
 in every timed step) and the single-threaded CPU oracle on a row sample.
 
+--variant warp_level / column_loop times one of the two ablation baselines of
+Table II instead (same workload, same step), for the ablation ratios.
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--F 16,32,...] [--no-cpu-baseline] [--copy-probe]
+                       [--F 16,32,...] [--variant block|warp_level|column_loop]
+                       [--no-cpu-baseline] [--copy-probe]
 """
 from __future__ import annotations
 
@@ -41,15 +45,21 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_bytes(st, F, n_ref):
+def kernel_bytes(st, F, n_ref, variant="block"):
     """Algorithmic HBM bytes of one launch of each execute kernel.
 
-    k_spmm:       8 nnz (sorted column index + value) + 16 per entry (metadata)
+    k_spmm (and k_spmm_colloop, same plan):
+                  8 nnz (sorted column index + value) + 16 per entry (metadata)
                   + 4 per non-hub row (perm) + 4 F per referenced X row (each once)
                   + 4 F per non-hub Y row + 4 F per hub chunk (partial row written)
     k_hub_reduce: 4 F per hub chunk (partial row read) + 4 F per hub row (Y)
                   + 8 per hub row (perm, chunk offset)
+    k_spmm_wl:    8 nnz + 16 per group (metadata) + 4 F per referenced X row
+                  + 4 F per Y row (rows cut by workgroups counted once)
+    k_wl_fixup:   8 per row (group offsets)
     """
+    if variant == "warp_level":
+        return 8 * st.nnz + 16 * st.n_entries + 4 * F * n_ref + 4 * F * st.n_rows, 8 * st.n_rows
     nonhub = st.n_rows - st.n_hub_rows
     k7 = (8 * st.nnz + 16 * st.n_entries + 4 * nonhub + 4 * F * n_ref + 4 * F * nonhub
           + 4 * F * st.n_hub_chunks)
@@ -57,12 +67,17 @@ def kernel_bytes(st, F, n_ref):
     return k7, k8
 
 
-def spmm_kernel_name(F):
+def spmm_kernel_name(F, variant="block"):
     """Instantiation the library picks for an aligned float32 X: 32-column
     slices (AGCN_SLICE_COLS overrides), lanes = slice columns / 4."""
+    if variant == "column_loop":
+        return "k_spmm_colloop"
     sc = int(os.environ.get("AGCN_SLICE_COLS", "32"))
     sc = sc if (4 <= sc <= 256 and sc % 4 == 0) else 32
     sc = min(F, sc)
+    if variant == "warp_level":
+        L = sc // 4 if F % 4 == 0 else min(F, sc)
+        return f"k_spmm_wl<{4 if F % 4 == 0 else 1}, {L if L in (4, 8) else 0}>"
     return f"k_spmm<4, {sc // 4}>" if F % 4 == 0 else f"k_spmm<1, {min(F, sc, 64)}>"
 
 
@@ -111,6 +126,8 @@ def main():
     ap.add_argument("--W", type=int, default=None)
     ap.add_argument("--Z", type=int, default=None)
     ap.add_argument("--H", type=int, default=None)
+    ap.add_argument("--variant", default="block", choices=["block", "warp_level", "column_loop"],
+                    help="ablation baselines of Table II (default: the block-level path)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-frac", type=float, default=0.4)
     ap.add_argument("--copy-probe", action="store_true",
@@ -140,6 +157,8 @@ def main():
         prm.max_wave_nzs = args.Z
     if args.H is not None:
         prm.hub_chunk_nnz = args.H
+    prm.flags = {"block": 0, "warp_level": agcn.AGCN_PLAN_WARP_LEVEL,
+                 "column_loop": agcn.AGCN_PLAN_COLUMN_LOOP}[args.variant]
 
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     d_rowptr, d_colidx, d_vals = t(g.rowptr), t(g.colidx), t(g.vals)
@@ -206,7 +225,7 @@ def main():
         k7 = np.array([events[k][F][0].elapsed_time(events[k][F][1]) for k in range(args.steps)])
         # hub-row reduction plus the launch gap up to the next marker
         k8 = np.array([events[k][F][1].elapsed_time(nxt(k)) for k in range(args.steps)])
-        b7, b8 = kernel_bytes(st, F, n_ref)
+        b7, b8 = kernel_bytes(st, F, n_ref, args.variant)
         ex_ms = float(np.mean(k7 + k8))
         exec_ms_sum += ex_ms
         fl = 2.0 * g.nnz * F
@@ -226,7 +245,7 @@ def main():
     # launch duration over that group's launches.
     groups = {}
     for F in Fs:
-        groups.setdefault(spmm_kernel_name(F), []).append(F)
+        groups.setdefault(spmm_kernel_name(F, args.variant), []).append(F)
     dom = max(groups, key=lambda k: sum(per_f[F]["spmm_ms"] for F in groups[k]))
     dom_F = groups[dom]
     mean_bytes = float(np.mean([per_f[F]["spmm_bytes"] for F in dom_F]))
@@ -263,13 +282,14 @@ def main():
         "config": {"workload": name, "n_rows": g.n_rows, "nnz": g.nnz, "F": Fs,
                    "max_block_waves": st.max_block_waves, "max_wave_nzs": st.max_wave_nzs,
                    "hub_chunk_nnz": st.hub_chunk_nnz, "n_entries": st.n_entries,
-                   "n_hub_rows": st.n_hub_rows, "parallelism": "single GPU"},
+                   "n_hub_rows": st.n_hub_rows, "variant": args.variant,
+                   "parallelism": "single GPU"},
         "plan_ms": round(plan_ms, 4),
         "spmm_only_gflops": round(flops_step / (exec_ms_sum * 1e-3) / 1e9, 2),
         "per_F": per_f,
         "roofline": roofline,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.variant == "block":
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(g, name, Fs, (st.max_block_waves, st.max_wave_nzs,
                                                          st.hub_chunk_nnz), args.cpu_frac)

@@ -53,7 +53,24 @@ enum agcn_status {
  * degree > deg_bound are cut into chunks of hub_chunk_nnz nnz (the paper
  * uses deg_bound; 0 selects deg_bound).
  * Limits: 1 <= W <= 32; 1 <= Z; W * Z <= 4096; 0 <= hub_chunk_nnz <= 4096.
- * flags must be 0 (reserved). */
+ * flags: 0 for the method itself, or one of the two baselines of the paper's
+ * ablation study (Table II):
+ *   AGCN_PLAN_WARP_LEVEL   no degree sort; each row in original order is cut
+ *                          into groups of at most Z nnz, one group per vwarp,
+ *                          W vwarps per workgroup regardless of row
+ *                          boundaries (the warp-level partition of Sec.
+ *                          III-C, panel (b)). Metadata per group:
+ *                          {row, first nnz, nnz count, 0}. Rows cut by a
+ *                          workgroup boundary are finished by a fixed-order
+ *                          reduction kernel (no atomics).
+ *   AGCN_PLAN_COLUMN_LOOP  the block-level partition, executed without the
+ *                          combined warp: each vwarp is one 64-lane wave,
+ *                          one float per lane, looping over F in strips of
+ *                          64 columns (the single-warp column traversal of
+ *                          Sec. III-D). */
+#define AGCN_PLAN_WARP_LEVEL 0x1u
+#define AGCN_PLAN_COLUMN_LOOP 0x2u
+
 typedef struct agcn_plan_params {
   int32_t max_block_waves;
   int32_t max_wave_nzs;
@@ -76,7 +93,7 @@ typedef struct agcn_plan_stats {
   int32_t max_deg;
   int32_t max_block_waves;
   int32_t max_wave_nzs;
-  int32_t reserved;
+  uint32_t flags;          /* the plan's AGCN_PLAN_* flags */
   size_t device_bytes;     /* device memory the plan holds */
 } agcn_plan_stats;
 
@@ -108,7 +125,9 @@ int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t n
                      const agcn_plan_params* params, void* stream);
 
 /* Device workspace agcn_spmm needs for feature width F: n_hub_chunks * F * 4
- * bytes (partial rows of the hub chunks; 0 when the plan has no hub rows). */
+ * bytes (partial rows of the hub chunks; 0 when the plan has no hub rows).
+ * For AGCN_PLAN_WARP_LEVEL plans: 2 * workgroups * F * 4 bytes (partial rows
+ * of the rows cut by workgroup boundaries). */
 int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes);
 
 /* Y = A X for one F (Sec. III-D). Asynchronous on `stream`.
@@ -124,7 +143,9 @@ int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes);
  * The plan is read-only here: concurrent calls on different streams are
  * safe when each has its own Y and ws. Must run on the plan's device.
  * Errors: INVALID_ARGUMENT (null plan or pointers, F < 1, ld < F, overlap,
- * missing workspace, wrong device), HIP. */
+ * missing workspace, wrong device), UNSUPPORTED (AGCN_PLAN_COLUMN_LOOP plans
+ * when W * F * 4 bytes of partial rows plus the staged entry exceed 64 KiB
+ * of LDS), HIP. */
 int agcn_spmm(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
               int64_t ldy, void* d_ws, void* stream);
 
@@ -146,7 +167,9 @@ int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* out);
  * h_vals_s[nnz] (the CSR with rows in sorted order), h_meta[4 * n_entries]
  * ({deg, loc, row, info} per entry: degree of the entry's rows; first nnz
  * in the sorted CSR; first sorted row; for deg <= deg_bound
- * warp_nzs << 16 | rows, else the chunk's nnz). */
+ * warp_nzs << 16 | rows, else the chunk's nnz). AGCN_PLAN_WARP_LEVEL plans:
+ * perm is the identity, the CSR is the input's, and h_meta holds one
+ * {row, first nnz, nnz count, 0} per group. */
 int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s,
                      int32_t* h_colidx_s, float* h_vals_s, int32_t* h_meta);
 

@@ -14,6 +14,7 @@ Functions and the passages of the paper they follow:
 * ``spmm``          Sec. II-A / II-B, the aggregation A' Y by definition
 * ``spmm_rows``     the same for selected rows
 * ``replay_meta``   Sec. III-C, last paragraph (warp workload from metadata)
+* ``warp_partition`` Sec. III-C panel (b): the warp-level partition baseline
 * ``plan``          degree_sort + relayout + partition in one call
 
 The readings taken where the paper is silent are listed in agcn_oracle.h.
@@ -63,6 +64,9 @@ def _load():
     lib.oracle_partition.argtypes = [ctypes.c_int32, _i32p, ctypes.c_int32, ctypes.c_int32,
                                      ctypes.c_int32, _i32p, ctypes.c_int64]
     lib.oracle_partition.restype = ctypes.c_int64
+    lib.oracle_warp_partition.argtypes = [ctypes.c_int32, _i32p, ctypes.c_int32, _i32p,
+                                          ctypes.c_int64]
+    lib.oracle_warp_partition.restype = ctypes.c_int64
     lib.oracle_spmm.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _i32p, _i32p,
                                 _f32p, _f32p, ctypes.c_int64, _f32p, ctypes.c_int64, _f64p, _f64p]
     lib.oracle_spmm.restype = ctypes.c_int
@@ -143,6 +147,20 @@ def partition(rowptr_s, max_block_warps: int, max_warp_nzs: int, hub_chunk_nnz: 
                                hub_chunk_nnz, _p(meta, _i32p), cnt)
     if got != cnt:
         raise OracleError("partition: count mismatch")
+    return meta[:cnt]
+
+
+def warp_partition(rowptr, max_warp_nzs: int):
+    """Warp-level partition: (n_groups, 4) int32 {row, first nnz, nnz count, 0}."""
+    rowptr = _i32(rowptr)
+    n = rowptr.size - 1
+    lib = _load()
+    cnt = lib.oracle_warp_partition(n, _p(rowptr, _i32p), max_warp_nzs, None, 0)
+    if cnt < 0:
+        raise OracleError("warp_partition: invalid input")
+    meta = np.zeros((max(cnt, 1), 4), dtype=np.int32)
+    if lib.oracle_warp_partition(n, _p(rowptr, _i32p), max_warp_nzs, _p(meta, _i32p), cnt) != cnt:
+        raise OracleError("warp_partition: count mismatch")
     return meta[:cnt]
 
 

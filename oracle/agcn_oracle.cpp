@@ -171,6 +171,30 @@ int64_t oracle_partition(int32_t n_rows, const int32_t* rowptr_s, int32_t max_bl
   return count;
 }
 
+// Sec. III-C, panel (b) of the metadata example: the warp-level partition.
+int64_t oracle_warp_partition(int32_t n_rows, const int32_t* rowptr, int32_t max_warp_nzs,
+                              int32_t* meta, int64_t cap) {
+  if (!rowptr_ok(n_rows, rowptr) || max_warp_nzs < 1) return -1;
+  int64_t count = 0;
+  for (int32_t row = 0; row < n_rows; ++row) {
+    const int64_t deg = rowptr[row + 1] - rowptr[row];
+    int64_t start = 0;
+    do {  // at least one group per row (R10w)
+      const int64_t len = std::min<int64_t>(max_warp_nzs, deg - start);
+      if (meta != nullptr) {
+        if (count >= cap) return -2;
+        meta[4 * count + 0] = row;
+        meta[4 * count + 1] = (int32_t)(rowptr[row] + start);
+        meta[4 * count + 2] = (int32_t)len;
+        meta[4 * count + 3] = 0;
+      }
+      ++count;
+      start += max_warp_nzs;
+    } while (start < deg);
+  }
+  return count;
+}
+
 // Sec. II-A/II-B: the aggregation A' Y by its definition.
 int oracle_spmm(int32_t n_rows, int32_t n_cols, int32_t F, const int32_t* rowptr,
                 const int32_t* colidx, const float* vals, const float* X, int64_t ldx,

@@ -71,6 +71,17 @@ int64_t oracle_partition(int32_t n_rows, const int32_t* rowptr_s,
                          int32_t max_block_warps, int32_t max_warp_nzs,
                          int32_t hub_chunk_nnz, int32_t* meta, int64_t cap);
 
+/* Warp-level partition, the baseline the paper compares block-level
+ * partitioning against (Sec. III-C metadata example, panel (b); Table II):
+ * no degree sort; each row, in original order, is cut into groups of at most
+ * max_warp_nzs consecutive nnz, one group per warp, metadata
+ * {row, first nnz, nnz count, 0} (96 bits padded to 128). Reading R10w: an
+ * empty row gets one group of length 0 so its output row is still written.
+ * meta = NULL counts only. Returns the number of groups, -1 on a bad
+ * argument, -2 if cap is too small. */
+int64_t oracle_warp_partition(int32_t n_rows, const int32_t* rowptr, int32_t max_warp_nzs,
+                              int32_t* meta, int64_t cap);
+
 /* Sec. II-A / II-B: Y = A X by its definition. For each row i and column k,
  * Y[i,k] = sum over e in [rowptr[i], rowptr[i+1]) of vals[e] * X[colidx[e], k],
  * summed in float64 in ascending e and rounded once to float32. Optional

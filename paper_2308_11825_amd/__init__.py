@@ -38,6 +38,9 @@ AGCN_ERR_UNSUPPORTED = 3
 AGCN_ERR_OUT_OF_MEMORY = 4
 AGCN_ERR_HIP = 5
 
+AGCN_PLAN_WARP_LEVEL = 0x1
+AGCN_PLAN_COLUMN_LOOP = 0x2
+
 
 class PlanParams(ctypes.Structure):
     _fields_ = [("max_block_waves", ctypes.c_int32), ("max_wave_nzs", ctypes.c_int32),
@@ -51,10 +54,10 @@ class PlanStats(ctypes.Structure):
                 ("hub_first_row", ctypes.c_int32), ("deg_bound", ctypes.c_int32),
                 ("hub_chunk_nnz", ctypes.c_int32), ("max_deg", ctypes.c_int32),
                 ("max_block_waves", ctypes.c_int32), ("max_wave_nzs", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("device_bytes", ctypes.c_size_t)]
+                ("flags", ctypes.c_uint32), ("device_bytes", ctypes.c_size_t)]
 
     def as_dict(self):
-        return {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        return {k: getattr(self, k) for k, _ in self._fields_}
 
 
 class AgcnError(RuntimeError):
@@ -222,7 +225,7 @@ class Plan:
     """
 
     def __init__(self, rowptr, colidx, vals, n_cols=None, max_block_waves=None,
-                 max_wave_nzs=None, hub_chunk_nnz=None, stream=None):
+                 max_wave_nzs=None, hub_chunk_nnz=None, flags=0, stream=None):
         import torch
         for name, t, dt in (("rowptr", rowptr, torch.int32), ("colidx", colidx, torch.int32),
                             ("vals", vals, torch.float32)):
@@ -243,6 +246,7 @@ class Plan:
             prm.max_wave_nzs = max_wave_nzs
         if hub_chunk_nnz is not None:
             prm.hub_chunk_nnz = hub_chunk_nnz
+        prm.flags = flags
         self.params = prm
         self._handle = None
         with torch.cuda.device(self.device):

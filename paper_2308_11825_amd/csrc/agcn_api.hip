@@ -193,7 +193,9 @@ int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t n
     return fail(AGCN_ERR_INVALID_ARGUMENT, "colidx or vals is NULL");
   agcn_plan_params prm;
   if (params == nullptr) agcn_default_params(&prm); else prm = *params;
-  if (prm.flags != 0) return fail(AGCN_ERR_INVALID_ARGUMENT, "flags must be 0");
+  if (prm.flags != 0 && prm.flags != AGCN_PLAN_WARP_LEVEL && prm.flags != AGCN_PLAN_COLUMN_LOOP)
+    return fail(AGCN_ERR_INVALID_ARGUMENT,
+                "flags must be 0, AGCN_PLAN_WARP_LEVEL or AGCN_PLAN_COLUMN_LOOP");
   if (prm.max_block_waves < 1 || prm.max_block_waves > agcn::kMaxBlockWaves)
     return fail(AGCN_ERR_INVALID_ARGUMENT, "max_block_waves must be in [1, 32]");
   if (prm.max_wave_nzs < 1 ||
@@ -223,6 +225,7 @@ int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t n
   p->Z = prm.max_wave_nzs;
   p->deg_bound = deg_bound;
   p->H = H;
+  p->flags = prm.flags;
   int rc;
   try {
     rc = agcn::build_plan(p, d_rowptr, d_colidx, d_vals, static_cast<hipStream_t>(stream));
@@ -244,7 +247,10 @@ int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t n
 int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes) {
   if (plan == nullptr || bytes == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "NULL argument");
   if (F < 1) return fail(AGCN_ERR_INVALID_ARGUMENT, "F must be >= 1");
-  const int64_t chunks = plan->n_hub_rows > 0 ? (int64_t)plan->n_entries - plan->hub_first_entry : 0;
+  const int64_t chunks =
+      plan->flags & AGCN_PLAN_WARP_LEVEL
+          ? 2 * agcn::warp_level_blocks(plan)
+          : (plan->n_hub_rows > 0 ? (int64_t)plan->n_entries - plan->hub_first_entry : 0);
   *bytes = (size_t)chunks * (size_t)F * sizeof(float);
   return AGCN_OK;
 }
@@ -301,6 +307,7 @@ int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* s) {
   s->max_deg = plan->max_deg;
   s->max_block_waves = plan->W;
   s->max_wave_nzs = plan->Z;
+  s->flags = plan->flags;
   s->device_bytes = plan->bytes;
   return AGCN_OK;
 }

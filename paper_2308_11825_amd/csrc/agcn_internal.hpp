@@ -43,6 +43,7 @@ struct agcn_plan {
   int32_t n_rows = 0, n_cols = 0;
   int64_t nnz = 0;
   int32_t W = 0, Z = 0, deg_bound = 0, H = 0;
+  uint32_t flags = 0;  // AGCN_PLAN_* (0: the block-level method)
   int32_t n_entries = 0, hub_first_entry = 0, n_hub_rows = 0, hub_first_row = 0, max_deg = 0;
   void* base = nullptr;  // single device allocation holding everything below
   size_t bytes = 0;
@@ -53,6 +54,7 @@ struct agcn_plan {
   int4* meta = nullptr;             // [entries upper bound] {deg, loc, row, info}
   int32_t* hub_chunk_off = nullptr; // [hub rows upper bound + 1] first chunk of each hub row
   int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
+  int32_t* group_off = nullptr;     // warp-level plans: [n_rows + 1] first group of each row
   hipEvent_t ready = nullptr;       // recorded after the launch order is built
 };
 
@@ -63,9 +65,14 @@ void set_error(const std::string& msg);
 int fail(int status, const std::string& msg);
 int hip_fail(hipError_t e, const char* what);
 
-// Plan construction (agcn_plan.hip).
+// Plan construction (agcn_plan.hip). build_plan dispatches on p->flags.
 int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
                const float* d_vals, hipStream_t stream);
+
+// Workgroups of a warp-level plan (W groups each).
+inline int64_t warp_level_blocks(const agcn_plan* p) {
+  return p->W > 0 ? (p->n_entries + p->W - 1) / p->W : 0;
+}
 
 // Execute (agcn_spmm.hip).
 int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,

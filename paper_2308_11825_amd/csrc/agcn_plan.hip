@@ -680,6 +680,82 @@ __global__ __launch_bounds__(kThreads) void k_order_fill(int32_t* __restrict__ o
     order[i] = hub_first - 1 - (int32_t)(i - n_chunks);
 }
 
+// --- warp-level partition (the baseline of the paper's Table II) -----------
+
+// Groups per row: ceil(deg / Z), at least one so an empty row is still written.
+__global__ __launch_bounds__(kThreads) void k_wl_groups(int32_t n, const int32_t* __restrict__ deg,
+                                                        int32_t Z, int32_t* __restrict__ ng,
+                                                        const uint32_t* err) {
+  if (failed(err)) return;
+  const int64_t r = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (r >= n) return;
+  const int32_t d = deg[r];
+  ng[r] = d > 0 ? (d + Z - 1) / Z : 1;
+}
+
+// Unsorted copy of the CSR (checked columns) and the identity permutation.
+__global__ __launch_bounds__(kThreads) void k_wl_copy(int32_t n, int64_t nnz, int32_t n_cols,
+                                                      const int32_t* __restrict__ rowptr,
+                                                      const int32_t* __restrict__ colidx,
+                                                      const float* __restrict__ vals,
+                                                      int32_t* __restrict__ perm,
+                                                      int32_t* __restrict__ rowptr_s,
+                                                      int32_t* __restrict__ colidx_s,
+                                                      float* __restrict__ vals_s, uint32_t* err) {
+  if (failed(err)) return;
+  uint32_t bad = 0;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < nnz || i <= n;
+       i += (int64_t)gridDim.x * kThreads) {
+    if (i < nnz) {
+      const int32_t c = colidx[i];
+      if ((uint32_t)c >= (uint32_t)n_cols) bad = kErrColumn;
+      colidx_s[i] = c;
+      vals_s[i] = vals[i];
+    }
+    if (i <= n) rowptr_s[i] = rowptr[i];
+    if (i < n) perm[i] = (int32_t)i;
+  }
+  if (bad) atomicOr(err, bad);
+}
+
+// Group g: row r = the last row whose first group is <= g; its j-th group
+// covers nnz [rowptr[r] + j Z, + min(Z, deg - j Z)).
+__global__ __launch_bounds__(kThreads) void k_wl_fill(int32_t n, const int32_t* __restrict__ rowptr,
+                                                      const int32_t* __restrict__ goff, int32_t Z,
+                                                      int4* __restrict__ meta, int64_t cap,
+                                                      const uint32_t* err) {
+  if (failed(err)) return;
+  const int64_t total = goff[n];
+  for (int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x; g < total && g < cap;
+       g += (int64_t)gridDim.x * kThreads) {
+    int32_t a = 0, b = n - 1;
+    while (a < b) {
+      const int32_t mid = (int32_t)(((int64_t)a + b + 1) >> 1);
+      if (goff[mid] <= g) a = mid; else b = mid - 1;
+    }
+    const int32_t j = (int32_t)(g - goff[a]);
+    const int32_t d = rowptr[a + 1] - rowptr[a];
+    const int32_t left = d - j * Z;
+    meta[g] = make_int4(a, rowptr[a] + j * Z, left < Z ? left : Z, 0);
+  }
+}
+
+__global__ void k_wl_summary(int32_t n, const int32_t* __restrict__ goff,
+                             const int32_t* __restrict__ dmax, PlanSummary* sum,
+                             const uint32_t* err) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const uint32_t e = err[0];
+  sum->err = e;
+  if (!e) {
+    sum->n_entries = goff[n];
+    sum->hub_first_entry = goff[n];
+    sum->n_hub_rows = 0;
+    sum->hub_first_row = n;
+    sum->max_deg = dmax[0];
+  }
+  __threadfence_system();
+}
+
 // ---------------------------------------------------------------------------
 
 inline unsigned grid_for(int64_t work, int per_block) {
@@ -780,8 +856,86 @@ struct Layout {
 
 }  // namespace
 
-int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
-               const float* d_vals, hipStream_t st) {
+namespace {
+
+// Warp-level plan: validation, an unsorted CSR copy, one group per <= Z nnz.
+int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
+                          const float* d_vals, hipStream_t st) {
+  const int64_t n = p->n_rows, nnz = p->nnz;
+  const int32_t Z = p->Z;
+  const int64_t g_ub = n + nnz / Z + 1;
+  const int64_t n_partials = ceil_div64(n + 1, kScanBlock) + 1;
+  if (g_ub >= INT32_MAX) return fail(AGCN_ERR_UNSUPPORTED, "too many warp groups for int32 indexing");
+  Layout L;
+  const size_t o_perm = L.take(4 * n);
+  const size_t o_rowptr_s = L.take(4 * (n + 1));
+  const size_t o_colidx_s = L.take(4 * nnz);
+  const size_t o_vals_s = L.take(4 * nnz);
+  const size_t o_meta = L.take(16 * g_ub);
+  const size_t o_goff = L.take(4 * (n + 1));
+  const size_t o_deg = L.take(4 * n);
+  const size_t o_ng = L.take(4 * n);
+  const size_t o_bmax = L.take(4 * (ceil_div64(n, kThreads) + 1));
+  const size_t o_partials = L.take(4 * n_partials);
+  const size_t o_err = L.take(64);
+  const size_t o_dmax = L.take(64);
+  void* base = nullptr;
+  size_t got = 0;
+  int rc = device_alloc(p->device, L.off, &base, &got);
+  if (rc) return rc;
+  char* b = static_cast<char*>(base);
+  p->base = base;
+  p->bytes = got;
+  p->perm = reinterpret_cast<int32_t*>(b + o_perm);
+  p->rowptr_s = reinterpret_cast<int32_t*>(b + o_rowptr_s);
+  p->colidx_s = reinterpret_cast<int32_t*>(b + o_colidx_s);
+  p->vals_s = reinterpret_cast<float*>(b + o_vals_s);
+  p->meta = reinterpret_cast<int4*>(b + o_meta);
+  p->group_off = reinterpret_cast<int32_t*>(b + o_goff);
+  int32_t* deg = reinterpret_cast<int32_t*>(b + o_deg);
+  int32_t* ng = reinterpret_cast<int32_t*>(b + o_ng);
+  int32_t* bmax = reinterpret_cast<int32_t*>(b + o_bmax);
+  int32_t* partials = reinterpret_cast<int32_t*>(b + o_partials);
+  uint32_t* err = reinterpret_cast<uint32_t*>(b + o_err);
+  int32_t* dmax = reinterpret_cast<int32_t*>(b + o_dmax);
+  PlanSummary* dsum = nullptr;
+  PlanSummary* hs = pinned_summary(&dsum);
+  if (hs == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "pinned host buffer allocation failed");
+  *hs = PlanSummary{};
+  const int64_t nb = ceil_div64(n, kThreads);
+  k_init<<<1, 64, 0, st>>>(err, dmax);
+  if (n > 0) {
+    k_degree<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err, bmax);
+    k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, (int32_t)nb, dmax, dsum);
+    k_wl_groups<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, deg, Z, ng, err);
+  }
+  const unsigned cgrid = (unsigned)std::min<int64_t>(grid_for(std::max(nnz, n + 1), kThreads), 65536);
+  k_wl_copy<<<cgrid, kThreads, 0, st>>>((int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals,
+                                        p->perm, p->rowptr_s, p->colidx_s, p->vals_s, err);
+  if ((rc = check_launch("warp-level plan"))) return rc;
+  if ((rc = scan_exclusive(ng, n, p->group_off, p->group_off + n, partials, err, st))) return rc;
+  if (n > 0) {
+    const unsigned fgrid = (unsigned)std::min<int64_t>(grid_for(g_ub, kThreads), 16384);
+    k_wl_fill<<<fgrid, kThreads, 0, st>>>((int32_t)n, d_rowptr, p->group_off, Z, p->meta, g_ub, err);
+  }
+  k_wl_summary<<<1, 64, 0, st>>>((int32_t)n, p->group_off, dmax, dsum, err);
+  if ((rc = check_launch("warp-level plan"))) return rc;
+  hipError_t he = hipStreamSynchronize(st);
+  if (he != hipSuccess) return hip_fail(he, "hipStreamSynchronize(plan)");
+  if (hs->err) {
+    if (hs->err & kErrInternal) return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
+    return fail(AGCN_ERR_INVALID_INPUT, "invalid CSR (row pointer or column index)");
+  }
+  p->n_entries = hs->n_entries;
+  p->hub_first_entry = hs->hub_first_entry;
+  p->n_hub_rows = 0;
+  p->hub_first_row = (int32_t)n;
+  p->max_deg = hs->max_deg;
+  return AGCN_OK;
+}
+
+int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
+                     const float* d_vals, hipStream_t st) {
   const int64_t n = p->n_rows, nnz = p->nnz;
   const int32_t W = p->W, Z = p->Z, DB = p->deg_bound, H = p->H;
   const int64_t ent_ub = n + nnz / H + 1;         // every entry holds a row or a full chunk
@@ -959,6 +1113,14 @@ int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
     return hip_fail(he, "hipEventCreate(plan ready)");
   if ((he = hipEventRecord(p->ready, st)) != hipSuccess) return hip_fail(he, "hipEventRecord(plan ready)");
   return AGCN_OK;
+}
+
+}  // namespace
+
+int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
+               const float* d_vals, hipStream_t st) {
+  return (p->flags & AGCN_PLAN_WARP_LEVEL) ? build_plan_warp_level(p, d_rowptr, d_colidx, d_vals, st)
+                                          : build_plan_block(p, d_rowptr, d_colidx, d_vals, st);
 }
 
 }  // namespace agcn

@@ -252,6 +252,189 @@ __global__ __launch_bounds__(1024) void k_hub_reduce(const int32_t* __restrict__
   }
 }
 
+// --- ablation baselines (the paper's Table II) ------------------------------
+
+// Warp-level partition: workgroup b runs groups [b W, b W + W); vwarp v takes
+// group b W + v (one row's slice of <= Z nnz). Consecutive vwarps of the same
+// row add their partials in order. A row cut by the workgroup's start or end
+// leaves its partial in ws[b][0] (cut at the start) or ws[b][1] (cut only at
+// the end); k_wl_fixup finishes those rows in workgroup order.
+template <int VW, int LT>
+__global__ __launch_bounds__(1024) void k_spmm_wl(
+    const int4* __restrict__ meta, int32_t n_groups, int32_t W,
+    const int32_t* __restrict__ colidx_s, const float* __restrict__ vals_s,
+    const float* __restrict__ X, int64_t ldx, float* __restrict__ Y, int64_t ldy,
+    float* __restrict__ ws, int32_t F, int32_t col_base, int32_t slice_cols, int32_t L_rt,
+    int32_t rounds, int32_t cap_pad) {
+  using V = typename VecOf<VW>::T;
+  const int L = LT > 0 ? LT : L_rt;
+  extern __shared__ float smem[];
+  int32_t* s_col = reinterpret_cast<int32_t*>(smem);
+  float* s_val = smem + cap_pad;
+  V* s_part = reinterpret_cast<V*>(smem + 2 * cap_pad);
+  __shared__ int4 s_meta[kMaxBlockWaves];
+  __shared__ int32_t s_prev_row, s_next_row;
+  const int T = blockDim.x;
+  const int32_t g0 = (int32_t)blockIdx.x * W;
+  const int32_t nv = min(W, n_groups - g0);
+  const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
+  if (threadIdx.x < nv) s_meta[threadIdx.x] = meta[g0 + threadIdx.x];
+  if (threadIdx.x == kMaxBlockWaves) s_prev_row = g0 > 0 ? meta[g0 - 1].x : -1;
+  if (threadIdx.x == kMaxBlockWaves + 1) s_next_row = g0 + nv < n_groups ? meta[g0 + nv].x : -1;
+  __syncthreads();
+  const int32_t base = s_meta[0].y;
+  const int32_t n_e = s_meta[nv - 1].y + s_meta[nv - 1].z - base;  // groups are contiguous
+  for (int i0 = 0; i0 < n_e; i0 += T * kStageUnroll) {
+    int32_t c[kStageUnroll];
+    float v[kStageUnroll];
+#pragma unroll
+    for (int u = 0; u < kStageUnroll; ++u) {
+      const int i = i0 + u * T + threadIdx.x;
+      if (i < n_e) {
+        c[u] = __builtin_nontemporal_load(colidx_s + base + i);
+        v[u] = __builtin_nontemporal_load(vals_s + base + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kStageUnroll; ++u) {
+      const int i = i0 + u * T + threadIdx.x;
+      if (i < n_e) {
+        s_col[pad_idx(i)] = c[u];
+        s_val[pad_idx(i)] = v[u];
+      }
+    }
+  }
+  __syncthreads();
+  const V* __restrict__ Xv = reinterpret_cast<const V*>(X + col0);
+  const int64_t ldxv = ldx / VW;
+  for (int k = 0; k < rounds; ++k) {
+    const int vt = threadIdx.x + k * T;
+    const int v = vt / L, l = vt - v * L;
+    if (v < nv)
+      s_part[part_idx<VW>(v * L + l)] =
+          gather_row<VW>(s_col, s_val, s_meta[v].y - base, s_meta[v].z, Xv, ldxv, l);
+  }
+  __syncthreads();
+  for (int k = 0; k < rounds; ++k) {
+    const int vt = threadIdx.x + k * T;
+    const int v = vt / L, l = vt - v * L;
+    if (v < nv && (v == 0 || s_meta[v].x != s_meta[v - 1].x)) {
+      const int32_t row = s_meta[v].x;
+      int e = v;
+      V sum = s_part[part_idx<VW>(v * L + l)];
+      while (e + 1 < nv && s_meta[e + 1].x == row) {
+        ++e;
+        sum += s_part[part_idx<VW>(e * L + l)];
+      }
+      const bool start_cut = v == 0 && s_prev_row == row;
+      const bool end_cut = e == nv - 1 && s_next_row == row;
+      if (start_cut || end_cut) {
+        V* wr = reinterpret_cast<V*>(ws + ((int64_t)blockIdx.x * 2 + (start_cut ? 0 : 1)) * F + col0);
+        wr[l] = sum;
+      } else {
+        V* yr = reinterpret_cast<V*>(Y + (int64_t)row * ldy + col0);
+        __builtin_nontemporal_store(sum, yr + l);
+      }
+    }
+  }
+}
+
+// Rows cut by workgroup boundaries: partials ws[b0][1], ws[b0+1][0], ...,
+// ws[b1][0] added in order, in runs of 16 (bounded rounding depth).
+template <int VW>
+__global__ __launch_bounds__(256) void k_wl_fixup(const int32_t* __restrict__ goff, int32_t n_rows,
+                                                  int32_t W, const float* __restrict__ ws, int32_t F,
+                                                  float* __restrict__ Y, int64_t ldy,
+                                                  int32_t col_base, int32_t slice_cols, int32_t L) {
+  using V = typename VecOf<VW>::T;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t r = t / L;
+  const int l = (int)(t - r * L);
+  if (r >= n_rows) return;
+  const int32_t b0 = goff[r] / W, b1 = (goff[r + 1] - 1) / W;
+  if (b0 == b1) return;
+  const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
+  auto part = [&](int32_t b) {
+    const int slot = b == b0 ? 1 : 0;
+    return reinterpret_cast<const V*>(ws + ((int64_t)b * 2 + slot) * F + col0)[l];
+  };
+  V total = V(0.0f);
+  for (int32_t b = b0; b <= b1; b += 16) {
+    V run = part(b);
+    const int32_t e = b + 16 <= b1 + 1 ? b + 16 : b1 + 1;
+    for (int32_t q = b + 1; q < e; ++q) run += part(q);
+    total = b == b0 ? run : total + run;
+  }
+  V* yr = reinterpret_cast<V*>(Y + r * ldy + col0);
+  __builtin_nontemporal_store(total, yr + l);
+}
+
+// Block-level partition without the combined warp: every vwarp is one
+// 64-lane wave, one float per lane, and loops over F in strips of 64 columns.
+// Split rows and hub chunks keep one F-wide partial per vwarp in LDS.
+__global__ __launch_bounds__(1024) void k_spmm_colloop(
+    const int4* __restrict__ meta, const int32_t* __restrict__ order, int32_t hub_first_entry,
+    int32_t deg_bound, int32_t W, const int32_t* __restrict__ colidx_s,
+    const float* __restrict__ vals_s, const int32_t* __restrict__ perm, const float* __restrict__ X,
+    int64_t ldx, float* __restrict__ Y, int64_t ldy, float* __restrict__ ws, int32_t F,
+    int32_t rounds, int32_t cap_pad) {
+  extern __shared__ float smem[];
+  int32_t* s_col = reinterpret_cast<int32_t*>(smem);
+  float* s_val = smem + cap_pad;
+  float* s_part = smem + 2 * cap_pad;  // [W][F]
+  const int T = blockDim.x;
+  const int32_t b = order[blockIdx.x];
+  const int4 m = meta[b];
+  const int32_t deg = m.x, loc = m.y, row = m.z, info = m.w;
+  const bool hub = deg > deg_bound;
+  const int32_t rows = info & 0xFFFF;
+  const int32_t n_e = hub ? info : rows * deg;
+  for (int i = threadIdx.x; i < n_e; i += T) {
+    s_col[pad_idx(i)] = __builtin_nontemporal_load(colidx_s + loc + i);
+    s_val[pad_idx(i)] = __builtin_nontemporal_load(vals_s + loc + i);
+  }
+  __syncthreads();
+  const int32_t wn = (int32_t)((uint32_t)info >> 16);
+  const int32_t wpr = hub ? W : (deg > 0 ? (deg + wn - 1) / wn : 1);
+  const int32_t nv = hub ? W : rows * wpr;
+  const int32_t sl = hub ? (n_e + W - 1) / W : 0;
+  for (int k = 0; k < rounds; ++k) {
+    const int vt = threadIdx.x + k * T;
+    const int v = vt >> 6, lane = vt & 63;
+    if (v >= nv) continue;
+    int s0, len, rl = 0;
+    if (hub) {
+      s0 = v * sl;
+      const int left = n_e - s0;
+      len = left < 0 ? 0 : (left < sl ? left : sl);
+    } else {
+      rl = v / wpr;
+      const int part = v - rl * wpr;
+      s0 = rl * deg + part * wn;
+      len = deg > 0 ? min(wn, deg - part * wn) : 0;
+    }
+    for (int c = lane; c < F; c += 64) {  // the single-warp column loop
+      const float acc = gather_row<1>(s_col, s_val, s0, len, X, ldx, c);
+      if (!hub && wpr == 1)
+        __builtin_nontemporal_store(acc, Y + (int64_t)perm[row + rl] * ldy + c);
+      else
+        s_part[(int64_t)v * F + c] = acc;
+    }
+  }
+  if (hub || wpr > 1) {
+    __syncthreads();
+    const int n_out = hub ? 1 : rows;
+    for (int64_t i = threadIdx.x; i < (int64_t)n_out * F; i += T) {
+      const int r = (int)(i / F), c = (int)(i - (int64_t)r * F);
+      const int first = hub ? 0 : r * wpr;
+      float sum = s_part[(int64_t)first * F + c];
+      for (int q = 1; q < wpr; ++q) sum += s_part[(int64_t)(first + q) * F + c];
+      if (hub) ws[(int64_t)(b - hub_first_entry) * F + c] = sum;
+      else __builtin_nontemporal_store(sum, Y + (int64_t)perm[row + r] * ldy + c);
+    }
+  }
+}
+
 inline int round_up(int a, int b) { return (a + b - 1) / b * b; }
 
 // LDS words for the staged (column, value) pairs of the largest entry.
@@ -384,6 +567,91 @@ size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz) {
   return (size_t)2 * stage_words(max_entry_nnz) * 4 + (size_t)part_floats(4, W, 64) * 4;
 }
 
+namespace {
+
+template <int VW, int LT>
+void launch_wl(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols, Marks& mk,
+               bool last_part) {
+  const agcn_plan* p = a.p;
+  const int cap_pad = stage_words(p->W * p->Z);
+  const int want = p->W * L;
+  const int T = std::min(1024, std::max(64, round_up(want, 64)));
+  const int rounds = (want + T - 1) / T;
+  const size_t lds = (size_t)2 * cap_pad * 4 + (size_t)part_floats(VW, p->W, L) * 4;
+  dim3 grid((unsigned)warp_level_blocks(p), (unsigned)n_slices);
+  const hipEvent_t stop = last_part ? mk.stop : nullptr;
+  hipExtLaunchKernelGGL(k_spmm_wl<VW, LT>, grid, dim3(T), (uint32_t)lds, a.st, mk.start, stop, 0,
+                        p->meta, p->n_entries, p->W, p->colidx_s, p->vals_s, a.X, a.ldx, a.Y,
+                        a.ldy, a.ws, a.F, col_base, slice_cols, L, rounds, cap_pad);
+  mk.start = nullptr;
+}
+
+template <int VW>
+int run_warp_level(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
+  const agcn_plan* p = a.p;
+  const int sc_max = VW == 4 ? slice_cols_setting() : std::min(64, slice_cols_setting());
+  const int sc = std::min(a.F, sc_max);
+  const int n_full = a.F / sc;
+  const int tail = a.F - n_full * sc;
+  for (int part = 0; part < 2; ++part) {
+    const int n_slices = part == 0 ? n_full : (tail > 0 ? 1 : 0);
+    if (n_slices == 0) continue;
+    const int L = (part == 0 ? sc : tail) / VW;
+    const int col_base = part == 0 ? 0 : n_full * sc;
+    const bool last_part = part == 1 || tail == 0;
+    switch (L) {
+      case 4: launch_wl<VW, 4>(a, L, n_slices, col_base, sc, mk, last_part); break;
+      case 8: launch_wl<VW, 8>(a, L, n_slices, col_base, sc, mk, last_part); break;
+      default: launch_wl<VW, 0>(a, L, n_slices, col_base, sc, mk, last_part); break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "k_spmm_wl launch");
+    const int rows_per_block = std::max(1, 256 / L);
+    dim3 fgrid((unsigned)ceil_div64(p->n_rows, rows_per_block), (unsigned)n_slices);
+    k_wl_fixup<VW><<<fgrid, rows_per_block * L, 0, a.st>>>(p->group_off, p->n_rows, p->W, a.ws, a.F,
+                                                           a.Y, a.ldy, col_base, sc, L);
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_wl_fixup launch");
+  }
+  hipError_t e;
+  if (ev_end && (e = hipEventRecord(ev_end, a.st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  return AGCN_OK;
+}
+
+int run_colloop(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
+  const agcn_plan* p = a.p;
+  const int cap_pad = stage_words(std::max(p->deg_bound, p->H));
+  const size_t lds = (size_t)2 * cap_pad * 4 + (size_t)p->W * a.F * 4;
+  if (lds > 65536)
+    return fail(AGCN_ERR_UNSUPPORTED, "column-loop execution needs W * F * 4 + staging <= 64 KiB of LDS");
+  const int want = p->W * 64;
+  const int T = std::min(1024, want);
+  const int rounds = (want + T - 1) / T;
+  hipError_t e;
+  hipExtLaunchKernelGGL(k_spmm_colloop, dim3((unsigned)p->n_entries), dim3(T), (uint32_t)lds, a.st,
+                        mk.start, mk.stop, 0, p->meta, p->order, p->hub_first_entry, p->deg_bound,
+                        p->W, p->colidx_s, p->vals_s, p->perm, a.X, a.ldx, a.Y, a.ldy, a.ws, a.F,
+                        rounds, cap_pad);
+  if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_spmm_colloop launch");
+  if (p->n_hub_rows > 0) {
+    const int L = std::min(64, a.F);
+    int G = 1;
+    while (G < 16 && 2 * G * L <= 1024) G *= 2;
+    const int n_slices = (int)ceil_div64(a.F, 64);
+    // one launch per 64-column strip (the last may be narrower)
+    for (int s = 0; s < n_slices; ++s) {
+      const int cols = std::min(64, a.F - s * 64);
+      k_hub_reduce<1><<<dim3((unsigned)p->n_hub_rows, 1), round_up(G * cols, 64),
+                        (size_t)G * cols * 4, a.st>>>(p->hub_chunk_off, p->hub_first_row, p->perm,
+                                                      a.ws, a.F, a.Y, a.ldy, s * 64, 64, cols, G);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_hub_reduce launch");
+  }
+  if (ev_end && (e = hipEventRecord(ev_end, a.st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  return AGCN_OK;
+}
+
+}  // namespace
+
 int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,
              float* ws, hipStream_t st, hipEvent_t ev_begin, hipEvent_t ev_mid,
              hipEvent_t ev_end) {
@@ -395,14 +663,17 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
   // stream after its host synchronisation; order this stream after them.
   if (p->ready && (e = hipStreamWaitEvent(st, p->ready, 0)) != hipSuccess)
     return hip_fail(e, "hipStreamWaitEvent(plan ready)");
-  Marks mk{ev_begin, ev_mid};
-  int rc = AGCN_OK;
-  if (p->n_entries > 0) rc = vec ? run_phase<4>(a, false, mk) : run_phase<1>(a, false, mk);
-  if (rc) return rc;
-  if (p->n_entries == 0) {  // nothing launched: keep the marks meaningful
-    if (ev_begin && (e = hipEventRecord(ev_begin, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    if (ev_mid && (e = hipEventRecord(ev_mid, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if (p->n_entries == 0) {  // no rows (hub rows need entries): keep the marks meaningful
+    for (hipEvent_t ev : {ev_begin, ev_mid, ev_end})
+      if (ev && (e = hipEventRecord(ev, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    return AGCN_OK;
   }
+  Marks mk{ev_begin, ev_mid};
+  if (p->flags & AGCN_PLAN_WARP_LEVEL)
+    return vec ? run_warp_level<4>(a, mk, ev_end) : run_warp_level<1>(a, mk, ev_end);
+  if (p->flags & AGCN_PLAN_COLUMN_LOOP) return run_colloop(a, mk, ev_end);
+  int rc = vec ? run_phase<4>(a, false, mk) : run_phase<1>(a, false, mk);
+  if (rc) return rc;
   Marks none{};
   if (p->n_hub_rows > 0) rc = vec ? run_phase<4>(a, true, none) : run_phase<1>(a, true, none);
   if (rc) return rc;

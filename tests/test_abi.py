@@ -82,7 +82,8 @@ def _params(W=16, Z=32, H=0, flags=0):
     (dict(params=_params(W=16, Z=257)), 1),
     (dict(params=_params(H=-1)), 1),
     (dict(params=_params(H=4097)), 1),
-    (dict(params=_params(flags=1)), 1),
+    (dict(params=_params(flags=4)), 1),             # unknown flag
+    (dict(params=_params(flags=3)), 1),             # the two ablations are exclusive
     (dict(params=_params(W=32, Z=128)), 1),         # needs > 64 KiB of LDS
     (dict(n_rows=2**31 - 2, nnz=2**31 - 1, params=_params(H=1)), 3),
 ])

@@ -389,3 +389,35 @@ def test_partition_rejects_bad_input():
         oracle.partition(np.array([0, 5, 3], np.int32), 16, 32)
     with pytest.raises(oracle.OracleError):
         oracle.partition(np.array([0, 1], np.int32), 0, 32)
+
+
+# --------------------------------------------------------------------------
+# Warp-level partition (the baseline of Table II)
+# --------------------------------------------------------------------------
+
+def test_warp_partition_worked_example():
+    g = _golden("worked_example_w2_z2.json")
+    meta = oracle.warp_partition(np.array(g["rowptr"], np.int32), g["max_warp_nzs"])
+    assert meta.tolist() == g["expected_warp_level_meta"]
+    assert len(meta) == g["warp_level_warps"]
+
+
+@pytest.mark.parametrize("Z", [1, 2, 7, 32, 64])
+def test_warp_partition_covers_every_nnz_once(Z):
+    g = _mixed_graph(50 + Z, n=300, dupes=True)
+    meta = oracle.warp_partition(g.rowptr, Z)
+    deg = g.degrees
+    assert len(meta) == int(np.maximum(1, -(-deg // Z)).sum())
+    cover = np.zeros(g.nnz, np.int64)
+    prev = (-1, -1)
+    for row, loc, ln, pad in meta.tolist():
+        assert pad == 0 and 0 <= ln <= Z
+        assert g.rowptr[row] <= loc and loc + ln <= g.rowptr[row + 1]
+        assert (row, loc) > prev
+        prev = (row, loc)
+        cover[loc:loc + ln] += 1
+        if ln == 0:
+            assert deg[row] == 0
+    assert np.all(cover == 1)
+    # every row, empty or not, owns at least one group
+    assert set(meta[:, 0].tolist()) == set(range(g.n_rows))
