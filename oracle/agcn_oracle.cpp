@@ -179,7 +179,7 @@ int64_t oracle_warp_partition(int32_t n_rows, const int32_t* rowptr, int32_t max
   for (int32_t row = 0; row < n_rows; ++row) {
     const int64_t deg = rowptr[row + 1] - rowptr[row];
     int64_t start = 0;
-    do {  // at least one group per row (R10w)
+    do {  // at least one group per row (R14)
       const int64_t len = std::min<int64_t>(max_warp_nzs, deg - start);
       if (meta != nullptr) {
         if (count >= cap) return -2;

@@ -75,7 +75,7 @@ int64_t oracle_partition(int32_t n_rows, const int32_t* rowptr_s,
  * partitioning against (Sec. III-C metadata example, panel (b); Table II):
  * no degree sort; each row, in original order, is cut into groups of at most
  * max_warp_nzs consecutive nnz, one group per warp, metadata
- * {row, first nnz, nnz count, 0} (96 bits padded to 128). Reading R10w: an
+ * {row, first nnz, nnz count, 0} (96 bits padded to 128). Reading R14: an
  * empty row gets one group of length 0 so its output row is still written.
  * meta = NULL counts only. Returns the number of groups, -1 on a bad
  * argument, -2 if cap is too small. */
