@@ -116,6 +116,76 @@ def cpu_baseline(g, name, Fs, params, frac, seed=0):
     }
 
 
+ROCSPARSE_ALGS = {"default": 0, "csr": 1, "csr_row_split": 4, "csr_nnz_split": 5, "csr_merge_path": 9}
+
+
+def rocsparse_compare(g, Fs, Xs, Ys, d_rowptr, d_colidx, d_vals, stream, reps):
+    """rocSPARSE's generic CSR SpMM (torch's bundled librocsparse) on the same
+    device arrays: row-major X and Y, fp32, original row order. Times the
+    compute stage only (buffer sizing and preprocessing excluded, as the plan
+    is excluded from `exec_ms`) for every CSR algorithm, and reports the
+    largest difference between its Y and the library's Y. Context for the
+    comparison, not a target."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(os.path.join(os.path.dirname(torch.__file__), "lib", "librocsparse.so"))
+    vp, i64 = ctypes.c_void_p, ctypes.c_int64
+    h = vp()
+    assert lib.rocsparse_create_handle(ctypes.byref(h)) == 0
+    assert lib.rocsparse_set_stream(h, vp(stream.cuda_stream)) == 0
+    A = vp()
+    st = lib.rocsparse_create_csr_descr(ctypes.byref(A), i64(g.n_rows), i64(g.n_cols), i64(g.nnz),
+                                        vp(d_rowptr.data_ptr()), vp(d_colidx.data_ptr()),
+                                        vp(d_vals.data_ptr()), 2, 2, 0, 151)
+    assert st == 0, st
+    alpha, beta = ctypes.c_float(1.0), ctypes.c_float(0.0)
+    out = {}
+    for F in Fs:
+        Yr = torch.empty_like(Ys[F])
+        B, C = vp(), vp()
+        assert lib.rocsparse_create_dnmat_descr(ctypes.byref(B), i64(g.n_cols), i64(F), i64(F),
+                                                vp(Xs[F].data_ptr()), 151, 0) == 0
+        assert lib.rocsparse_create_dnmat_descr(ctypes.byref(C), i64(g.n_rows), i64(F), i64(F),
+                                                vp(Yr.data_ptr()), 151, 0) == 0
+        res = {}
+        for name, alg in ROCSPARSE_ALGS.items():
+            def call(stage, nbytes, buf):
+                return lib.rocsparse_spmm(h, 111, 111, ctypes.byref(alpha), A, B, ctypes.byref(beta),
+                                          C, 151, alg, stage, nbytes, buf)
+            nbytes = ctypes.c_size_t(0)
+            if call(1, ctypes.byref(nbytes), None) != 0:
+                res[name] = "unsupported"
+                continue
+            buf = torch.empty(max(1, nbytes.value), dtype=torch.uint8, device=Ys[F].device)
+            t0 = time.perf_counter()
+            if call(2, ctypes.byref(nbytes), vp(buf.data_ptr())) != 0:
+                res[name] = "preprocess failed"
+                continue
+            torch.cuda.synchronize()
+            t_pre = time.perf_counter() - t0
+            Yr.fill_(float("nan"))
+            if call(3, ctypes.byref(nbytes), vp(buf.data_ptr())) != 0:
+                res[name] = "compute failed"
+                continue
+            torch.cuda.synchronize()
+            diff = float((Yr - Ys[F]).abs().max()) if Yr.numel() else 0.0
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                call(3, ctypes.byref(nbytes), vp(buf.data_ptr()))
+            e1.record(stream)
+            torch.cuda.synchronize()
+            res[name] = {"ms": round(e0.elapsed_time(e1) / reps, 5), "preprocess_s": round(t_pre, 4),
+                         "max_abs_diff_vs_agcn": diff}
+            del buf
+        out[F] = res
+        lib.rocsparse_destroy_dnmat_descr(B)
+        lib.rocsparse_destroy_dnmat_descr(C)
+    lib.rocsparse_destroy_spmat_descr(A)
+    lib.rocsparse_destroy_handle(h)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -128,6 +198,8 @@ def main():
     ap.add_argument("--H", type=int, default=None)
     ap.add_argument("--variant", default="block", choices=["block", "warp_level", "column_loop"],
                     help="ablation baselines of Table II (default: the block-level path)")
+    ap.add_argument("--rocsparse", action="store_true",
+                    help="also time rocSPARSE's CSR SpMM on the same inputs (context)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-frac", type=float, default=0.4)
     ap.add_argument("--copy-probe", action="store_true",
@@ -289,6 +361,16 @@ def main():
         "per_F": per_f,
         "roofline": roofline,
     }
+    if args.rocsparse:
+        log("rocSPARSE comparison ...")
+        rs = rocsparse_compare(g, Fs, Xs, Ys, d_rowptr, d_colidx, d_vals, stream, reps=10)
+        summary = {}
+        for F in Fs:
+            timed = {k: v["ms"] for k, v in rs[F].items() if isinstance(v, dict)}
+            best = min(timed, key=timed.get) if timed else None
+            summary[F] = {"algs": rs[F], "best": best,
+                          "exec_ms_ratio": (round(timed[best] / per_f[F]["exec_ms"], 3) if best else None)}
+        out["rocsparse"] = summary
     if not args.no_cpu_baseline and args.variant == "block":
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(g, name, Fs, (st.max_block_waves, st.max_wave_nzs,
