@@ -16,6 +16,9 @@ Functions and the passages of the paper they follow:
 * ``replay_meta``   Sec. III-C, last paragraph (warp workload from metadata)
 * ``warp_partition`` Sec. III-C panel (b): the warp-level partition baseline
 * ``plan``          degree_sort + relayout + partition in one call
+* ``linear``        Sec. II-A, the linear transformation H = X W
+* ``gcn_layer``     Sec. II-A, a GCNConv forward act(A' (X W)), optionally for
+                    selected rows
 
 The readings taken where the paper is silent are listed in agcn_oracle.h.
 """
@@ -79,6 +82,14 @@ def _load():
                                        ctypes.c_int32, _f32p, ctypes.c_int64, _f32p, _i32p, _i32p,
                                        _i32p]
     lib.oracle_replay_meta.restype = ctypes.c_int
+    lib.oracle_linear.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _f32p,
+                                  ctypes.c_int64, _f32p, ctypes.c_int64, _f32p, ctypes.c_int64]
+    lib.oracle_linear.restype = ctypes.c_int
+    lib.oracle_gcn_layer_rows.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_int32, _i32p, _i32p, _f32p, _f32p,
+                                          ctypes.c_int64, _f32p, ctypes.c_int64, ctypes.c_int32,
+                                          _i32p, ctypes.c_int32, _f32p, _f64p]
+    lib.oracle_gcn_layer_rows.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -231,3 +242,40 @@ def plan(rowptr, colidx, vals, max_block_warps, max_warp_nzs, hub_chunk_nnz=0):
     rowptr_s, colidx_s, vals_s = relayout(rowptr, colidx, vals, perm)
     meta = partition(rowptr_s, max_block_warps, max_warp_nzs, hub_chunk_nnz)
     return dict(perm=perm, rowptr_s=rowptr_s, colidx_s=colidx_s, vals_s=vals_s, meta=meta)
+
+
+def linear(X, W):
+    """H = X W (float32 result of float64 sums)."""
+    X, W = _f32(X), _f32(W)
+    n, fin = X.shape
+    fin2, fout = W.shape
+    if fin2 != fin:
+        raise OracleError("linear: inner dimensions differ")
+    H = np.empty((n, fout), dtype=np.float32)
+    if _load().oracle_linear(n, fin, fout, _p(X, _f32p), max(fin, 1), _p(W, _f32p), max(fout, 1),
+                             _p(H, _f32p), max(fout, 1)) != 0:
+        raise OracleError("linear: invalid input")
+    return H
+
+
+def gcn_layer(rowptr, colidx, vals, X, W, act="relu", rows=None, n_cols=None, want_scale=False):
+    """act(A' (X W)) for all rows or for `rows`; optionally the scale S2."""
+    rowptr, colidx, vals = _i32(rowptr), _i32(colidx), _f32(vals)
+    X, W = _f32(X), _f32(W)
+    n = rowptr.size - 1
+    fin, fout = W.shape
+    if X.shape[1] != fin:
+        raise OracleError("gcn_layer: X and W disagree on fin")
+    n_cols = X.shape[0] if n_cols is None else n_cols
+    a = {"none": 0, "relu": 1}[act]
+    rows_a = None if rows is None else _i32(rows)
+    m = n if rows_a is None else rows_a.size
+    Y = np.empty((m, fout), dtype=np.float32)
+    S2 = np.empty((m, fout), dtype=np.float64) if want_scale else None
+    rc = _load().oracle_gcn_layer_rows(n, n_cols, fin, fout, _p(rowptr, _i32p), _p(colidx, _i32p),
+                                       _p(vals, _f32p), _p(X, _f32p), max(fin, 1), _p(W, _f32p),
+                                       max(fout, 1), a, _p(rows_a, _i32p), m, _p(Y, _f32p),
+                                       _p(S2, _f64p))
+    if rc != 0:
+        raise OracleError("gcn_layer: invalid input")
+    return (Y, S2) if want_scale else Y

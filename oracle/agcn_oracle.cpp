@@ -322,4 +322,65 @@ int oracle_replay_meta(int32_t n_rows, int32_t n_cols, int32_t F, const int32_t*
   return 0;
 }
 
+// Sec. II-A, linear transformation.
+int oracle_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx,
+                  const float* W, int64_t ldw, float* H, int64_t ldh) {
+  if (n < 0 || fin < 0 || fout < 0 || ldx < fin || ldw < fout || ldh < fout) return -1;
+  if (n > 0 && fout > 0 && (H == nullptr || (fin > 0 && (X == nullptr || W == nullptr))))
+    return -1;
+  for (int64_t i = 0; i < n; ++i)
+    for (int32_t c = 0; c < fout; ++c) {
+      double acc = 0.0;
+      for (int32_t k = 0; k < fin; ++k) acc += (double)X[i * ldx + k] * (double)W[(int64_t)k * ldw + c];
+      H[i * ldh + c] = (float)acc;
+    }
+  return 0;
+}
+
+// Sec. II-A, GCNConv forward: X^{l+1} = act(A' (X^l W^l)).
+int oracle_gcn_layer_rows(int32_t n_rows, int32_t n_cols, int32_t fin, int32_t fout,
+                          const int32_t* rowptr, const int32_t* colidx, const float* vals,
+                          const float* X, int64_t ldx, const float* W, int64_t ldw, int32_t act,
+                          const int32_t* rows, int32_t m, float* Y, double* S2) {
+  if (n_rows < 0 || n_cols < 0 || fin < 0 || fout < 0 || ldx < fin || ldw < fout ||
+      rowptr == nullptr || (act != 0 && act != 1))
+    return -1;
+  if (rows == nullptr) m = n_rows;
+  if (m < 0) return -1;
+  std::vector<double> h((size_t)fout), hmag((size_t)fout), acc((size_t)fout), mag((size_t)fout);
+  for (int32_t q = 0; q < m; ++q) {
+    const int32_t i = rows ? rows[q] : q;
+    if (i < 0 || i >= n_rows || rowptr[i + 1] < rowptr[i]) return -1;
+    std::fill(acc.begin(), acc.end(), 0.0);
+    std::fill(mag.begin(), mag.end(), 0.0);
+    for (int32_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+      const int32_t j = colidx[e];
+      if (j < 0 || j >= n_cols) return -1;
+      // row j of X W, and of |X| |W|
+      for (int32_t c = 0; c < fout; ++c) {
+        double s = 0.0, sm = 0.0;
+        for (int32_t k = 0; k < fin; ++k) {
+          const double p = (double)X[(int64_t)j * ldx + k] * (double)W[(int64_t)k * ldw + c];
+          s += p;
+          sm += p < 0 ? -p : p;
+        }
+        h[c] = s;
+        hmag[c] = sm;
+      }
+      const double a = (double)vals[e];
+      const double am = a < 0 ? -a : a;
+      for (int32_t c = 0; c < fout; ++c) {
+        acc[c] += a * h[c];
+        mag[c] += am * hmag[c];
+      }
+    }
+    for (int32_t c = 0; c < fout; ++c) {
+      const double v = (act == 1 && acc[c] < 0.0) ? 0.0 : acc[c];
+      Y[(int64_t)q * fout + c] = (float)v;
+      if (S2) S2[(int64_t)q * fout + c] = mag[c];
+    }
+  }
+  return 0;
+}
+
 }  // extern "C"

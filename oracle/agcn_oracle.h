@@ -111,6 +111,27 @@ int oracle_replay_meta(int32_t n_rows, int32_t n_cols, int32_t F, const int32_t*
                        int32_t max_warp_nzs, const float* X, int64_t ldx, float* Y,
                        int32_t* cover, int32_t* row_hits, int32_t* hub_chunks);
 
+/* Sec. II-A, the linear transformation of a GCNConv layer: H = X W by its
+ * definition. X is n x fin (ld ldx), W is fin x fout (ld ldw), H is n x fout
+ * (ld ldh), all row-major. H[i,c] = sum over k ascending of X[i,k] W[k,c],
+ * summed in float64 and rounded once to float32. */
+int oracle_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx,
+                  const float* W, int64_t ldw, float* H, int64_t ldh);
+
+/* Sec. II-A, one GCNConv layer's forward: the linear transformation followed
+ * by the aggregation and the element-wise activation,
+ *   Y[q,c] = act( sum_e vals[e] * sum_k X[colidx[e],k] W[k,c] ),  i = rows[q],
+ * e over row i of the CSR in ascending order, all in float64 (the product
+ * X W is not rounded), then rounded once to float32. act: 0 = identity,
+ * 1 = ReLU, max(v, 0). Optional S2 (NULL to skip) receives
+ * sum_e |vals[e]| sum_k |X[colidx[e],k]| |W[k,c]|, the scale used by
+ * tolerances. rows = NULL means every row in order (then m = n_rows). Y and S2
+ * are m x fout (ld fout). */
+int oracle_gcn_layer_rows(int32_t n_rows, int32_t n_cols, int32_t fin, int32_t fout,
+                          const int32_t* rowptr, const int32_t* colidx, const float* vals,
+                          const float* X, int64_t ldx, const float* W, int64_t ldw, int32_t act,
+                          const int32_t* rows, int32_t m, float* Y, double* S2);
+
 #ifdef __cplusplus
 }
 #endif

@@ -421,3 +421,101 @@ def test_warp_partition_covers_every_nnz_once(Z):
     assert np.all(cover == 1)
     # every row, empty or not, owns at least one group
     assert set(meta[:, 0].tolist()) == set(range(g.n_rows))
+
+
+# --------------------------------------------------------------------------
+# GCNConv layer of Sec. II-A: linear transformation, aggregation, activation
+# --------------------------------------------------------------------------
+
+def _ulp_close(a, b, ulps=1):
+    """|a - b| <= ulps units in the last place of float32 at |b| (plus the
+    smallest normal, for values that round to zero)."""
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return np.all(np.abs(a - b) <= ulps * np.spacing(np.abs(b).astype(np.float32)).astype(np.float64)
+                  + np.finfo(np.float32).tiny)
+
+
+@pytest.mark.parametrize("n,fin,fout", [(7, 5, 3), (33, 64, 17), (1, 1, 1), (50, 3, 130)])
+def test_linear_matches_numpy_float64(n, fin, fout):
+    rng = np.random.default_rng(n * 1000 + fin * 10 + fout)
+    X = rng.standard_normal((n, fin)).astype(np.float32)
+    W = rng.standard_normal((fin, fout)).astype(np.float32)
+    H = oracle.linear(X, W)
+    ref = X.astype(np.float64) @ W.astype(np.float64)
+    assert H.shape == (n, fout) and H.dtype == np.float32
+    assert _ulp_close(H, ref)
+
+
+def test_linear_closed_forms():
+    rng = np.random.default_rng(1)
+    X = rng.standard_normal((40, 6)).astype(np.float32)
+    assert np.array_equal(oracle.linear(X, np.eye(6, dtype=np.float32)), X)
+    # W selects and scales columns: H[:, c] = 2 * X[:, p[c]] exactly
+    p = np.array([4, 0, 5, 5, 1])
+    W = np.zeros((6, 5), np.float32)
+    W[p, np.arange(5)] = 2.0
+    assert np.array_equal(oracle.linear(X, W), 2.0 * X[:, p])
+    assert oracle.linear(np.zeros((0, 6), np.float32), W).shape == (0, 5)
+    assert np.array_equal(oracle.linear(X, np.zeros((6, 0), np.float32)), np.zeros((40, 0)))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_gcn_layer_matches_dense_bruteforce(seed):
+    """act(A (X W)) against a dense float64 evaluation of the same formula,
+    with repeated columns and empty rows; non-square W catches a transposed
+    operand."""
+    rng = np.random.default_rng(seed)
+    n, n_cols, fin, fout = 23, 19, 7, 5
+    deg = rng.integers(0, 9, size=n)
+    g = graphgen.random_csr(n, n_cols, deg, seed=seed + 40, dupes=True)
+    A = np.zeros((n, n_cols))
+    Aabs = np.zeros((n, n_cols))      # entry-wise |a|: repeated columns add magnitudes
+    for i in range(n):
+        for e in range(g.rowptr[i], g.rowptr[i + 1]):
+            A[i, g.colidx[e]] += float(g.vals[e])
+            Aabs[i, g.colidx[e]] += abs(float(g.vals[e]))
+    X = rng.standard_normal((n_cols, fin)).astype(np.float32)
+    W = rng.standard_normal((fin, fout)).astype(np.float32)
+    Z = A @ (X.astype(np.float64) @ W.astype(np.float64))
+    for act, ref in (("none", Z), ("relu", np.maximum(Z, 0.0))):
+        Y, S2 = oracle.gcn_layer(g.rowptr, g.colidx, g.vals, X, W, act=act, want_scale=True)
+        assert Y.shape == (n, fout)
+        assert np.all(np.abs(Y.astype(np.float64) - ref) <= 1e-6 * S2 + 1e-30), act
+        Smag = Aabs @ (np.abs(X.astype(np.float64)) @ np.abs(W.astype(np.float64)))
+        assert np.allclose(S2, Smag, rtol=1e-12, atol=0)
+
+
+def test_gcn_layer_reduces_to_spmm_with_identity_weights():
+    g = _mixed_graph(5, n=120, max_deg=500, dupes=True)
+    X = np.random.default_rng(6).standard_normal((g.n_cols, 9)).astype(np.float32)
+    Y = oracle.gcn_layer(g.rowptr, g.colidx, g.vals, X, np.eye(9, dtype=np.float32), act="none")
+    Ys = oracle.spmm(g.rowptr, g.colidx, g.vals, X)
+    assert np.array_equal(Y.view(np.uint32), Ys.view(np.uint32))
+
+
+def test_gcn_layer_relu_rows_and_nonnegative_case():
+    g = _mixed_graph(7, n=90, max_deg=400)
+    rng = np.random.default_rng(8)
+    X = rng.standard_normal((g.n_cols, 6)).astype(np.float32)
+    W = rng.standard_normal((6, 4)).astype(np.float32)
+    Yn = oracle.gcn_layer(g.rowptr, g.colidx, g.vals, X, W, act="none")
+    Yr = oracle.gcn_layer(g.rowptr, g.colidx, g.vals, X, W, act="relu")
+    assert np.array_equal(Yr, np.maximum(Yn, 0.0))
+    rows = np.array([5, 0, 89, 5], np.int32)
+    assert np.array_equal(oracle.gcn_layer(g.rowptr, g.colidx, g.vals, X, W, rows=rows), Yr[rows])
+    # all inputs non-negative: the scale is the value itself
+    Xa, Wa, va = np.abs(X), np.abs(W), np.abs(g.vals)
+    Y, S2 = oracle.gcn_layer(g.rowptr, g.colidx, va, Xa, Wa, want_scale=True)
+    assert _ulp_close(Y, S2)
+
+
+def test_gcn_layer_rejects_bad_input():
+    g = graphgen.random_csr(4, 4, np.array([1, 2, 0, 1]), seed=1)
+    X = np.ones((4, 3), np.float32)
+    with pytest.raises(oracle.OracleError):
+        oracle.gcn_layer(g.rowptr, g.colidx, g.vals, X, np.ones((2, 2), np.float32))
+    bad = g.colidx.copy()
+    bad[0] = 4
+    with pytest.raises(oracle.OracleError):
+        oracle.gcn_layer(g.rowptr, bad, g.vals, X, np.ones((3, 2), np.float32))
