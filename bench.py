@@ -14,6 +14,9 @@ in every timed step) and the single-threaded CPU oracle on a row sample.
 
 --variant warp_level / column_loop times one of the two ablation baselines of
 Table II instead (same workload, same step), for the ablation ratios.
+--gcn-layer times one GCNConv forward of Sec. II-A instead (plan built once,
+outside the timed steps): H = X W on the matrix cores, then the aggregation
+with the ReLU epilogue, X of width --fin, W fin x --fout (default 128 x 128).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--F 16,32,...] [--variant block|warp_level|column_loop]
@@ -186,6 +189,94 @@ def rocsparse_compare(g, Fs, Xs, Ys, d_rowptr, d_colidx, d_vals, stream, reps):
     return out
 
 
+MFMA_FP32_PEAK_TFLOPS = 157.3
+
+
+def bench_layer(args):
+    """One GCNConv forward per step over a plan built once."""
+    import torch
+    import paper_2308_11825_amd as agcn
+    name, fin, fout = args.workload, args.fin, args.fout
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = graphgen.make(name, verbose=False)
+    log(f"workload {name}: {graphgen.stats(g)}; layer {fin} -> {fout}")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    d_rowptr, d_colidx, d_vals = t(g.rowptr), t(g.colidx), t(g.vals)
+    X = t(graphgen.workload_features(name, g, fin))
+    W = t(graphgen.weights(fin, fout, seed=7))
+    Y = torch.empty((g.n_rows, fout), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    sh = stream.cuda_stream
+    prm = agcn.agcn_default_params()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    p0, p1 = ev(), ev()
+    p0.record(stream)
+    plan = agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(), d_colidx.data_ptr(),
+                                 d_vals.data_ptr(), prm, sh)
+    p1.record(stream)
+    torch.cuda.synchronize()
+    plan_ms = p0.elapsed_time(p1)
+    st = agcn.agcn_plan_info(plan)
+    nb = agcn.agcn_gcn_workspace_size(plan, fout)
+    ws = torch.empty((nb + 3) // 4, dtype=torch.float32, device=dev)
+    H = ws[: g.n_cols * fout].view(g.n_cols, fout)
+    relu = agcn.AGCN_EPILOGUE_RELU
+
+    def layer():
+        agcn.agcn_gcn_layer(plan, fin, fout, X.data_ptr(), fin, W.data_ptr(), fout, Y.data_ptr(),
+                            fout, ws.data_ptr(), sh, relu)
+
+    for _ in range(args.warmup):
+        layer()
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record(stream)
+    for _ in range(args.steps):
+        layer()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    log(f"timed {args.steps} layer steps: {ms_step:.4f} ms/step")
+    # The two halves of the same call, timed on their own for the roofline:
+    # agcn_linear into the same workspace, then the aggregation with ReLU.
+    marks = [(ev(), ev(), ev()) for _ in range(args.steps)]
+    for a, b, c in marks:
+        a.record(stream)
+        agcn.agcn_linear(g.n_cols, fin, fout, X.data_ptr(), fin, W.data_ptr(), fout, H.data_ptr(),
+                         fout, sh)
+        b.record(stream)
+        agcn.agcn_spmm_ex(plan, fout, H.data_ptr(), fout, Y.data_ptr(), fout,
+                          ws[(nb - agcn.agcn_spmm_workspace_size(plan, fout)) // 4:].data_ptr()
+                          if agcn.agcn_spmm_workspace_size(plan, fout) else None, sh, relu)
+        c.record(stream)
+    torch.cuda.synchronize()
+    lin_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in marks]))
+    agg_ms = float(np.mean([b.elapsed_time(c) for _, b, c in marks]))
+    agcn.agcn_plan_destroy(plan)
+    fl_lin = 2.0 * g.n_cols * fin * fout
+    fl_agg = 2.0 * g.nnz * fout
+    ach = fl_lin / (lin_ms * 1e-3) / 1e12
+    kname = f"k_linear<{32 if fout <= 32 else 64 if fout <= 64 else 128}, true>"
+    out = {
+        "metric": "GCNConv layer forward GFLOP/s (2·N·fin·fout + 2·nnz·fout)",
+        "value": round((fl_lin + fl_agg) / (ms_step * 1e-3) / 1e9, 3), "unit": "GFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": name, "n_rows": g.n_rows, "nnz": g.nnz, "fin": fin, "fout": fout,
+                   "activation": "relu", "parallelism": "single GPU"},
+        "plan_ms_once": round(plan_ms, 4), "linear_ms": round(lin_ms, 5),
+        "aggregation_ms": round(agg_ms, 5),
+        "roofline": {"bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_FP32_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(ach / MFMA_FP32_PEAK_TFLOPS, 4),
+                     "traffic": None, "kernel": kname,
+                     "hbm_bytes_alg": int(4 * g.n_cols * (fin + fout) + 4 * fin * fout)},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -200,6 +291,10 @@ def main():
                     help="ablation baselines of Table II (default: the block-level path)")
     ap.add_argument("--rocsparse", action="store_true",
                     help="also time rocSPARSE's CSR SpMM on the same inputs (context)")
+    ap.add_argument("--gcn-layer", action="store_true",
+                    help="time one GCNConv layer forward (linear + aggregation + ReLU)")
+    ap.add_argument("--fin", type=int, default=128)
+    ap.add_argument("--fout", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-frac", type=float, default=0.4)
     ap.add_argument("--copy-probe", action="store_true",
@@ -214,6 +309,8 @@ def main():
     import torch
     import paper_2308_11825_amd as agcn
 
+    if args.gcn_layer:
+        return bench_layer(args)
     name = args.workload
     Fs = [int(f) for f in args.F.split(",")] if args.F else list(graphgen.CONFIGS[name]["F"])
     dev = torch.device("cuda:0")

@@ -219,6 +219,14 @@ def features(n_rows: int, F: int, seed: int, dist: str = "normal") -> np.ndarray
     raise ValueError(dist)
 
 
+def weights(fin: int, fout: int, seed: int) -> np.ndarray:
+    """A layer weight matrix fin x fout, float32, Glorot-uniform
+    U[-sqrt(6 / (fin + fout)), +sqrt(6 / (fin + fout))] (the usual GCN init)."""
+    rng = np.random.default_rng(seed)
+    lim = np.sqrt(6.0 / max(1, fin + fout))
+    return rng.uniform(-lim, lim, size=(fin, fout)).astype(np.float32)
+
+
 def workload_features(name: str, g: Graph, F: int) -> np.ndarray:
     """Features for a named workload: drawn once at the widest F of that
     workload and column-sliced, so narrower F see the same leading columns."""

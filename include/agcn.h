@@ -158,6 +158,52 @@ int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, 
                     int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
                     void* ev_end);
 
+/* Epilogues of the aggregation, applied where Y is written: the layer's
+ * element-wise activation of Sec. II-A, X^{l+1} = act(A' Y^l). ReLU maps
+ * v < 0 to 0 and keeps every other value (NaN and -0 included). */
+#define AGCN_EPILOGUE_NONE 0
+#define AGCN_EPILOGUE_RELU 1
+
+/* agcn_spmm followed by the epilogue on every element of Y (Sec. II-A). Same
+ * arguments, layouts, errors and launches as agcn_spmm, plus epilogue
+ * (AGCN_EPILOGUE_NONE or AGCN_EPILOGUE_RELU, else INVALID_ARGUMENT). Rows
+ * split over several vwarps or hub chunks get it after their final sum. */
+int agcn_spmm_ex(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+                 int64_t ldy, void* d_ws, void* stream, int32_t epilogue);
+
+/* H = X W, the linear transformation of a GCNConv layer (Sec. II-A), on the
+ * fp32 matrix cores. Asynchronous on `stream`; no plan needed.
+ *
+ * d_X: n rows of fin floats, row stride ldx >= fin; d_W: fin rows of fout
+ * floats, stride ldw >= fout; d_H: n rows of fout floats, stride ldh >= fout.
+ * All row-major, device memory owned by the caller; H must not overlap X or
+ * W. fin = 0 gives H = 0. fp32 products and sums (matrix-core accumulation,
+ * fin terms per element). The 128-bit load path runs when fin, fout, ldx and
+ * ldw are multiples of 4 and X, W are 16-byte aligned; otherwise 32-bit loads
+ * (same results).
+ * Errors: INVALID_ARGUMENT (negative sizes, ld too small, NULL pointers with
+ * non-empty extents, overlap), UNSUPPORTED (more than 2^32 - 1 tiles), HIP. */
+int agcn_linear(int64_t n, int32_t fin, int32_t fout, const float* d_X, int64_t ldx,
+                const float* d_W, int64_t ldw, float* d_H, int64_t ldh, void* stream);
+
+/* Workspace bytes for agcn_gcn_layer with output width fout: H (n_cols x
+ * fout floats, rounded up to 256 bytes) followed by the SpMM workspace of
+ * agcn_spmm_workspace_size(plan, fout). */
+int agcn_gcn_workspace_size(agcn_plan_t plan, int32_t fout, size_t* bytes);
+
+/* One GCNConv layer forward over the plan's graph (Sec. II-A):
+ *   H = X W  (agcn_linear into the workspace),  Y = epilogue(A' H)  (the
+ *   plan's SpMM with the epilogue fused into its Y writes).
+ * d_X: n_cols rows of fin floats (stride ldx); d_W: fin x fout (stride ldw);
+ * d_Y: n_rows rows of fout floats (stride ldy); d_ws: at least
+ * agcn_gcn_workspace_size(plan, fout) bytes, 16-byte aligned, not
+ * overlapping X, W or Y. Asynchronous on `stream`; two launches (three with
+ * hub rows). Errors: those of agcn_linear and agcn_spmm_ex, plus
+ * INVALID_ARGUMENT for a missing or misaligned workspace. */
+int agcn_gcn_layer(agcn_plan_t plan, int32_t fin, int32_t fout, const float* d_X, int64_t ldx,
+                   const float* d_W, int64_t ldw, float* d_Y, int64_t ldy, void* d_ws,
+                   void* stream, int32_t epilogue);
+
 /* Fills *out. Host-only, no HIP call. */
 int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* out);
 

@@ -337,7 +337,10 @@ int oracle_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t 
   return 0;
 }
 
-// Sec. II-A, GCNConv forward: X^{l+1} = act(A' (X^l W^l)).
+// Sec. II-A, GCNConv forward in the paper's two steps: (1) the linear
+// transformation H = X W, kept in float64 (with |X| |W| for the scale), for
+// every node some selected row references; (2) the aggregation A' H with the
+// activation, float64, rounded once.
 int oracle_gcn_layer_rows(int32_t n_rows, int32_t n_cols, int32_t fin, int32_t fout,
                           const int32_t* rowptr, const int32_t* colidx, const float* vals,
                           const float* X, int64_t ldx, const float* W, int64_t ldw, int32_t act,
@@ -347,31 +350,49 @@ int oracle_gcn_layer_rows(int32_t n_rows, int32_t n_cols, int32_t fin, int32_t f
     return -1;
   if (rows == nullptr) m = n_rows;
   if (m < 0) return -1;
-  std::vector<double> h((size_t)fout), hmag((size_t)fout), acc((size_t)fout), mag((size_t)fout);
+  // nodes whose row of H is needed
+  std::vector<int64_t> slot((size_t)n_cols, -1);
+  int64_t n_need = 0;
   for (int32_t q = 0; q < m; ++q) {
     const int32_t i = rows ? rows[q] : q;
     if (i < 0 || i >= n_rows || rowptr[i + 1] < rowptr[i]) return -1;
-    std::fill(acc.begin(), acc.end(), 0.0);
-    std::fill(mag.begin(), mag.end(), 0.0);
     for (int32_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
       const int32_t j = colidx[e];
       if (j < 0 || j >= n_cols) return -1;
-      // row j of X W, and of |X| |W|
-      for (int32_t c = 0; c < fout; ++c) {
-        double s = 0.0, sm = 0.0;
-        for (int32_t k = 0; k < fin; ++k) {
-          const double p = (double)X[(int64_t)j * ldx + k] * (double)W[(int64_t)k * ldw + c];
-          s += p;
-          sm += p < 0 ? -p : p;
-        }
-        h[c] = s;
-        hmag[c] = sm;
+      if (slot[j] < 0) slot[j] = n_need++;
+    }
+  }
+  // step (1): H = X W and |X| |W| for those nodes
+  std::vector<double> H((size_t)n_need * fout), Hm((size_t)n_need * fout);
+  for (int32_t j = 0; j < n_cols; ++j) {
+    if (slot[j] < 0) continue;
+    double* h = &H[(size_t)slot[j] * fout];
+    double* hm = &Hm[(size_t)slot[j] * fout];
+    for (int32_t c = 0; c < fout; ++c) {
+      double s = 0.0, sm = 0.0;
+      for (int32_t k = 0; k < fin; ++k) {
+        const double p = (double)X[(int64_t)j * ldx + k] * (double)W[(int64_t)k * ldw + c];
+        s += p;
+        sm += p < 0 ? -p : p;
       }
+      h[c] = s;
+      hm[c] = sm;
+    }
+  }
+  // step (2): act(A' H)
+  std::vector<double> acc((size_t)fout), mag((size_t)fout);
+  for (int32_t q = 0; q < m; ++q) {
+    const int32_t i = rows ? rows[q] : q;
+    std::fill(acc.begin(), acc.end(), 0.0);
+    std::fill(mag.begin(), mag.end(), 0.0);
+    for (int32_t e = rowptr[i]; e < rowptr[i + 1]; ++e) {
+      const double* h = &H[(size_t)slot[colidx[e]] * fout];
+      const double* hm = &Hm[(size_t)slot[colidx[e]] * fout];
       const double a = (double)vals[e];
       const double am = a < 0 ? -a : a;
       for (int32_t c = 0; c < fout; ++c) {
         acc[c] += a * h[c];
-        mag[c] += am * hmag[c];
+        mag[c] += am * hm[c];
       }
     }
     for (int32_t c = 0; c < fout; ++c) {

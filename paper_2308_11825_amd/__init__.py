@@ -18,8 +18,8 @@ __all__ = [
     "LIB_PATH", "AgcnError", "load_library", "agcn_default_params", "agcn_plan_create",
     "agcn_spmm_workspace_size", "agcn_spmm", "agcn_spmm_timed", "agcn_plan_info",
     "agcn_plan_export", "agcn_plan_destroy", "agcn_status_string", "agcn_last_error",
-    "agcn_release_cached_memory", "Plan",
-    "PlanParams", "PlanStats", "EXPORTED_SYMBOLS",
+    "agcn_release_cached_memory", "agcn_spmm_ex", "agcn_linear", "agcn_gcn_workspace_size",
+    "agcn_gcn_layer", "Plan", "linear", "PlanParams", "PlanStats", "EXPORTED_SYMBOLS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -28,7 +28,8 @@ LIB_PATH = os.path.join(_HERE, "libagcn.so")
 EXPORTED_SYMBOLS = [
     "agcn_default_params", "agcn_plan_create", "agcn_spmm_workspace_size", "agcn_spmm",
     "agcn_spmm_timed", "agcn_plan_info", "agcn_plan_export", "agcn_plan_destroy",
-    "agcn_status_string", "agcn_last_error", "agcn_release_cached_memory",
+    "agcn_status_string", "agcn_last_error", "agcn_release_cached_memory", "agcn_spmm_ex",
+    "agcn_linear", "agcn_gcn_workspace_size", "agcn_gcn_layer",
 ]
 
 AGCN_OK = 0
@@ -40,6 +41,10 @@ AGCN_ERR_HIP = 5
 
 AGCN_PLAN_WARP_LEVEL = 0x1
 AGCN_PLAN_COLUMN_LOOP = 0x2
+
+AGCN_EPILOGUE_NONE = 0
+AGCN_EPILOGUE_RELU = 1
+_EPILOGUES = {None: AGCN_EPILOGUE_NONE, "none": AGCN_EPILOGUE_NONE, "relu": AGCN_EPILOGUE_RELU}
 
 
 class PlanParams(ctypes.Structure):
@@ -119,6 +124,17 @@ def load_library(path: str | None = None):
     lib.agcn_spmm_timed.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, ctypes.c_int64,
                                     _vp, _vp, _vp, _vp, _vp]
     lib.agcn_spmm_timed.restype = ctypes.c_int
+    lib.agcn_spmm_ex.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, ctypes.c_int64,
+                                 _vp, _vp, ctypes.c_int32]
+    lib.agcn_spmm_ex.restype = ctypes.c_int
+    lib.agcn_linear.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _vp,
+                                ctypes.c_int64, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp]
+    lib.agcn_linear.restype = ctypes.c_int
+    lib.agcn_gcn_workspace_size.argtypes = [_vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
+    lib.agcn_gcn_workspace_size.restype = ctypes.c_int
+    lib.agcn_gcn_layer.argtypes = [_vp, ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_int64, _vp,
+                                   ctypes.c_int64, _vp, ctypes.c_int64, _vp, _vp, ctypes.c_int32]
+    lib.agcn_gcn_layer.restype = ctypes.c_int
     lib.agcn_plan_info.argtypes = [_vp, ctypes.POINTER(PlanStats)]
     lib.agcn_plan_info.restype = ctypes.c_int
     lib.agcn_plan_export.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp]
@@ -171,6 +187,25 @@ def agcn_spmm(plan, F, d_X, ldx, d_Y, ldy, d_ws=None, stream=0):
 def agcn_spmm_timed(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, ev_begin, ev_mid, ev_end):
     _check(load_library().agcn_spmm_timed(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, ev_begin,
                                           ev_mid, ev_end))
+
+
+def agcn_spmm_ex(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, epilogue):
+    _check(load_library().agcn_spmm_ex(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, epilogue))
+
+
+def agcn_linear(n, fin, fout, d_X, ldx, d_W, ldw, d_H, ldh, stream=0):
+    _check(load_library().agcn_linear(n, fin, fout, d_X, ldx, d_W, ldw, d_H, ldh, stream))
+
+
+def agcn_gcn_workspace_size(plan, fout) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().agcn_gcn_workspace_size(plan, fout, ctypes.byref(n)))
+    return n.value
+
+
+def agcn_gcn_layer(plan, fin, fout, d_X, ldx, d_W, ldw, d_Y, ldy, d_ws, stream, epilogue):
+    _check(load_library().agcn_gcn_layer(plan, fin, fout, d_X, ldx, d_W, ldw, d_Y, ldy, d_ws,
+                                         stream, epilogue))
 
 
 def agcn_plan_info(plan) -> PlanStats:
@@ -278,7 +313,8 @@ class Plan:
             self._ws[F] = ws
         return ws
 
-    def spmm(self, X, out=None, ws=None, stream=None):
+    def spmm(self, X, out=None, ws=None, stream=None, act=None):
+        """A @ X, with act ("relu") applied where Y is written."""
         import torch
         if not isinstance(X, torch.Tensor) or X.device != self.device or X.dtype != torch.float32:
             raise TypeError("X must be a float32 tensor on the plan's device")
@@ -296,8 +332,35 @@ class Plan:
             ws = self.workspace(F)
         st = stream.cuda_stream if stream is not None else _stream_handle(self.device)
         with torch.cuda.device(self.device):
-            agcn_spmm(self.handle, F, X.data_ptr(), _row_stride(X), out.data_ptr(),
-                      _row_stride(out), ws.data_ptr() if ws is not None else None, st)
+            agcn_spmm_ex(self.handle, F, X.data_ptr(), _row_stride(X), out.data_ptr(),
+                         _row_stride(out), ws.data_ptr() if ws is not None else None, st,
+                         _EPILOGUES[act])
+        return out
+
+    def gcn_layer(self, X, W, act="relu", out=None, ws=None, stream=None):
+        """One GCNConv forward: act(A @ (X @ W)), X (n_cols, fin), W (fin, fout)."""
+        import torch
+        for name, t in (("X", X), ("W", W)):
+            if (not isinstance(t, torch.Tensor) or t.device != self.device
+                    or t.dtype != torch.float32 or t.dim() != 2 or not _unit_col_stride(t)):
+                raise TypeError(f"{name} must be a 2-D float32 tensor on the plan's device with "
+                                "unit column stride")
+        fin, fout = W.shape
+        if X.shape != (self.n_cols, fin):
+            raise ValueError("X must be (n_cols, fin) with fin = W.shape[0]")
+        if out is None:
+            out = torch.empty((self.n_rows, fout), dtype=torch.float32, device=self.device)
+        if (tuple(out.shape) != (self.n_rows, fout) or not _unit_col_stride(out)
+                or out.dtype != torch.float32 or out.device != self.device):
+            raise ValueError("out must be a float32 (n_rows, fout) tensor with unit column stride")
+        if ws is None:
+            nb = agcn_gcn_workspace_size(self.handle, fout)
+            ws = torch.empty((nb + 3) // 4, dtype=torch.float32, device=self.device)
+        st = stream.cuda_stream if stream is not None else _stream_handle(self.device)
+        with torch.cuda.device(self.device):
+            agcn_gcn_layer(self.handle, fin, fout, X.data_ptr(), _row_stride(X), W.data_ptr(),
+                           _row_stride(W), out.data_ptr(), _row_stride(out), ws.data_ptr(), st,
+                           _EPILOGUES[act])
         return out
 
     def export(self):
@@ -326,3 +389,25 @@ class Plan:
             self.destroy()
         except Exception:
             pass
+
+
+def linear(X, W, out=None, stream=None):
+    """X @ W on the matrix cores: X (n, fin), W (fin, fout), float32 CUDA tensors."""
+    import torch
+    for name, t in (("X", X), ("W", W)):
+        if (not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.dtype != torch.float32
+                or t.dim() != 2 or not _unit_col_stride(t)):
+            raise TypeError(f"{name} must be a 2-D float32 CUDA tensor with unit column stride")
+    n, fin = X.shape
+    if W.shape[0] != fin or W.device != X.device:
+        raise ValueError("W must be (fin, fout) on X's device")
+    fout = W.shape[1]
+    if out is None:
+        out = torch.empty((n, fout), dtype=torch.float32, device=X.device)
+    if tuple(out.shape) != (n, fout) or not _unit_col_stride(out) or out.dtype != torch.float32:
+        raise ValueError("out must be a float32 (n, fout) tensor with unit column stride")
+    st = stream.cuda_stream if stream is not None else _stream_handle(X.device)
+    with torch.cuda.device(X.device):
+        agcn_linear(n, fin, fout, X.data_ptr(), _row_stride(X), W.data_ptr(), _row_stride(W),
+                    out.data_ptr(), _row_stride(out), st)
+    return out

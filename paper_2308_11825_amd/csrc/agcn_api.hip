@@ -255,10 +255,25 @@ int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes) {
   return AGCN_OK;
 }
 
-int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
-                    int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
-                    void* ev_end) {
+}  // extern "C"
+
+namespace {
+
+int check_device(const agcn_plan* plan) {
+  int dev = -1;
+  hipError_t he = hipGetDevice(&dev);
+  if (he != hipSuccess) return agcn::hip_fail(he, "hipGetDevice");
+  if (dev != plan->device)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "current device differs from the plan's device");
+  return AGCN_OK;
+}
+
+int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+                 int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
+                 void* ev_end, int32_t epilogue) {
   if (plan == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "plan is NULL");
+  if (epilogue != AGCN_EPILOGUE_NONE && epilogue != AGCN_EPILOGUE_RELU)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "epilogue must be AGCN_EPILOGUE_NONE or AGCN_EPILOGUE_RELU");
   if (F < 1) return fail(AGCN_ERR_INVALID_ARGUMENT, "F must be >= 1");
   if (ldx < F || ldy < F) return fail(AGCN_ERR_INVALID_ARGUMENT, "ldx and ldy must be >= F");
   if (plan->n_rows > 0 && d_Y == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "Y is NULL");
@@ -276,19 +291,107 @@ int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, 
   if (ws_need > 0 && (agcn::ranges_overlap(d_ws, ws_need, d_Y, yb) ||
                       agcn::ranges_overlap(d_ws, ws_need, d_X, xb)))
     return fail(AGCN_ERR_INVALID_ARGUMENT, "workspace overlaps X or Y");
-  int dev = -1;
-  hipError_t he = hipGetDevice(&dev);
-  if (he != hipSuccess) return agcn::hip_fail(he, "hipGetDevice");
-  if (dev != plan->device)
-    return fail(AGCN_ERR_INVALID_ARGUMENT, "current device differs from the plan's device");
+  if (int rc = check_device(plan)) return rc;
   return agcn::run_spmm(plan, F, d_X, ldx, d_Y, ldy, static_cast<float*>(d_ws),
                         static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(ev_begin),
-                        static_cast<hipEvent_t>(ev_mid), static_cast<hipEvent_t>(ev_end));
+                        static_cast<hipEvent_t>(ev_mid), static_cast<hipEvent_t>(ev_end), epilogue);
+}
+
+// Bytes of the transformed features H (n_cols x fout floats) at the start of
+// a layer workspace, rounded up so the SpMM workspace after it is aligned.
+size_t layer_h_bytes(const agcn_plan* plan, int32_t fout) {
+  const size_t b = (size_t)plan->n_cols * (size_t)fout * sizeof(float);
+  return (b + 255) & ~(size_t)255;
+}
+
+int linear_checked(int64_t n, int32_t fin, int32_t fout, const float* d_X, int64_t ldx,
+                   const float* d_W, int64_t ldw, float* d_H, int64_t ldh, void* stream) {
+  if (n < 0 || fin < 0 || fout < 0)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "n, fin and fout must be >= 0");
+  if (ldx < fin || ldw < fout || ldh < fout)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "ldx >= fin, ldw >= fout and ldh >= fout are required");
+  if (n > 0 && fout > 0 && d_H == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "H is NULL");
+  if (n > 0 && fin > 0 && d_X == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "X is NULL");
+  if (fin > 0 && fout > 0 && d_W == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "W is NULL");
+  size_t xb = 0, wb = 0, hb = 0;
+  if (!agcn::span_bytes(n, ldx, fin, &xb) || !agcn::span_bytes(fin, ldw, fout, &wb) ||
+      !agcn::span_bytes(n, ldh, fout, &hb))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "matrix extent overflows");
+  if (agcn::ranges_overlap(d_H, hb, d_X, xb) || agcn::ranges_overlap(d_H, hb, d_W, wb))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "H overlaps X or W");
+  return agcn::run_linear(n, fin, fout, d_X, ldx, d_W, ldw, d_H, ldh,
+                          static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+                    int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
+                    void* ev_end) {
+  return spmm_checked(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, ev_begin, ev_mid, ev_end,
+                      AGCN_EPILOGUE_NONE);
 }
 
 int agcn_spmm(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
               int64_t ldy, void* d_ws, void* stream) {
-  return agcn_spmm_timed(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, nullptr, nullptr, nullptr);
+  return spmm_checked(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, nullptr, nullptr, nullptr,
+                      AGCN_EPILOGUE_NONE);
+}
+
+int agcn_spmm_ex(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+                 int64_t ldy, void* d_ws, void* stream, int32_t epilogue) {
+  return spmm_checked(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, nullptr, nullptr, nullptr,
+                      epilogue);
+}
+
+int agcn_linear(int64_t n, int32_t fin, int32_t fout, const float* d_X, int64_t ldx,
+                const float* d_W, int64_t ldw, float* d_H, int64_t ldh, void* stream) {
+  return linear_checked(n, fin, fout, d_X, ldx, d_W, ldw, d_H, ldh, stream);
+}
+
+int agcn_gcn_workspace_size(agcn_plan_t plan, int32_t fout, size_t* bytes) {
+  if (plan == nullptr || bytes == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "NULL argument");
+  if (fout < 1) return fail(AGCN_ERR_INVALID_ARGUMENT, "fout must be >= 1");
+  size_t spmm_ws = 0;
+  if (int rc = agcn_spmm_workspace_size(plan, fout, &spmm_ws)) return rc;
+  *bytes = layer_h_bytes(plan, fout) + spmm_ws;
+  return AGCN_OK;
+}
+
+int agcn_gcn_layer(agcn_plan_t plan, int32_t fin, int32_t fout, const float* d_X, int64_t ldx,
+                   const float* d_W, int64_t ldw, float* d_Y, int64_t ldy, void* d_ws,
+                   void* stream, int32_t epilogue) {
+  if (plan == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "plan is NULL");
+  if (fin < 0 || fout < 1) return fail(AGCN_ERR_INVALID_ARGUMENT, "fin >= 0 and fout >= 1 are required");
+  if (epilogue != AGCN_EPILOGUE_NONE && epilogue != AGCN_EPILOGUE_RELU)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "epilogue must be AGCN_EPILOGUE_NONE or AGCN_EPILOGUE_RELU");
+  size_t need = 0;
+  agcn_gcn_workspace_size(plan, fout, &need);
+  const size_t hbytes = layer_h_bytes(plan, fout);
+  if (plan->n_cols > 0 && d_ws == nullptr)
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "a workspace of agcn_gcn_workspace_size bytes is required");
+  if (d_ws != nullptr && !agcn::aligned16(d_ws))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "the workspace must be 16-byte aligned");
+  size_t xb = 0, yb = 0;
+  if (!agcn::span_bytes(plan->n_cols, ldx, fin, &xb) || !agcn::span_bytes(plan->n_rows, ldy, fout, &yb))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "matrix extent overflows");
+  size_t wb = 0;
+  if (!agcn::span_bytes(fin, ldw, fout, &wb))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "matrix extent overflows");
+  if (agcn::ranges_overlap(d_ws, need, d_X, xb) || agcn::ranges_overlap(d_ws, need, d_Y, yb) ||
+      agcn::ranges_overlap(d_ws, need, d_W, wb))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "workspace overlaps X, W or Y");
+  if (agcn::ranges_overlap(d_Y, yb, d_X, xb) || agcn::ranges_overlap(d_Y, yb, d_W, wb))
+    return fail(AGCN_ERR_INVALID_ARGUMENT, "Y overlaps X or W");
+  if (int rc = check_device(plan)) return rc;
+  float* H = static_cast<float*>(d_ws);
+  if (int rc = linear_checked(plan->n_cols, fin, fout, d_X, ldx, d_W, ldw, H, fout, stream))
+    return rc;
+  void* spmm_ws = need > hbytes ? static_cast<char*>(d_ws) + hbytes : nullptr;
+  return spmm_checked(plan, fout, H, fout, d_Y, ldy, spmm_ws, stream, nullptr, nullptr, nullptr,
+                      epilogue);
 }
 
 int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* s) {

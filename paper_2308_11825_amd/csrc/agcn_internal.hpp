@@ -74,10 +74,14 @@ inline int64_t warp_level_blocks(const agcn_plan* p) {
   return p->W > 0 ? (p->n_entries + p->W - 1) / p->W : 0;
 }
 
-// Execute (agcn_spmm.hip).
+// Execute (agcn_spmm.hip). act: 0 = identity, 1 = ReLU on every Y write.
 int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,
              float* ws, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_mid,
-             hipEvent_t ev_end);
+             hipEvent_t ev_end, int32_t act);
+
+// H = X W on matrix cores (agcn_linear.hip).
+int run_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx, const float* W,
+               int64_t ldw, float* H, int64_t ldh, hipStream_t stream);
 
 // Dynamic LDS bytes the SpMM kernel needs for a plan (worst case over F).
 size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz);
@@ -89,5 +93,6 @@ int device_alloc(int device, size_t bytes, void** out, size_t* got);
 void device_release(int device, void* ptr, size_t bytes);
 
 inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; }
 
 }  // namespace agcn

@@ -81,6 +81,13 @@ __device__ inline f4 fma_v(float a, f4 x, f4 acc) {
 }
 __device__ inline float fma_v(float a, float x, float acc) { return __builtin_fmaf(a, x, acc); }
 
+// Epilogue at the Y write: act = 1 applies ReLU (negative values become 0;
+// NaN and -0 pass through, as max(v, 0) defined by v < 0 ? 0 : v).
+__device__ inline float act_v(float v, int32_t act) { return (act && v < 0.0f) ? 0.0f : v; }
+__device__ inline f4 act_v(f4 v, int32_t act) {
+  return act ? f4{act_v(v.x, 1), act_v(v.y, 1), act_v(v.z, 1), act_v(v.w, 1)} : v;
+}
+
 // acc = sum over j in [s0, s0 + len) of val[j] * X[col[j], lane], in order.
 // Groups of kGatherUnroll loads are issued before the first is consumed; the
 // tail of a group is predicated, so short slices still overlap their loads.
@@ -117,7 +124,8 @@ __global__ __launch_bounds__(1024) void k_spmm(
     int32_t deg_bound, int32_t W, const int32_t* __restrict__ colidx_s,
     const float* __restrict__ vals_s, const int32_t* __restrict__ perm, const float* __restrict__ X,
     int64_t ldx, float* __restrict__ Y, int64_t ldy, float* __restrict__ ws, int32_t F,
-    int32_t col_base, int32_t slice_cols, int32_t L_rt, int32_t rounds, int32_t cap_pad) {
+    int32_t col_base, int32_t slice_cols, int32_t L_rt, int32_t rounds, int32_t cap_pad,
+    int32_t act) {
   using V = typename VecOf<VW>::T;
   const int L = LT > 0 ? LT : L_rt;
   extern __shared__ float smem[];
@@ -172,7 +180,7 @@ __global__ __launch_bounds__(1024) void k_spmm(
         const V acc = gather_row<VW>(s_col, s_val, s0, len, Xv, ldxv, l);
         if (wpr == 1) {
           V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[row + rl] * ldy + col0);
-          __builtin_nontemporal_store(acc, yr + l);
+          __builtin_nontemporal_store(act_v(acc, act), yr + l);
         } else {
           s_part[part_idx<VW>(v * L + l)] = acc;
         }
@@ -187,7 +195,7 @@ __global__ __launch_bounds__(1024) void k_spmm(
           V sum = s_part[part_idx<VW>((r * wpr) * L + l)];
           for (int q = 1; q < wpr; ++q) sum += s_part[part_idx<VW>((r * wpr + q) * L + l)];
           V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[row + r] * ldy + col0);
-          __builtin_nontemporal_store(sum, yr + l);
+          __builtin_nontemporal_store(act_v(sum, act), yr + l);
         }
       }
     }
@@ -223,7 +231,7 @@ __global__ __launch_bounds__(1024) void k_hub_reduce(const int32_t* __restrict__
                                                      const float* __restrict__ ws, int32_t F,
                                                      float* __restrict__ Y, int64_t ldy,
                                                      int32_t col_base, int32_t slice_cols,
-                                                     int32_t L, int32_t G) {
+                                                     int32_t L, int32_t G, int32_t act) {
   using V = typename VecOf<VW>::T;
   extern __shared__ float smem[];
   V* s_acc = reinterpret_cast<V*>(smem);  // [G][L]
@@ -248,7 +256,7 @@ __global__ __launch_bounds__(1024) void k_hub_reduce(const int32_t* __restrict__
   }
   if (g == 0) {
     V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[hub_first_row + h] * ldy + col0);
-    __builtin_nontemporal_store(s_acc[l], yr + l);
+    __builtin_nontemporal_store(act_v(s_acc[l], act), yr + l);
   }
 }
 
@@ -265,7 +273,7 @@ __global__ __launch_bounds__(1024) void k_spmm_wl(
     const int32_t* __restrict__ colidx_s, const float* __restrict__ vals_s,
     const float* __restrict__ X, int64_t ldx, float* __restrict__ Y, int64_t ldy,
     float* __restrict__ ws, int32_t F, int32_t col_base, int32_t slice_cols, int32_t L_rt,
-    int32_t rounds, int32_t cap_pad) {
+    int32_t rounds, int32_t cap_pad, int32_t act) {
   using V = typename VecOf<VW>::T;
   const int L = LT > 0 ? LT : L_rt;
   extern __shared__ float smem[];
@@ -333,7 +341,7 @@ __global__ __launch_bounds__(1024) void k_spmm_wl(
         wr[l] = sum;
       } else {
         V* yr = reinterpret_cast<V*>(Y + (int64_t)row * ldy + col0);
-        __builtin_nontemporal_store(sum, yr + l);
+        __builtin_nontemporal_store(act_v(sum, act), yr + l);
       }
     }
   }
@@ -345,7 +353,8 @@ template <int VW>
 __global__ __launch_bounds__(256) void k_wl_fixup(const int32_t* __restrict__ goff, int32_t n_rows,
                                                   int32_t W, const float* __restrict__ ws, int32_t F,
                                                   float* __restrict__ Y, int64_t ldy,
-                                                  int32_t col_base, int32_t slice_cols, int32_t L) {
+                                                  int32_t col_base, int32_t slice_cols, int32_t L,
+                                                  int32_t act) {
   using V = typename VecOf<VW>::T;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t r = t / L;
@@ -366,7 +375,7 @@ __global__ __launch_bounds__(256) void k_wl_fixup(const int32_t* __restrict__ go
     total = b == b0 ? run : total + run;
   }
   V* yr = reinterpret_cast<V*>(Y + r * ldy + col0);
-  __builtin_nontemporal_store(total, yr + l);
+  __builtin_nontemporal_store(act_v(total, act), yr + l);
 }
 
 // Block-level partition without the combined warp: every vwarp is one
@@ -377,7 +386,7 @@ __global__ __launch_bounds__(1024) void k_spmm_colloop(
     int32_t deg_bound, int32_t W, const int32_t* __restrict__ colidx_s,
     const float* __restrict__ vals_s, const int32_t* __restrict__ perm, const float* __restrict__ X,
     int64_t ldx, float* __restrict__ Y, int64_t ldy, float* __restrict__ ws, int32_t F,
-    int32_t rounds, int32_t cap_pad) {
+    int32_t rounds, int32_t cap_pad, int32_t act) {
   extern __shared__ float smem[];
   int32_t* s_col = reinterpret_cast<int32_t*>(smem);
   float* s_val = smem + cap_pad;
@@ -416,7 +425,7 @@ __global__ __launch_bounds__(1024) void k_spmm_colloop(
     for (int c = lane; c < F; c += 64) {  // the single-warp column loop
       const float acc = gather_row<1>(s_col, s_val, s0, len, X, ldx, c);
       if (!hub && wpr == 1)
-        __builtin_nontemporal_store(acc, Y + (int64_t)perm[row + rl] * ldy + c);
+        __builtin_nontemporal_store(act_v(acc, act), Y + (int64_t)perm[row + rl] * ldy + c);
       else
         s_part[(int64_t)v * F + c] = acc;
     }
@@ -430,7 +439,7 @@ __global__ __launch_bounds__(1024) void k_spmm_colloop(
       float sum = s_part[(int64_t)first * F + c];
       for (int q = 1; q < wpr; ++q) sum += s_part[(int64_t)(first + q) * F + c];
       if (hub) ws[(int64_t)(b - hub_first_entry) * F + c] = sum;
-      else __builtin_nontemporal_store(sum, Y + (int64_t)perm[row + r] * ldy + c);
+      else __builtin_nontemporal_store(act_v(sum, act), Y + (int64_t)perm[row + r] * ldy + c);
     }
   }
 }
@@ -469,6 +478,7 @@ struct SpmmArgs {
   int64_t ldy;
   float* ws;
   hipStream_t st;
+  int32_t act;
 };
 
 // Timing marks for k_spmm: the first launch records `start` when it begins
@@ -497,13 +507,13 @@ void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice
       hipExtLaunchKernelGGL(k_spmm<VW, LT>, grid, dim3(T), (uint32_t)lds, a.st, mk.start, stop, 0,
                             p->meta, p->order, (int32_t)e0, p->hub_first_entry, p->deg_bound, p->W,
                             p->colidx_s, p->vals_s, p->perm, a.X, a.ldx, a.Y, a.ldy, a.ws, a.F,
-                            col_base, slice_cols, L, rounds, cap_pad);
+                            col_base, slice_cols, L, rounds, cap_pad, a.act);
       mk.start = nullptr;
     } else {
       k_spmm<VW, LT><<<grid, T, lds, a.st>>>(p->meta, p->order, (int32_t)e0, p->hub_first_entry,
                                              p->deg_bound, p->W, p->colidx_s, p->vals_s, p->perm,
                                              a.X, a.ldx, a.Y, a.ldy, a.ws, a.F, col_base,
-                                             slice_cols, L, rounds, cap_pad);
+                                             slice_cols, L, rounds, cap_pad, a.act);
     }
   }
 }
@@ -532,7 +542,7 @@ void launch_hub(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_
   const size_t lds = (size_t)G * L * VW * 4;
   dim3 grid((unsigned)p->n_hub_rows, (unsigned)n_slices);
   k_hub_reduce<VW><<<grid, T, lds, a.st>>>(p->hub_chunk_off, p->hub_first_row, p->perm, a.ws, a.F,
-                                           a.Y, a.ldy, col_base, slice_cols, L, G);
+                                           a.Y, a.ldy, col_base, slice_cols, L, G, a.act);
 }
 
 // Runs one phase (aggregation or hub reduction) over all column slices: the
@@ -558,7 +568,6 @@ int run_phase(const SpmmArgs& a, bool hub_phase, Marks& mk) {
   return AGCN_OK;
 }
 
-inline bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; }
 
 }  // namespace
 
@@ -582,7 +591,7 @@ void launch_wl(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_c
   const hipEvent_t stop = last_part ? mk.stop : nullptr;
   hipExtLaunchKernelGGL(k_spmm_wl<VW, LT>, grid, dim3(T), (uint32_t)lds, a.st, mk.start, stop, 0,
                         p->meta, p->n_entries, p->W, p->colidx_s, p->vals_s, a.X, a.ldx, a.Y,
-                        a.ldy, a.ws, a.F, col_base, slice_cols, L, rounds, cap_pad);
+                        a.ldy, a.ws, a.F, col_base, slice_cols, L, rounds, cap_pad, a.act);
   mk.start = nullptr;
 }
 
@@ -609,7 +618,7 @@ int run_warp_level(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
     const int rows_per_block = std::max(1, 256 / L);
     dim3 fgrid((unsigned)ceil_div64(p->n_rows, rows_per_block), (unsigned)n_slices);
     k_wl_fixup<VW><<<fgrid, rows_per_block * L, 0, a.st>>>(p->group_off, p->n_rows, p->W, a.ws, a.F,
-                                                           a.Y, a.ldy, col_base, sc, L);
+                                                           a.Y, a.ldy, col_base, sc, L, a.act);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_wl_fixup launch");
   }
   hipError_t e;
@@ -630,7 +639,7 @@ int run_colloop(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
   hipExtLaunchKernelGGL(k_spmm_colloop, dim3((unsigned)p->n_entries), dim3(T), (uint32_t)lds, a.st,
                         mk.start, mk.stop, 0, p->meta, p->order, p->hub_first_entry, p->deg_bound,
                         p->W, p->colidx_s, p->vals_s, p->perm, a.X, a.ldx, a.Y, a.ldy, a.ws, a.F,
-                        rounds, cap_pad);
+                        rounds, cap_pad, a.act);
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_spmm_colloop launch");
   if (p->n_hub_rows > 0) {
     const int L = std::min(64, a.F);
@@ -642,7 +651,8 @@ int run_colloop(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
       const int cols = std::min(64, a.F - s * 64);
       k_hub_reduce<1><<<dim3((unsigned)p->n_hub_rows, 1), round_up(G * cols, 64),
                         (size_t)G * cols * 4, a.st>>>(p->hub_chunk_off, p->hub_first_row, p->perm,
-                                                      a.ws, a.F, a.Y, a.ldy, s * 64, 64, cols, G);
+                                                      a.ws, a.F, a.Y, a.ldy, s * 64, 64, cols, G,
+                                                      a.act);
     }
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_hub_reduce launch");
   }
@@ -654,10 +664,10 @@ int run_colloop(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
 
 int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,
              float* ws, hipStream_t st, hipEvent_t ev_begin, hipEvent_t ev_mid,
-             hipEvent_t ev_end) {
+             hipEvent_t ev_end, int32_t act) {
   const bool vec = (F % 4 == 0) && (ldx % 4 == 0) && (ldy % 4 == 0) && aligned16(X) &&
                    aligned16(Y) && (ws == nullptr || aligned16(ws));
-  const SpmmArgs a{p, F, X, ldx, Y, ldy, ws, st};
+  const SpmmArgs a{p, F, X, ldx, Y, ldy, ws, st, act};
   hipError_t e;
   // The plan's last kernels (the launch order) were queued on the plan's
   // stream after its host synchronisation; order this stream after them.

@@ -96,6 +96,10 @@ def test_plan_create_rejects_on_host(lib, kw, status):
 
 
 def test_null_plan_calls(lib):
+    assert lib.agcn_spmm_ex(None, 16, 0x1000, 16, 0x2000, 16, None, None, 1) == 1
+    n = ctypes.c_size_t()
+    assert lib.agcn_gcn_workspace_size(None, 16, ctypes.byref(n)) == 1
+    assert lib.agcn_gcn_layer(None, 8, 16, 0x1000, 8, 0x2000, 16, 0x3000, 16, 0x4000, None, 1) == 1
     assert lib.agcn_spmm(None, 16, 0x1000, 16, 0x2000, 16, None, None) == 1
     assert lib.agcn_spmm_timed(None, 16, 0x1000, 16, 0x2000, 16, None, None, None, None, None) == 1
     n = ctypes.c_size_t()
@@ -122,3 +126,21 @@ def test_product_package_does_not_reference_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text, f
                 assert "agcn_oracle" not in text, f
+
+
+@pytest.mark.parametrize("args,status", [
+    ((-1, 4, 4, 0x1000, 4, 0x2000, 4, 0x3000, 4), 1),          # negative n
+    ((8, -1, 4, 0x1000, 4, 0x2000, 4, 0x3000, 4), 1),          # negative fin
+    ((8, 4, -2, 0x1000, 4, 0x2000, 4, 0x3000, 4), 1),          # negative fout
+    ((8, 4, 4, 0x1000, 3, 0x2000, 4, 0x3000, 4), 1),           # ldx < fin
+    ((8, 4, 4, 0x1000, 4, 0x2000, 3, 0x3000, 4), 1),           # ldw < fout
+    ((8, 4, 4, 0x1000, 4, 0x2000, 4, 0x3000, 3), 1),           # ldh < fout
+    ((8, 4, 4, None, 4, 0x2000, 4, 0x3000, 4), 1),             # X missing
+    ((8, 4, 4, 0x1000, 4, None, 4, 0x3000, 4), 1),             # W missing
+    ((8, 4, 4, 0x1000, 4, 0x2000, 4, None, 4), 1),             # H missing
+    ((8, 4, 4, 0x1000, 4, 0x2000, 4, 0x1010, 4), 1),           # H overlaps X
+    ((0, 4, 4, None, 4, 0x2000, 4, None, 4), 0),               # empty: nothing to launch
+    ((8, 4, 0, 0x1000, 4, None, 0, None, 0), 0),               # fout = 0: nothing to launch
+])
+def test_linear_rejects_on_host(lib, args, status):
+    assert lib.agcn_linear(*args, None) == status, agcn.agcn_last_error()

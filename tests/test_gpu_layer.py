@@ -1,0 +1,179 @@
+"""GPU parity of the GCNConv layer (Sec. II-A) through the C ABI:
+agcn_linear (H = X W on the matrix cores), agcn_spmm_ex (the aggregation
+with the ReLU epilogue) and agcn_gcn_layer (both in one call), against the
+CPU oracle.
+
+Tolerances, from the rounding depth of the device arithmetic (u = 2^-24):
+* linear: |H - H_oracle| <= (fin + 2) u |X||W| + 1e-30 (fp32 products and a
+  chain of at most fin additions per element, the oracle rounded once);
+* aggregation with ReLU: the SpMM bound 1e-5 S + 1e-7 (ReLU is 1-Lipschitz);
+* layer: (1e-5 + (fin + 3) u) S2 + 1e-7, S2 = sum_e |a_e| sum_k |x||w|: the
+  linear step's error carried through A, plus the SpMM bound over the
+  computed H, plus the oracle's single rounding.
+"""
+import numpy as np
+import pytest
+
+import graphgen
+import oracle
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2308_11825_amd as agcn  # noqa: E402
+
+from gpu_helpers import DEV, _dev, _mixed, _plan, _sample_rows, _workload, assert_close  # noqa: E402
+
+U = 2.0 ** -24
+
+
+def _check_linear(X, W, H, what=""):
+    fin = W.shape[0]
+    Hr = oracle.linear(X, W)
+    S = np.abs(X.astype(np.float64)) @ np.abs(W.astype(np.float64))
+    err = np.abs(H.astype(np.float64) - Hr.astype(np.float64))
+    tol = (fin + 2) * U * S + 1e-30
+    bad = err > tol
+    assert not bad.any(), (f"{what}: {int(bad.sum())} out of tolerance; first "
+                           f"{tuple(np.argwhere(bad)[0])}")
+
+
+@pytest.mark.parametrize("n,fin,fout", [(1000, 128, 128), (777, 33, 17), (5000, 64, 16),
+                                        (130, 1, 1), (300, 256, 300), (2000, 100, 40),
+                                        (129, 32, 32), (64, 0, 8), (4097, 12, 200)])
+def test_linear_matches_oracle(n, fin, fout):
+    rng = np.random.default_rng(n + fin + fout)
+    X = rng.standard_normal((n, fin)).astype(np.float32)
+    W = graphgen.weights(fin, fout, seed=fin * 1000 + fout)
+    print(f"[linear] n={n} fin={fin} fout={fout}", flush=True)
+    H = agcn.linear(_dev(X), _dev(W)).cpu().numpy()
+    _check_linear(X, W, H, f"n={n} fin={fin} fout={fout}")
+
+
+def test_linear_strided_unaligned_and_deterministic():
+    rng = np.random.default_rng(3)
+    n, fin, fout = 3001, 64, 48
+    X = rng.standard_normal((n, fin)).astype(np.float32)
+    W = graphgen.weights(fin, fout, seed=4)
+    Xd, Wd = _dev(X), _dev(W)
+    H1 = agcn.linear(Xd, Wd).cpu().numpy()
+    H2 = agcn.linear(Xd, Wd).cpu().numpy()
+    assert np.array_equal(H1.view(np.uint32), H2.view(np.uint32))
+    _check_linear(X, W, H1, "aligned")
+    # X one float past an aligned address, W with a padded row stride, H strided: 32-bit path
+    buf = torch.empty(n * fin + 1, device=DEV)
+    Xu = buf[1:].view(n, fin)
+    Xu.copy_(Xd)
+    Wp = torch.zeros((fin, fout + 3), device=DEV)
+    Wp[:, :fout] = Wd
+    Hs = torch.full((n, fout + 5), 9.0, device=DEV)
+    agcn.linear(Xu, Wp[:, :fout], out=Hs[:, :fout])
+    _check_linear(X, W, Hs[:, :fout].cpu().numpy(), "unaligned/strided")
+    assert torch.all(Hs[:, fout:] == 9.0)
+
+
+def test_linear_identity_is_exact():
+    X = np.random.default_rng(5).standard_normal((1000, 96)).astype(np.float32)
+    H = agcn.linear(_dev(X), _dev(np.eye(96, dtype=np.float32))).cpu().numpy()
+    assert np.array_equal(H.view(np.uint32), X.view(np.uint32))
+
+
+@pytest.fixture(scope="module")
+def layer_graph():
+    return _mixed(61, n=9000, hub_max=5000)
+
+
+@pytest.mark.parametrize("flags", [0, agcn.AGCN_PLAN_WARP_LEVEL, agcn.AGCN_PLAN_COLUMN_LOOP])
+@pytest.mark.parametrize("F", [1, 16, 17, 64, 128])
+def test_spmm_relu_epilogue(layer_graph, flags, F):
+    g = layer_graph
+    plan = _plan(g, flags=flags)
+    X = np.random.default_rng(F).standard_normal((g.n_cols, F)).astype(np.float32)
+    Y, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, want_scale=True)
+    Yg = plan.spmm(_dev(X), act="relu").cpu().numpy()
+    assert np.all(Yg >= 0)
+    assert_close(Yg, np.maximum(Y, 0.0), S, f"relu flags={flags} F={F}")
+    # the epilogue only touches negative values
+    Yn = plan.spmm(_dev(X)).cpu().numpy()
+    assert np.array_equal(Yg, np.where(Yn < 0, np.float32(0), Yn))
+    plan.destroy()
+
+
+def _check_layer(plan, g, X, W, act, rows=None, Yg=None):
+    fin = W.shape[0]
+    if Yg is None:
+        Yg = plan.gcn_layer(_dev(X), _dev(W), act=act).cpu().numpy()
+    Yr, S2 = oracle.gcn_layer(g.rowptr, g.colidx, g.vals, X, W, act=act, rows=rows,
+                              n_cols=g.n_cols, want_scale=True)
+    Yc = Yg if rows is None else Yg[rows]
+    err = np.abs(Yc.astype(np.float64) - Yr.astype(np.float64))
+    tol = (1e-5 + (fin + 3) * U) * S2 + 1e-7
+    bad = err > tol
+    assert not bad.any(), (f"layer act={act}: {int(bad.sum())} out of tolerance; first "
+                           f"{tuple(np.argwhere(bad)[0])}")
+    return Yg
+
+
+@pytest.mark.parametrize("flags", [0, agcn.AGCN_PLAN_WARP_LEVEL, agcn.AGCN_PLAN_COLUMN_LOOP])
+@pytest.mark.parametrize("fin,fout", [(32, 16), (64, 64), (48, 17), (128, 128)])
+def test_gcn_layer_matches_oracle(layer_graph, flags, fin, fout):
+    g = layer_graph
+    plan = _plan(g, flags=flags)
+    X = np.random.default_rng(fin).standard_normal((g.n_cols, fin)).astype(np.float32)
+    W = graphgen.weights(fin, fout, seed=fout)
+    print(f"[layer] flags={flags} fin={fin} fout={fout}", flush=True)
+    Y1 = _check_layer(plan, g, X, W, "relu")
+    Y2 = plan.gcn_layer(_dev(X), _dev(W), act="relu").cpu().numpy()
+    assert np.array_equal(Y1.view(np.uint32), Y2.view(np.uint32))
+    _check_layer(plan, g, X, W, "none")
+    plan.destroy()
+
+
+def test_gcn_layer_equals_linear_then_spmm(layer_graph):
+    """The fused call runs the same kernels as linear followed by spmm_ex."""
+    g = layer_graph
+    plan = _plan(g)
+    X = _dev(np.random.default_rng(1).standard_normal((g.n_cols, 64)).astype(np.float32))
+    W = _dev(graphgen.weights(64, 32, seed=2))
+    Y1 = plan.gcn_layer(X, W, act="relu")
+    Y2 = plan.spmm(agcn.linear(X, W), act="relu")
+    assert torch.equal(Y1, Y2)
+    plan.destroy()
+
+
+def test_gcn_layer_argument_errors(layer_graph):
+    g = layer_graph
+    plan = _plan(g)
+    X = torch.zeros((g.n_cols, 8), device=DEV)
+    W = torch.zeros((8, 16), device=DEV)
+    Y = torch.zeros((g.n_rows, 16), device=DEV)
+    nb = agcn.agcn_gcn_workspace_size(plan.handle, 16)
+    assert nb >= g.n_cols * 16 * 4
+    ws = torch.empty(nb // 4 + 8, device=DEV)
+    h = plan.handle
+    cases = [((h, 8, 16, X.data_ptr(), 8, W.data_ptr(), 16, Y.data_ptr(), 16, None, None, 1), 1),
+             ((h, 8, 16, X.data_ptr(), 8, W.data_ptr(), 16, Y.data_ptr(), 16, ws.data_ptr(), None, 2), 1),
+             ((h, 8, 16, X.data_ptr(), 8, W.data_ptr(), 16, Y.data_ptr(), 16, ws.data_ptr() + 4, None, 1), 1),
+             ((h, 8, 16, X.data_ptr(), 8, W.data_ptr(), 16, X.data_ptr(), 16, ws.data_ptr(), None, 1), 1),
+             ((h, 8, 0, X.data_ptr(), 8, W.data_ptr(), 16, Y.data_ptr(), 16, ws.data_ptr(), None, 1), 1)]
+    for args, status in cases:
+        with pytest.raises(agcn.AgcnError) as ei:
+            agcn.agcn_gcn_layer(*args)
+        assert ei.value.status == status
+    with pytest.raises(agcn.AgcnError):
+        agcn.agcn_spmm_ex(h, 16, W.data_ptr(), 16, Y.data_ptr(), 16, None, None, 5)
+    plan.destroy()
+
+
+@pytest.mark.slow
+def test_gcn_layer_workload_parity():
+    """The layer at the benchmark's size: sweep_powerlaw graph, fin = fout = 128."""
+    name = "sweep_powerlaw"
+    g = _workload(name)
+    plan = _plan(g)
+    X = graphgen.workload_features(name, g, 128)
+    W = graphgen.weights(128, 128, seed=7)
+    rows = _sample_rows(g, plan, k=1500)
+    _check_layer(plan, g, X, W, "relu", rows=rows)
+    print(f"[layer] {name} fin=fout=128 ok ({rows.size} rows checked)", flush=True)
+    plan.destroy()
