@@ -302,8 +302,9 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(how the path would shard is documented, not built).", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path "
+              "(row or column sharding of the aggregation is described, not implemented).",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch

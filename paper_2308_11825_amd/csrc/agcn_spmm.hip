@@ -34,6 +34,13 @@
 // column they gather, so chunks running side by side read neighbouring X rows
 // and share them in L2; then the other entries heaviest first (the metadata
 // is in ascending degree order).
+//
+// Every kernel that writes Y takes `act` and applies the layer's activation
+// there (ReLU, Sec. II-A), after a split row's final sum.
+//
+// The two baselines of Table II live here too: k_spmm_wl + k_wl_fixup execute
+// the warp-level partition, k_spmm_colloop the block-level partition without
+// the combined warp (one float per lane, a loop over F).
 #include <algorithm>
 #include <climits>
 #include <cstdlib>
