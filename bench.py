@@ -84,9 +84,17 @@ def spmm_kernel_name(F, variant="block"):
     return f"k_spmm<4, {sc // 4}>" if F % 4 == 0 else f"k_spmm<1, {min(F, sc, 64)}>"
 
 
-def source_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def source_hash(path=KERNEL_SRC):
+    """Hash of the aggregation kernels' code with comments and whitespace
+    removed: a comment edit keeps stored counter figures valid, a code edit
+    voids them."""
+    import re
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    text = "".join(text.split())
+    return hashlib.sha256(text.encode()).hexdigest()[:16]
 
 
 def cpu_baseline(g, name, Fs, params, frac, seed=0):
