@@ -118,13 +118,50 @@ def cpu_baseline(g, name, Fs, params, frac, seed=0):
     scale = g.nnz / max(nnz_s, 1)
     t_step = t_plan + t_spmm * scale
     flops = sum(2.0 * g.nnz * F for F in Fs)
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {
         "value": round(flops / t_step / 1e9, 4), "unit": "GFLOP/s", "cores": 1, "kind": "oracle",
+        "cpu_model": model, "host_cpus": os.cpu_count(),
         "sample": (f"full oracle plan ({t_plan:.2f}s) + oracle SpMM over {rows.size} random rows "
                    f"({nnz_s} nnz, {100 * nnz_s / g.nnz:.1f}% of nnz) for F={Fs} "
                    f"({t_spmm:.2f}s), extrapolated by nnz to the full step"),
         "measured_s": round(t_plan + t_spmm, 3),
     }
+
+
+def cache_protocol(agcn, plan, Fs, Xs, Ys, ws, stream, reps, dev):
+    """Execute timings per F in the two cache states: cold (a 1 GiB buffer is
+    written before every rep, outside the events, so X, the CSR and Y start
+    outside L2 and the Infinity Cache) and warm (reps back to back).
+    Median, p10 and p90 of the per-rep times, in ms."""
+    import torch
+    flush = torch.empty(256 * 2**20, dtype=torch.float32, device=dev)
+    sh = stream.cuda_stream
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    out = {}
+    for F in Fs:
+        res = {}
+        for mode in ("cold", "warm"):
+            marks = [(ev(), ev()) for _ in range(reps)]
+            for a, b in marks:
+                if mode == "cold":
+                    flush.fill_(float(len(res)))
+                a.record(stream)
+                agcn.agcn_spmm(plan, F, Xs[F].data_ptr(), F, Ys[F].data_ptr(), F, ws.data_ptr(), sh)
+                b.record(stream)
+            torch.cuda.synchronize()
+            t = np.array([a.elapsed_time(b) for a, b in marks])
+            res[mode] = {"median_ms": round(float(np.median(t)), 5),
+                         "p10_ms": round(float(np.percentile(t, 10)), 5),
+                         "p90_ms": round(float(np.percentile(t, 90)), 5)}
+        out[F] = res
+    del flush
+    return out
 
 
 ROCSPARSE_ALGS = {"default": 0, "csr": 1, "csr_row_split": 4, "csr_nnz_split": 5, "csr_merge_path": 9}
@@ -303,6 +340,8 @@ def main():
                     help="time one GCNConv layer forward (linear + aggregation + ReLU)")
     ap.add_argument("--fin", type=int, default=128)
     ap.add_argument("--fout", type=int, default=128)
+    ap.add_argument("--cache-reps", type=int, default=20,
+                    help="reps per F for the cold/warm execute protocol (0 skips it)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-frac", type=float, default=0.4)
     ap.add_argument("--copy-probe", action="store_true",
@@ -467,6 +506,13 @@ def main():
         "per_F": per_f,
         "roofline": roofline,
     }
+    if args.cache_reps > 0:
+        log("cold / warm execute protocol ...")
+        plan = agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
+                                     d_colidx.data_ptr(), d_vals.data_ptr(), prm, sh)
+        out["execute_cold_warm"] = cache_protocol(agcn, plan, Fs, Xs, Ys, ws, stream,
+                                                  args.cache_reps, dev)
+        agcn.agcn_plan_destroy(plan)
     if args.rocsparse:
         log("rocSPARSE comparison ...")
         rs = rocsparse_compare(g, Fs, Xs, Ys, d_rowptr, d_colidx, d_vals, stream, reps=10)
