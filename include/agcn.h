@@ -15,7 +15,12 @@
  *                     the block's column indices and values, warp workloads
  *                     deduced from the block's metadata entry, lanes laid
  *                     across F ("combined warp"), fixed-order partial sums
- *                     in place of the paper's atomics.
+ *                     in place of the paper's atomics. agcn_spmm_ex adds the
+ *                     layer's activation at the Y writes.
+ *
+ * and, for a whole GCNConv layer (Sec. II-A), agcn_linear (X W on the matrix
+ * cores, no plan needed) and agcn_gcn_layer (linear, then the aggregation
+ * with the activation).
  *
  * Conventions for every call:
  *   - Pointers named d_* are device pointers (memory of the current HIP
