@@ -224,15 +224,19 @@ int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* out);
 int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s,
                      int32_t* h_colidx_s, float* h_vals_s, int32_t* h_meta);
 
-/* Releases the plan. Synchronises the plan's device first, so work still
- * queued on any stream finishes before the memory is reused. The device
- * block is kept in a per-device cache (one block per device) that the next
- * agcn_plan_create on that device reuses when it fits; see
- * agcn_release_cached_memory. NULL is ignored. */
+/* Releases the plan without blocking. Its device block is kept in a
+ * per-device cache (one block per device) together with events that mark the
+ * plan's last work on every stream that used it (its creation and each
+ * agcn_spmm* / agcn_gcn_layer call). The next agcn_plan_create on that device
+ * that reuses the block makes its own stream wait on those events, so work
+ * still queued with the old plan finishes before the memory is overwritten;
+ * see agcn_release_cached_memory. The plan must not be used after this call.
+ * NULL is ignored. */
 void agcn_plan_destroy(agcn_plan_t plan);
 
-/* Frees the device memory cached by destroyed plans, on every device. Plans
- * that are still alive are not affected. */
+/* Frees the device memory cached by destroyed plans, on every device, after
+ * waiting (on the host) for the work those plans still had queued. Plans that
+ * are still alive are not affected. */
 void agcn_release_cached_memory(void);
 
 /* Static text for a status code. */

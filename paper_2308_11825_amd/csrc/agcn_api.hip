@@ -52,14 +52,29 @@ int hip_fail(hipError_t e, const char* what) {
 // same graph re-planned) would otherwise pay a hipMalloc and a hipFree --
 // which synchronises the device -- each time. A destroyed plan's block stays
 // cached, one block per device, and the next plan on that device reuses it
-// when it fits without wasting more than half of it.
+// when it fits without wasting more than half of it. The block travels with
+// events marking its previous owner's last work on every stream; the reusing
+// plan's stream waits on them, so nothing blocks on the host.
 namespace {
 struct CachedBlock {
   void* ptr = nullptr;
   size_t bytes = 0;
+  std::vector<hipEvent_t> pending;
 };
 std::mutex g_cache_mu;
 std::map<int, CachedBlock> g_cache;
+
+// Frees a block no plan will reuse (the caller has made its device current).
+void free_block(CachedBlock& b) {
+  for (hipEvent_t ev : b.pending) {
+    (void)hipEventSynchronize(ev);
+    (void)hipEventDestroy(ev);
+  }
+  b.pending.clear();
+  if (b.ptr) (void)hipFree(b.ptr);
+  b.ptr = nullptr;
+  b.bytes = 0;
+}
 
 int with_device(int device, int* prev) {
   hipError_t e = hipGetDevice(prev);
@@ -69,17 +84,28 @@ int with_device(int device, int* prev) {
 }
 }  // namespace
 
-int device_alloc(int device, size_t bytes, void** out, size_t* got) {
+int device_alloc(int device, size_t bytes, hipStream_t stream, void** out, size_t* got) {
+  CachedBlock reuse;
   {
     std::lock_guard<std::mutex> lk(g_cache_mu);
     auto it = g_cache.find(device);
     if (it != g_cache.end() && it->second.ptr != nullptr && it->second.bytes >= bytes &&
         it->second.bytes / 2 <= bytes) {
-      *out = it->second.ptr;
-      *got = it->second.bytes;
+      reuse = std::move(it->second);
       it->second = CachedBlock{};
-      return AGCN_OK;
     }
+  }
+  if (reuse.ptr != nullptr) {
+    for (hipEvent_t ev : reuse.pending) {
+      if (hipStreamWaitEvent(stream, ev, 0) != hipSuccess) {
+        (void)hipGetLastError();
+        (void)hipEventSynchronize(ev);
+      }
+      (void)hipEventDestroy(ev);
+    }
+    *out = reuse.ptr;
+    *got = reuse.bytes;
+    return AGCN_OK;
   }
   void* p = nullptr;
   hipError_t e = hipMalloc(&p, bytes);
@@ -89,10 +115,10 @@ int device_alloc(int device, size_t bytes, void** out, size_t* got) {
     CachedBlock old;
     {
       std::lock_guard<std::mutex> lk(g_cache_mu);
-      old = g_cache[device];
+      old = std::move(g_cache[device]);
       g_cache[device] = CachedBlock{};
     }
-    if (old.ptr) (void)hipFree(old.ptr);
+    free_block(old);
     e = hipMalloc(&p, bytes);
   }
   if (e != hipSuccess) {
@@ -106,25 +132,47 @@ int device_alloc(int device, size_t bytes, void** out, size_t* got) {
   return AGCN_OK;
 }
 
-void device_release(int device, void* ptr, size_t bytes) {
-  if (ptr == nullptr) return;
+void device_release(int device, void* ptr, size_t bytes, std::vector<hipEvent_t> pending) {
   int prev = 0;
   if (with_device(device, &prev) != AGCN_OK) return;
-  // Kernels of this plan may still run on any stream: wait for all of them.
-  (void)hipDeviceSynchronize();
+  CachedBlock incoming{ptr, bytes, std::move(pending)};
   CachedBlock evict;
-  {
+  if (ptr == nullptr) {
+    evict = std::move(incoming);
+  } else {
     std::lock_guard<std::mutex> lk(g_cache_mu);
     CachedBlock& slot = g_cache[device];
     if (slot.ptr == nullptr || slot.bytes <= bytes) {
-      evict = slot;
-      slot = CachedBlock{ptr, bytes};
+      evict = std::move(slot);
+      slot = std::move(incoming);
     } else {
-      evict = CachedBlock{ptr, bytes};
+      evict = std::move(incoming);
     }
   }
-  if (evict.ptr) (void)hipFree(evict.ptr);
+  free_block(evict);
   if (prev != device) (void)hipSetDevice(prev);
+}
+
+void note_use(agcn_plan* p, hipStream_t stream) {
+  std::lock_guard<std::mutex> lk(p->use_mu);
+  for (auto& u : p->uses) {
+    if (u.first == stream) {
+      if (hipEventRecord(u.second, stream) != hipSuccess) {
+        (void)hipGetLastError();
+        p->sync_on_release = true;
+      }
+      return;
+    }
+  }
+  hipEvent_t ev = nullptr;
+  if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess ||
+      hipEventRecord(ev, stream) != hipSuccess) {
+    (void)hipGetLastError();
+    if (ev) (void)hipEventDestroy(ev);
+    p->sync_on_release = true;
+    return;
+  }
+  p->uses.emplace_back(stream, ev);
 }
 
 }  // namespace agcn
@@ -157,8 +205,17 @@ const char* agcn_last_error(void) { return agcn::g_last_error.c_str(); }
 
 static void plan_free(agcn_plan* p) {
   if (p == nullptr) return;
-  agcn::device_release(p->device, p->base, p->bytes);
-  if (p->ready != nullptr) (void)hipEventDestroy(p->ready);
+  std::vector<hipEvent_t> pending;
+  if (p->ready != nullptr) pending.push_back(p->ready);
+  for (auto& u : p->uses) pending.push_back(u.second);
+  if (p->sync_on_release) {
+    int prev = 0;
+    if (agcn::with_device(p->device, &prev) == AGCN_OK) {
+      (void)hipDeviceSynchronize();
+      if (prev != p->device) (void)hipSetDevice(prev);
+    }
+  }
+  agcn::device_release(p->device, p->base, p->bytes, std::move(pending));
   delete p;
 }
 
@@ -169,10 +226,10 @@ void agcn_release_cached_memory(void) {
     blocks.swap(agcn::g_cache);
   }
   for (auto& kv : blocks) {
-    if (kv.second.ptr == nullptr) continue;
+    if (kv.second.ptr == nullptr && kv.second.pending.empty()) continue;
     int prev = 0;
     if (agcn::with_device(kv.first, &prev) != AGCN_OK) continue;
-    (void)hipFree(kv.second.ptr);
+    agcn::free_block(kv.second);
     if (prev != kv.first) (void)hipSetDevice(prev);
   }
 }
@@ -292,9 +349,12 @@ int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
                       agcn::ranges_overlap(d_ws, ws_need, d_X, xb)))
     return fail(AGCN_ERR_INVALID_ARGUMENT, "workspace overlaps X or Y");
   if (int rc = check_device(plan)) return rc;
-  return agcn::run_spmm(plan, F, d_X, ldx, d_Y, ldy, static_cast<float*>(d_ws),
-                        static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(ev_begin),
-                        static_cast<hipEvent_t>(ev_mid), static_cast<hipEvent_t>(ev_end), epilogue);
+  const int rc = agcn::run_spmm(plan, F, d_X, ldx, d_Y, ldy, static_cast<float*>(d_ws),
+                                static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(ev_begin),
+                                static_cast<hipEvent_t>(ev_mid), static_cast<hipEvent_t>(ev_end),
+                                epilogue);
+  agcn::note_use(plan, static_cast<hipStream_t>(stream));  // also after a failed launch
+  return rc;
 }
 
 // Bytes of the transformed features H (n_cols x fout floats) at the start of

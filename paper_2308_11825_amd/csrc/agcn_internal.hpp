@@ -5,7 +5,10 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <mutex>
 #include <string>
+#include <utility>
+#include <vector>
 
 #include "../../include/agcn.h"
 
@@ -56,6 +59,12 @@ struct agcn_plan {
   int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
   int32_t* group_off = nullptr;     // warp-level plans: [n_rows + 1] first group of each row
   hipEvent_t ready = nullptr;       // recorded after the launch order is built
+  // Last work of the plan on each stream that ran an execute with it (one
+  // event per stream, re-recorded by every call; guarded by use_mu). A later
+  // plan that reuses this memory makes its stream wait on them.
+  std::mutex use_mu;
+  std::vector<std::pair<hipStream_t, hipEvent_t>> uses;
+  bool sync_on_release = false;     // an event could not be created: release waits on the device
 };
 
 namespace agcn {
@@ -87,10 +96,15 @@ int run_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx
 size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz);
 
 // Plan memory. device_alloc may hand back the block a destroyed plan left in
-// the per-device cache (*got receives its size, >= bytes); device_release
-// synchronises the device and keeps the block cached (one per device).
-int device_alloc(int device, size_t bytes, void** out, size_t* got);
-void device_release(int device, void* ptr, size_t bytes);
+// the per-device cache (*got receives its size, >= bytes); `stream` then
+// waits (device-side) on the events that mark the previous owner's last work.
+// device_release keeps the block cached (one per device) with those events and
+// takes ownership of them; it does not block.
+int device_alloc(int device, size_t bytes, hipStream_t stream, void** out, size_t* got);
+void device_release(int device, void* ptr, size_t bytes, std::vector<hipEvent_t> pending);
+
+// Records, on `stream`, the event that marks the plan's last work there.
+void note_use(agcn_plan* p, hipStream_t stream);
 
 inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; }

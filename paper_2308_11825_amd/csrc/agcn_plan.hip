@@ -881,7 +881,7 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   const size_t o_dmax = L.take(64);
   void* base = nullptr;
   size_t got = 0;
-  int rc = device_alloc(p->device, L.off, &base, &got);
+  int rc = device_alloc(p->device, L.off, st, &base, &got);
   if (rc) return rc;
   char* b = static_cast<char*>(base);
   p->base = base;
@@ -976,7 +976,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
 
   void* base = nullptr;
   size_t got = 0;
-  int rc = device_alloc(p->device, L.off, &base, &got);
+  int rc = device_alloc(p->device, L.off, st, &base, &got);
   if (rc) return rc;
   char* b = static_cast<char*>(base);
   p->base = base;

@@ -265,6 +265,35 @@ def test_plan_memory_reused_across_plans():
     p3.destroy()
 
 
+def test_destroy_while_executing_then_reuse_on_another_stream():
+    """agcn_plan_destroy does not block; a plan that reuses the destroyed
+    plan's cached memory on another stream must wait for the work still
+    queued with the old plan (it would otherwise overwrite the sorted CSR the
+    running execute reads)."""
+    g1 = _mixed(81, n=40000, hub_max=8000)
+    g2 = _mixed(82, n=39000, hub_max=8000)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    agcn.agcn_release_cached_memory()
+    p1 = _plan(g1, stream=s1)
+    F = 512
+    X1 = np.random.default_rng(83).standard_normal((g1.n_cols, F)).astype(np.float32)
+    X1d = _dev(X1)
+    ws1 = p1.workspace(F)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        Y1 = torch.empty((g1.n_rows, F), device=DEV)
+        for _ in range(3):      # several launches keep s1 busy for a while
+            p1.spmm(X1d, out=Y1, ws=ws1, stream=s1)
+    p1.destroy()
+    p2 = _plan(g2, stream=s2)   # reuses p1's block: s2 waits on s1's last execute
+    assert_plan_matches_oracle(p2, g2)
+    torch.cuda.synchronize()
+    Y, S = oracle.spmm(g1.rowptr, g1.colidx, g1.vals, X1, want_scale=True)
+    assert_close(Y1.cpu().numpy(), Y, S, "execute of the destroyed plan")
+    _spmm_check(p2, g2, 64)
+    p2.destroy()
+
+
 def test_long_hub_rows_column_ordered_launch():
     """Hub rows of tens of thousands of nnz (many chunks each) take the
     column-ordered launch path; Y must still match the oracle everywhere."""
