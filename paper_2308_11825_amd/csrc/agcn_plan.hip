@@ -1,11 +1,9 @@
 // Device-side preprocessing: degree sort and block-level partition
 // (Sec. III-C "Degree Sorting" and "Block-level Partition", Alg. 1 and Alg. 2).
 //
-// Pipeline (all on one stream, one host synchronisation at the end):
+// Pipeline (all on one stream; the host waits twice: on an event once the
+// maximum degree is known, and on the stream before the launch order):
 //   k_init          clear the error word and the maximum degree
-// The two read-backs (maximum degree, summary) are written by the kernels
-// straight into pinned, host-coherent memory; the host reads them after an
-// event or stream synchronisation, with no copy launched.
 //   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
 //                   per-workgroup maximum degree
 //   k_dmax          maximum degree (one workgroup); copied to pinned host
@@ -27,9 +25,19 @@
 //                   column (two radix passes, when hub rows are long), then
 //                   the other entries heaviest first; an event marks it ready
 //
+// The two read-backs (maximum degree, summary) are written by the kernels
+// straight into pinned, host-coherent memory; the host reads them after the
+// event or stream synchronisation, with no copy launched.
+//
 // Stability of the radix sort comes from giving each 64-lane wave a tile of
 // consecutive rows that it walks in order, ranking equal digits inside a
 // round with ballots; every count is an integer, so the result is exact.
+//
+// The warp-level plan of the ablation (Table II) has its own short pipeline:
+// k_degree and k_dmax as above, k_wl_groups (groups per row), k_wl_copy (the
+// CSR copied in input order, columns checked, identity permutation), a scan
+// of the group counts, k_wl_fill (one {row, first nnz, count, 0} per group)
+// and k_wl_summary.
 #include <algorithm>
 #include <climits>
 #include <cstdlib>
