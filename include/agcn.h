@@ -147,6 +147,9 @@ int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes);
  * Result: bitwise reproducible run to run; no atomics.
  * The plan is read-only here: concurrent calls on different streams are
  * safe when each has its own Y and ws. Must run on the plan's device.
+ * The call launches kernels only (no allocation, no memset, no host wait), so
+ * it may be captured into a HIP graph; the plan must then outlive every
+ * replay of that graph.
  * Errors: INVALID_ARGUMENT (null plan or pointers, F < 1, ld < F, overlap,
  * missing workspace, wrong device), UNSUPPORTED (AGCN_PLAN_COLUMN_LOOP plans
  * when W * F * 4 bytes of partial rows plus the staged entry exceed 64 KiB
