@@ -312,3 +312,49 @@ def test_long_hub_rows_column_ordered_launch():
     X = _dev(np.random.default_rng(1).standard_normal((n, 64)).astype(np.float32))
     assert np.array_equal(plan.spmm(X).cpu().numpy(), plan.spmm(X).cpu().numpy())
     plan.destroy()
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("flags", [0, agcn.AGCN_PLAN_WARP_LEVEL])
+def test_nnz_just_below_the_int32_limit(flags):
+    """The largest matrix the int32 format holds: nnz = 2^31 - 3 over about
+    1.9 M rows of mixed degree (empty, small, the deg_bound edges, hubs of
+    several chunks). Entry counts checked against the closed forms, Y on
+    sampled rows (first, last, every degree) against the oracle."""
+    pattern = np.array([0, 1, 7, 64, 511, 512, 513, 2000, 4000], np.int64)
+    n_cols = 1 << 20
+    target = (1 << 31) - 3
+    reps = target // int(pattern.sum())
+    deg = np.tile(pattern, reps)
+    deg = np.append(deg, target - int(deg.sum()))          # last row takes the remainder
+    n = deg.size
+    rowptr = np.zeros(n + 1, np.int64)
+    np.cumsum(deg, out=rowptr[1:])
+    assert rowptr[-1] == target
+    rowptr = rowptr.astype(np.int32)
+    rng = np.random.default_rng(97)
+    colidx = rng.integers(0, n_cols, size=target, dtype=np.int32)
+    vals = rng.random(target, dtype=np.float32)
+    print(f"[max] n={n} nnz={target} flags={flags}", flush=True)
+    d_rp, d_ci, d_v = _dev(rowptr), _dev(colidx), _dev(vals)
+    plan = agcn.Plan(d_rp, d_ci, d_v, n_cols=n_cols, flags=flags)
+    s = plan.stats
+    assert s.nnz == target and s.max_deg == int(deg.max())
+    Z = s.max_wave_nzs
+    if flags:
+        assert s.n_entries == int(np.maximum(1, -(-deg // Z)).sum())
+    else:
+        assert s.n_hub_rows == int((deg > s.deg_bound).sum())
+        assert s.n_hub_chunks == int(-(-deg[deg > s.deg_bound] // s.hub_chunk_nnz).sum())
+    del d_ci, d_v
+    F = 8
+    X = rng.standard_normal((n_cols, F)).astype(np.float32)
+    Yg = plan.spmm(_dev(X)).cpu().numpy()
+    rows = np.unique(np.concatenate([np.arange(len(pattern)), np.arange(n - 20, n),
+                                     rng.choice(n, 400, replace=False)])).astype(np.int32)
+    g = graphgen.Graph("max", n, n_cols, rowptr, colidx, vals)
+    Yr, Sr = oracle.spmm_rows(g.rowptr, g.colidx, g.vals, X, rows, n_cols=n_cols)
+    assert_close(Yg[rows], Yr, Sr, f"nnz=2^31-3 flags={flags}")
+    print(f"[max] ok ({rows.size} rows checked)", flush=True)
+    plan.destroy()
+    agcn.agcn_release_cached_memory()
