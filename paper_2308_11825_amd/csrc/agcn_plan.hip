@@ -819,7 +819,9 @@ PlanSummary* pinned_summary(PlanSummary** dev) {
   thread_local PlanSummary* dbuf = nullptr;
   if (buf == nullptr) {
     void* q = nullptr;
-    if (hipHostMalloc(&q, sizeof(PlanSummary), hipHostMallocMapped | hipHostMallocCoherent) !=
+    // Portable: one buffer serves plans built on any device from this thread.
+    if (hipHostMalloc(&q, sizeof(PlanSummary),
+                      hipHostMallocMapped | hipHostMallocCoherent | hipHostMallocPortable) !=
         hipSuccess) {
       (void)hipGetLastError();
       return nullptr;
