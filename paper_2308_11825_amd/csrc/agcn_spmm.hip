@@ -276,7 +276,7 @@ __global__ __launch_bounds__(1024) void k_hub_reduce(const int32_t* __restrict__
 // the end); k_wl_fixup finishes those rows in workgroup order.
 template <int VW, int LT>
 __global__ __launch_bounds__(1024) void k_spmm_wl(
-    const int4* __restrict__ meta, int32_t n_groups, int32_t W,
+    const int4* __restrict__ meta, int32_t n_groups, int32_t W, int64_t block_base,
     const int32_t* __restrict__ colidx_s, const float* __restrict__ vals_s,
     const float* __restrict__ X, int64_t ldx, float* __restrict__ Y, int64_t ldy,
     float* __restrict__ ws, int32_t F, int32_t col_base, int32_t slice_cols, int32_t L_rt,
@@ -290,7 +290,8 @@ __global__ __launch_bounds__(1024) void k_spmm_wl(
   __shared__ int4 s_meta[kMaxBlockWaves];
   __shared__ int32_t s_prev_row, s_next_row;
   const int T = blockDim.x;
-  const int32_t g0 = (int32_t)blockIdx.x * W;
+  const int64_t blk = block_base + blockIdx.x;
+  const int32_t g0 = (int32_t)(blk * W);
   const int32_t nv = min(W, n_groups - g0);
   const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
   if (threadIdx.x < nv) s_meta[threadIdx.x] = meta[g0 + threadIdx.x];
@@ -344,7 +345,7 @@ __global__ __launch_bounds__(1024) void k_spmm_wl(
       const bool start_cut = v == 0 && s_prev_row == row;
       const bool end_cut = e == nv - 1 && s_next_row == row;
       if (start_cut || end_cut) {
-        V* wr = reinterpret_cast<V*>(ws + ((int64_t)blockIdx.x * 2 + (start_cut ? 0 : 1)) * F + col0);
+        V* wr = reinterpret_cast<V*>(ws + (blk * 2 + (start_cut ? 0 : 1)) * F + col0);
         wr[l] = sum;
       } else {
         V* yr = reinterpret_cast<V*>(Y + (int64_t)row * ldy + col0);
@@ -363,34 +364,36 @@ __global__ __launch_bounds__(256) void k_wl_fixup(const int32_t* __restrict__ go
                                                   int32_t col_base, int32_t slice_cols, int32_t L,
                                                   int32_t act) {
   using V = typename VecOf<VW>::T;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t r = t / L;
-  const int l = (int)(t - r * L);
-  if (r >= n_rows) return;
-  const int32_t b0 = goff[r] / W, b1 = (goff[r + 1] - 1) / W;
-  if (b0 == b1) return;
   const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
-  auto part = [&](int32_t b) {
-    const int slot = b == b0 ? 1 : 0;
-    return reinterpret_cast<const V*>(ws + ((int64_t)b * 2 + slot) * F + col0)[l];
-  };
-  V total = V(0.0f);
-  for (int32_t b = b0; b <= b1; b += 16) {
-    V run = part(b);
-    const int32_t e = b + 16 <= b1 + 1 ? b + 16 : b1 + 1;
-    for (int32_t q = b + 1; q < e; ++q) run += part(q);
-    total = b == b0 ? run : total + run;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < (int64_t)n_rows * L;
+       t += stride) {
+    const int64_t r = t / L;
+    const int l = (int)(t - r * L);
+    const int32_t b0 = goff[r] / W, b1 = (goff[r + 1] - 1) / W;
+    if (b0 == b1) continue;
+    auto part = [&](int32_t b) {
+      const int slot = b == b0 ? 1 : 0;
+      return reinterpret_cast<const V*>(ws + ((int64_t)b * 2 + slot) * F + col0)[l];
+    };
+    V total = V(0.0f);
+    for (int32_t b = b0; b <= b1; b += 16) {
+      V run = part(b);
+      const int32_t e = b + 16 <= b1 + 1 ? b + 16 : b1 + 1;
+      for (int32_t q = b + 1; q < e; ++q) run += part(q);
+      total = b == b0 ? run : total + run;
+    }
+    V* yr = reinterpret_cast<V*>(Y + r * ldy + col0);
+    __builtin_nontemporal_store(act_v(total, act), yr + l);
   }
-  V* yr = reinterpret_cast<V*>(Y + r * ldy + col0);
-  __builtin_nontemporal_store(act_v(total, act), yr + l);
 }
 
 // Block-level partition without the combined warp: every vwarp is one
 // 64-lane wave, one float per lane, and loops over F in strips of 64 columns.
 // Split rows and hub chunks keep one F-wide partial per vwarp in LDS.
 __global__ __launch_bounds__(1024) void k_spmm_colloop(
-    const int4* __restrict__ meta, const int32_t* __restrict__ order, int32_t hub_first_entry,
-    int32_t deg_bound, int32_t W, const int32_t* __restrict__ colidx_s,
+    const int4* __restrict__ meta, const int32_t* __restrict__ order, int32_t entry_base,
+    int32_t hub_first_entry, int32_t deg_bound, int32_t W, const int32_t* __restrict__ colidx_s,
     const float* __restrict__ vals_s, const int32_t* __restrict__ perm, const float* __restrict__ X,
     int64_t ldx, float* __restrict__ Y, int64_t ldy, float* __restrict__ ws, int32_t F,
     int32_t rounds, int32_t cap_pad, int32_t act) {
@@ -399,7 +402,7 @@ __global__ __launch_bounds__(1024) void k_spmm_colloop(
   float* s_val = smem + cap_pad;
   float* s_part = smem + 2 * cap_pad;  // [W][F]
   const int T = blockDim.x;
-  const int32_t b = order[blockIdx.x];
+  const int32_t b = order[entry_base + (int32_t)blockIdx.x];
   const int4 m = meta[b];
   const int32_t deg = m.x, loc = m.y, row = m.z, info = m.w;
   const bool hub = deg > deg_bound;
@@ -594,12 +597,17 @@ void launch_wl(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_c
   const int T = std::min(1024, std::max(64, round_up(want, 64)));
   const int rounds = (want + T - 1) / T;
   const size_t lds = (size_t)2 * cap_pad * 4 + (size_t)part_floats(VW, p->W, L) * 4;
-  dim3 grid((unsigned)warp_level_blocks(p), (unsigned)n_slices);
-  const hipEvent_t stop = last_part ? mk.stop : nullptr;
-  hipExtLaunchKernelGGL(k_spmm_wl<VW, LT>, grid, dim3(T), (uint32_t)lds, a.st, mk.start, stop, 0,
-                        p->meta, p->n_entries, p->W, p->colidx_s, p->vals_s, a.X, a.ldx, a.Y,
-                        a.ldy, a.ws, a.F, col_base, slice_cols, L, rounds, cap_pad, a.act);
-  mk.start = nullptr;
+  const int64_t blocks = warp_level_blocks(p);
+  const int64_t max_grid = (int64_t)(UINT32_MAX / (uint32_t)T);
+  for (int64_t b0 = 0; b0 < blocks; b0 += max_grid) {
+    const int64_t cnt = std::min<int64_t>(max_grid, blocks - b0);
+    const hipEvent_t stop = (last_part && b0 + cnt >= blocks) ? mk.stop : nullptr;
+    hipExtLaunchKernelGGL(k_spmm_wl<VW, LT>, dim3((unsigned)cnt, (unsigned)n_slices), dim3(T),
+                          (uint32_t)lds, a.st, mk.start, stop, 0, p->meta, p->n_entries, p->W, b0,
+                          p->colidx_s, p->vals_s, a.X, a.ldx, a.Y, a.ldy, a.ws, a.F, col_base,
+                          slice_cols, L, rounds, cap_pad, a.act);
+    mk.start = nullptr;
+  }
 }
 
 template <int VW>
@@ -623,7 +631,8 @@ int run_warp_level(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "k_spmm_wl launch");
     const int rows_per_block = std::max(1, 256 / L);
-    dim3 fgrid((unsigned)ceil_div64(p->n_rows, rows_per_block), (unsigned)n_slices);
+    dim3 fgrid((unsigned)std::min<int64_t>(ceil_div64(p->n_rows, rows_per_block), 1 << 20),
+               (unsigned)n_slices);
     k_wl_fixup<VW><<<fgrid, rows_per_block * L, 0, a.st>>>(p->group_off, p->n_rows, p->W, a.ws, a.F,
                                                            a.Y, a.ldy, col_base, sc, L, a.act);
     if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_wl_fixup launch");
@@ -643,10 +652,16 @@ int run_colloop(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
   const int T = std::min(1024, want);
   const int rounds = (want + T - 1) / T;
   hipError_t e;
-  hipExtLaunchKernelGGL(k_spmm_colloop, dim3((unsigned)p->n_entries), dim3(T), (uint32_t)lds, a.st,
-                        mk.start, mk.stop, 0, p->meta, p->order, p->hub_first_entry, p->deg_bound,
-                        p->W, p->colidx_s, p->vals_s, p->perm, a.X, a.ldx, a.Y, a.ldy, a.ws, a.F,
-                        rounds, cap_pad, a.act);
+  const int64_t max_grid = (int64_t)(UINT32_MAX / (uint32_t)T);
+  for (int64_t e0 = 0; e0 < p->n_entries; e0 += max_grid) {
+    const int64_t cnt = std::min<int64_t>(max_grid, p->n_entries - e0);
+    const hipEvent_t stop = e0 + cnt >= p->n_entries ? mk.stop : nullptr;
+    hipExtLaunchKernelGGL(k_spmm_colloop, dim3((unsigned)cnt), dim3(T), (uint32_t)lds, a.st,
+                          mk.start, stop, 0, p->meta, p->order, (int32_t)e0, p->hub_first_entry,
+                          p->deg_bound, p->W, p->colidx_s, p->vals_s, p->perm, a.X, a.ldx, a.Y,
+                          a.ldy, a.ws, a.F, rounds, cap_pad, a.act);
+    mk.start = nullptr;
+  }
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_spmm_colloop launch");
   if (p->n_hub_rows > 0) {
     const int L = std::min(64, a.F);
