@@ -301,16 +301,22 @@ class Plan:
     def workspace_bytes(self, F: int) -> int:
         return agcn_spmm_workspace_size(self.handle, F)
 
-    def workspace(self, F: int):
-        """A cached device workspace for feature width F (None if not needed)."""
+    def workspace(self, F: int, stream=None):
+        """A cached device workspace for feature width F on `stream` (None if
+        not needed). One per stream, so executes on different streams never
+        share hub-row partials."""
         import torch
         nb = self.workspace_bytes(F)
         if nb == 0:
             return None
-        ws = self._ws.get(F)
+        key = (F, stream.cuda_stream if stream is not None else _stream_handle(self.device))
+        ws = self._ws.get(key)
         if ws is None:
-            ws = torch.empty((nb + 3) // 4, dtype=torch.float32, device=self.device)
-            self._ws[F] = ws
+            # allocated on the stream that uses it, so torch's allocator orders
+            # any later reuse of the memory after that stream's work
+            with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream(self.device)):
+                ws = torch.empty((nb + 3) // 4, dtype=torch.float32, device=self.device)
+            self._ws[key] = ws
         return ws
 
     def spmm(self, X, out=None, ws=None, stream=None, act=None):
@@ -329,7 +335,7 @@ class Plan:
                 or out.dtype != torch.float32 or out.device != self.device):
             raise ValueError("out must be a float32 (n_rows, F) tensor with unit column stride")
         if ws is None:
-            ws = self.workspace(F)
+            ws = self.workspace(F, stream)
         st = stream.cuda_stream if stream is not None else _stream_handle(self.device)
         with torch.cuda.device(self.device):
             agcn_spmm_ex(self.handle, F, X.data_ptr(), _row_stride(X), out.data_ptr(),
