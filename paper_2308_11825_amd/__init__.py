@@ -361,7 +361,8 @@ class Plan:
             raise ValueError("out must be a float32 (n_rows, fout) tensor with unit column stride")
         if ws is None:
             nb = agcn_gcn_workspace_size(self.handle, fout)
-            ws = torch.empty((nb + 3) // 4, dtype=torch.float32, device=self.device)
+            with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream(self.device)):
+                ws = torch.empty((nb + 3) // 4, dtype=torch.float32, device=self.device)
         st = stream.cuda_stream if stream is not None else _stream_handle(self.device)
         with torch.cuda.device(self.device):
             agcn_gcn_layer(self.handle, fin, fout, X.data_ptr(), _row_stride(X), W.data_ptr(),
