@@ -27,6 +27,22 @@ PARAM_SETS = [dict(), dict(max_block_waves=12, max_wave_nzs=32), dict(max_block_
               max_wave_nzs=64), dict(max_block_waves=16, max_wave_nzs=32, hub_chunk_nnz=1000),
               dict(max_block_waves=2, max_wave_nzs=2), dict(max_block_waves=6, max_wave_nzs=3)]
 
+# Parameter extremes: the widest block (W = 32), the largest block (W Z = 4096),
+# the largest hub chunk, a single vwarp per block.
+EXTREME_PARAMS = [dict(max_block_waves=32, max_wave_nzs=64), dict(max_block_waves=4, max_wave_nzs=1024),
+                  dict(max_block_waves=16, max_wave_nzs=32, hub_chunk_nnz=4096),
+                  dict(max_block_waves=1, max_wave_nzs=1), dict(max_block_waves=1, max_wave_nzs=512)]
+
+
+@pytest.mark.parametrize("kw", EXTREME_PARAMS)
+def test_parameter_extremes_plan_and_spmm(kw):
+    g = _mixed(13, n=6000, hub_max=9000, dupes=True)
+    plan = _plan(g, **kw)
+    assert_plan_matches_oracle(plan, g)
+    for F in (2, 5, 32, 48, 100):
+        _spmm_check(plan, g, F, seed=F)
+    plan.destroy()
+
 
 @pytest.mark.parametrize("kw", PARAM_SETS)
 @pytest.mark.parametrize("seed", [0, 1])
@@ -98,7 +114,8 @@ def mixed_plan():
     plan.destroy()
 
 
-@pytest.mark.parametrize("F", [1, 3, 4, 8, 16, 17, 32, 64, 96, 128, 256, 257, 320, 512])
+@pytest.mark.parametrize("F", [1, 2, 3, 4, 5, 8, 16, 17, 32, 33, 48, 64, 96, 128, 256, 257, 320,
+                               512, 1024])
 def test_spmm_matches_oracle(mixed_plan, F):
     g, plan = mixed_plan
     _spmm_check(plan, g, F, seed=F)
