@@ -48,9 +48,17 @@ def assert_plan_matches_oracle(plan, g):
 
 
 def assert_close(Yg, Y, S, what=""):
-    err = np.abs(Yg.astype(np.float64) - Y.astype(np.float64))
+    """Per element |Yg - Y| <= RTOL * S + ATOL. A NaN or infinity on either
+    side must be the same non-finite value on the other (a NaN error would
+    otherwise compare as within tolerance)."""
+    assert Yg.shape == Y.shape, (what, Yg.shape, Y.shape)
+    yg, y = Yg.astype(np.float64), Y.astype(np.float64)
+    fin = np.isfinite(yg) & np.isfinite(y)
+    same_nonfinite = (np.isnan(yg) & np.isnan(y)) | (~fin & (yg == y))
+    with np.errstate(invalid="ignore"):   # inf - inf where not both finite: masked below
+        err = np.where(fin, np.abs(yg - y), 0.0)
     tol = RTOL * S + ATOL
-    bad = err > tol
+    bad = (err > tol) | (~fin & ~same_nonfinite)
     if bad.any():
         i = np.argwhere(bad)[0]
         raise AssertionError(f"{what}: {int(bad.sum())} elements out of tolerance; first at {tuple(i)}: "

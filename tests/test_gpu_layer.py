@@ -33,7 +33,7 @@ def _check_linear(X, W, H, what=""):
     S = np.abs(X.astype(np.float64)) @ np.abs(W.astype(np.float64))
     err = np.abs(H.astype(np.float64) - Hr.astype(np.float64))
     tol = (fin + 2) * U * S + 1e-30
-    bad = err > tol
+    bad = ~(err <= tol)                    # NaN counts as out of tolerance
     assert not bad.any(), (f"{what}: {int(bad.sum())} out of tolerance; first "
                            f"{tuple(np.argwhere(bad)[0])}")
 
@@ -108,7 +108,7 @@ def _check_layer(plan, g, X, W, act, rows=None, Yg=None):
     Yc = Yg if rows is None else Yg[rows]
     err = np.abs(Yc.astype(np.float64) - Yr.astype(np.float64))
     tol = (1e-5 + (fin + 3) * U) * S2 + 1e-7
-    bad = err > tol
+    bad = ~(err <= tol)                    # NaN counts as out of tolerance
     assert not bad.any(), (f"layer act={act}: {int(bad.sum())} out of tolerance; first "
                            f"{tuple(np.argwhere(bad)[0])}")
     return Yg

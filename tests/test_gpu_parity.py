@@ -181,6 +181,25 @@ def test_row_permutation_equivariance_bit_exact():
     pb.destroy()
 
 
+def test_non_finite_features_propagate_like_the_oracle(mixed_plan):
+    """NaN and infinite X rows reach exactly the Y elements the definition
+    says (NaN anywhere -> NaN, +inf with -inf -> NaN, +inf alone -> +inf),
+    also through the ReLU epilogue (NaN kept, -inf -> 0)."""
+    g, plan = mixed_plan
+    rng = np.random.default_rng(17)
+    F = 12
+    X = rng.standard_normal((g.n_cols, F)).astype(np.float32)
+    X[rng.choice(g.n_cols, 40, replace=False)] = np.nan
+    X[rng.choice(g.n_cols, 40, replace=False), :6] = np.inf
+    X[rng.choice(g.n_cols, 40, replace=False), 3:9] = -np.inf
+    Y, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, want_scale=True)
+    assert np.isnan(Y).any() and np.isinf(Y).any()
+    Xd = _dev(X)
+    assert_close(plan.spmm(Xd).cpu().numpy(), Y, np.nan_to_num(S), "non-finite")
+    Yr = np.where(Y < 0, np.float32(0), Y)
+    assert_close(plan.spmm(Xd, act="relu").cpu().numpy(), Yr, np.nan_to_num(S), "non-finite relu")
+
+
 def test_ones_gives_row_sums(mixed_plan):
     g, plan = mixed_plan
     X = np.ones((g.n_cols, 4), np.float32)
