@@ -481,6 +481,11 @@ def main():
                 "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "kernel": dom, "launches_per_step": len(dom_F), "F": dom_F,
                 "alg_bytes_per_launch": int(mean_bytes), "avg_launch_ms": round(mean_ms, 5)}
+    if traffic is not None:
+        # the counter-measured bytes past L2 (Infinity Cache hits included) over the same time
+        tg = traffic / (mean_ms * 1e-3) / 1e9
+        roofline["traffic_GBps"] = round(tg, 1)
+        roofline["traffic_frac"] = round(tg / HBM_PEAK_GBPS, 4)
 
     if args.copy_probe:
         src = torch.empty(256 * 2**20, dtype=torch.float32, device=dev).fill_(1.0)
