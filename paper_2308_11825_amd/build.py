@@ -13,6 +13,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB_PATH = os.path.join(PKG, "libagcn.so")
 CSRC = os.path.join(PKG, "csrc")
+PROBE_SRC = os.path.join(PKG, "probe", "gather_probe.hip")
+PROBE_PATH = os.path.join(PKG, "probe", "gather_probe")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -29,10 +31,9 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into libagcn.so (always recompiles)."""
-    tmp = LIB_PATH + ".tmp"
-    cmd = [HIPCC, *HIP_FLAGS, "-shared", *sources(), "-o", tmp]
+def _hipcc(args, out_path, verbose):
+    tmp = out_path + ".tmp"
+    cmd = [HIPCC, *HIP_FLAGS, *args, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -44,7 +45,15 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed:\n" + "\n".join(lines))
     if verbose and lines:
         print("\n".join(lines), flush=True)
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, out_path)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every HIP source into libagcn.so, and the memory-ceiling probe
+    (probe/gather_probe, a standalone executable the library does not use).
+    Always recompiles."""
+    _hipcc(["-shared", *sources()], LIB_PATH, verbose)
+    _hipcc([PROBE_SRC], PROBE_PATH, verbose)
     return LIB_PATH
 
 
