@@ -9,8 +9,10 @@ released. Inputs (CSR and X for every F) are resident in HBM before timing.
 Prints ONE JSON line. value = whole-step throughput in GFLOP/s, FLOPs being
 2 * nnz * F summed over the F sweep (the plan adds time, not FLOPs).
 Extra keys: per-F execute timings, plan time, the roofline of the dominant
-kernel (measured with HIP events recorded by the library around that kernel
-in every timed step) and the single-threaded CPU oracle on a row sample.
+kernel (measured with HIP events the library attaches to that kernel's
+launch; each timed step marks the executes of one F, rotating through the
+sweep, since every mark costs launch time) and the single-threaded CPU oracle
+on a row sample.
 
 --variant warp_level / column_loop times one of the two ablation baselines of
 Table II instead (same workload, same step), for the ablation ratios.
@@ -399,17 +401,23 @@ def main():
         e.record(stream)  # creates the underlying hipEvent_t
         return e
 
+    # Timing marks cost several microseconds per marked launch, so each timed
+    # step marks the executes of one F only, rotating through the F sweep
+    # (every F when there are fewer steps than widths).
+    def timed_fs(k):
+        return [Fs[k % len(Fs)]] if args.steps >= len(Fs) else list(Fs)
+
     def step(evs):
-        # evs: per F (before k_spmm, after k_spmm) and one event after the last
-        # execute; the library records them on the launch stream.
+        # evs: per marked F (k_spmm start, k_spmm end, after the execute); the
+        # library records the first two on the launch stream.
         plan = agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
                                      d_colidx.data_ptr(), d_vals.data_ptr(), prm, sh)
         for F in Fs:
-            b, m = evs[F] if evs is not None else (None, None)
+            b, m, a = evs[F] if evs is not None and F in evs else (None, None, None)
             agcn.agcn_spmm_timed(plan, F, Xs[F].data_ptr(), F, Ys[F].data_ptr(), F, ws.data_ptr(),
                                  sh, b.cuda_event if b else None, m.cuda_event if m else None, None)
-        if evs is not None:
-            evs["end"].record(stream)
+            if a is not None:
+                a.record(stream)
         agcn.agcn_plan_destroy(plan)
 
     for i in range(args.warmup):
@@ -417,11 +425,8 @@ def main():
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
 
-    events = []
-    for _ in range(args.steps):
-        ev = {F: (new_event(), new_event()) for F in Fs}
-        ev["end"] = new_event()
-        events.append(ev)
+    events = [{F: (new_event(), new_event(), new_event()) for F in timed_fs(k)}
+              for k in range(args.steps)]
     torch.cuda.synchronize()
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -437,11 +442,11 @@ def main():
     per_f = {}
     flops_step = 0.0
     exec_ms_sum = 0.0
-    for i, F in enumerate(Fs):
-        nxt = (lambda k: events[k][Fs[i + 1]][0]) if i + 1 < len(Fs) else (lambda k: events[k]["end"])
-        k7 = np.array([events[k][F][0].elapsed_time(events[k][F][1]) for k in range(args.steps)])
-        # hub-row reduction plus the launch gap up to the next marker
-        k8 = np.array([events[k][F][1].elapsed_time(nxt(k)) for k in range(args.steps)])
+    for F in Fs:
+        marks = [ev[F] for ev in events if F in ev]
+        k7 = np.array([b.elapsed_time(m) for b, m, _ in marks])
+        # hub-row reduction and the launch gap before it
+        k8 = np.array([m.elapsed_time(a) for _, m, a in marks])
         b7, b8 = kernel_bytes(st, F, n_ref, args.variant)
         ex_ms = float(np.mean(k7 + k8))
         exec_ms_sum += ex_ms
@@ -449,13 +454,13 @@ def main():
         flops_step += fl
         per_f[F] = {
             "exec_ms": round(ex_ms, 5), "spmm_ms": round(float(k7.mean()), 5),
-            "hub_reduce_and_gap_ms": round(float(k8.mean()), 5),
+            "hub_reduce_ms": round(float(k8.mean()), 5), "timed_launches": len(marks),
             "gflops": round(fl / (ex_ms * 1e-3) / 1e9, 2),
             "alg_GBps": round((b7 + b8) / (ex_ms * 1e-3) / 1e9, 1),
             "frac_hbm": round((b7 + b8) / (ex_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
             "spmm_bytes": int(b7), "spmm_GBps": round(b7 / (k7.mean() * 1e-3) / 1e9, 1),
         }
-    plan_ms = ms_step - exec_ms_sum
+    plan_ms = ms_step - exec_ms_sum  # the plan, plus the launch gaps between executes
     # Group the aggregation launches by kernel instantiation (lanes per vwarp),
     # as rocprofv3 reports them; the dominant one is the group with the most
     # time per step. achieved = mean algorithmic bytes per launch / mean

@@ -114,7 +114,9 @@ void agcn_default_params(agcn_plan_params* p);
  * device; params NULL = defaults. The plan copies what it needs (sorted
  * permutation, sorted CSR copy, metadata); the inputs may be freed once the
  * call returns. Work is ordered on `stream`; the call synchronises that
- * stream once (to read back the number of metadata entries).
+ * stream once (to read back the number of metadata entries). `stream` must
+ * remain valid until the plan is destroyed (agcn_plan_destroy marks the
+ * plan's last work on it).
  *
  * The CSR is validated on the device: rowptr[0] == 0, non-decreasing,
  * rowptr[n_rows] == nnz, 0 <= colidx[e] < n_cols. A violation returns
@@ -229,8 +231,10 @@ int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s,
 
 /* Releases the plan without blocking. Its device block is kept in a
  * per-device cache (one block per device) together with events that mark the
- * plan's last work on every stream that used it (its creation and each
- * agcn_spmm* / agcn_gcn_layer call). The next agcn_plan_create on that device
+ * plan's last work on every stream that used it: one recorded here on the
+ * stream the plan was created on (covering its creation and every call made
+ * on that stream), and one per other stream, re-recorded by each agcn_spmm* /
+ * agcn_gcn_layer call made on it. The next agcn_plan_create on that device
  * that reuses the block makes its own stream wait on those events, so work
  * still queued with the old plan finishes before the memory is overwritten;
  * see agcn_release_cached_memory. The plan must not be used after this call.

@@ -208,6 +208,25 @@ static void plan_free(agcn_plan* p) {
   std::vector<hipEvent_t> pending;
   if (p->ready != nullptr) pending.push_back(p->ready);
   for (auto& u : p->uses) pending.push_back(u.second);
+  // Calls on the plan's own stream record no event of their own: one event
+  // recorded now on that stream follows all of them (and the plan's kernels).
+  if (p->base != nullptr) {
+    int prev = 0;
+    hipEvent_t ev = nullptr;
+    if (agcn::with_device(p->device, &prev) == AGCN_OK) {
+      if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess &&
+          hipEventRecord(ev, p->stream) == hipSuccess) {
+        pending.push_back(ev);
+      } else {
+        (void)hipGetLastError();
+        if (ev) (void)hipEventDestroy(ev);
+        p->sync_on_release = true;
+      }
+      if (prev != p->device) (void)hipSetDevice(prev);
+    } else {
+      p->sync_on_release = true;
+    }
+  }
   if (p->sync_on_release) {
     int prev = 0;
     if (agcn::with_device(p->device, &prev) == AGCN_OK) {
@@ -353,7 +372,10 @@ int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
                                 static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(ev_begin),
                                 static_cast<hipEvent_t>(ev_mid), static_cast<hipEvent_t>(ev_end),
                                 epilogue);
-  agcn::note_use(plan, static_cast<hipStream_t>(stream));  // also after a failed launch
+  // Last use on a stream other than the plan's own (also after a failed
+  // launch); uses on the plan's stream are covered at release.
+  if (static_cast<hipStream_t>(stream) != plan->stream)
+    agcn::note_use(plan, static_cast<hipStream_t>(stream));
   return rc;
 }
 

@@ -59,9 +59,11 @@ struct agcn_plan {
   int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
   int32_t* group_off = nullptr;     // warp-level plans: [n_rows + 1] first group of each row
   hipEvent_t ready = nullptr;       // recorded after the launch order is built
-  // Last work of the plan on each stream that ran an execute with it (one
-  // event per stream, re-recorded by every call; guarded by use_mu). A later
-  // plan that reuses this memory makes its stream wait on them.
+  hipStream_t stream = nullptr;     // the stream the plan was built on (valid until destroy)
+  // Last work of the plan on each stream other than its own that ran an
+  // execute with it (one event per stream, re-recorded by every call; guarded
+  // by use_mu). Release adds one event recorded on the plan's own stream. A
+  // later plan that reuses this memory makes its stream wait on them.
   std::mutex use_mu;
   std::vector<std::pair<hipStream_t, hipEvent_t>> uses;
   bool sync_on_release = false;     // an event could not be created: release waits on the device

@@ -2,13 +2,14 @@
 // (Sec. III-C "Degree Sorting" and "Block-level Partition", Alg. 1 and Alg. 2).
 //
 // Pipeline (all on one stream; the host waits twice: on an event once the
-// maximum degree is known, and on the stream before the launch order):
-//   k_init          clear the error word and the maximum degree
+// maximum degree is known -- radix passes 0 and 1 are already queued -- and on
+// the stream after the partition):
 //   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
-//                   per-workgroup maximum degree
-//   k_dmax          maximum degree (one workgroup); copied to pinned host
-//                   memory while radix pass 0 runs, so the host launches only
-//                   the passes the maximum degree needs
+//                   per-workgroup maximum degree and error flags
+//   k_dmax          maximum degree (one workgroup); written to pinned host
+//                   memory while radix passes 0 and 1 run, so the host
+//                   launches passes 2 and 3 only if the maximum degree needs
+//                   them
 //   radix passes    stable LSD radix sort of row ids by degree, 8-bit digits:
 //                   k_radix_hist -> exclusive scan -> k_radix_scatter. Buffers
 //                   alternate so that the last pass writes the final
@@ -18,12 +19,14 @@
 //   k_class_start   first sorted row of each degree class 0..deg_bound+1
 //   k_seg_count     blocks per degree class / chunks per hub row
 //   scan            entry offsets of every segment
-//   k_meta_fill     one int4 {deg, loc, row, info} per entry, in Alg. 2's order
-//   k_hub_offsets   first chunk of each hub row + summary for the host
+//   k_partition_fill one int4 {deg, loc, row, info} per entry, in Alg. 2's
+//                   order; first chunk of each hub row; summary for the host;
+//                   launch order: hub chunks, then the other entries
+//                   heaviest first
 //   (host sync)     entry counts read back
-//   launch order    hub-chunk entries sorted by a 16-bit key of their first
-//                   column (two radix passes, when hub rows are long), then
-//                   the other entries heaviest first; an event marks it ready
+//   launch order    when hub rows are long: hub-chunk entries re-sorted by a
+//                   16-bit key of their first column (two radix passes), then
+//                   the other entries; an event marks the plan ready
 //
 // The two read-backs (maximum degree, summary) are written by the kernels
 // straight into pinned, host-coherent memory; the host reads them after the
@@ -102,6 +105,12 @@ __device__ inline int32_t wave_max(int32_t v) {
   return v;
 }
 
+__device__ inline uint32_t wave_or(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v |= (uint32_t)__shfl_xor((int32_t)v, o, 64);
+  return v;
+}
+
 // Inclusive scan over the 64 lanes of a wave.
 __device__ inline int32_t wave_inclusive_scan(int32_t v, int lane) {
 #pragma unroll
@@ -157,24 +166,19 @@ __device__ inline int32_t pattern_of(int32_t d, int32_t W, int32_t Z) {
 
 // ---------------------------------------------------------------------------
 
-__global__ void k_init(uint32_t* err, int32_t* dmax) {
-  if (threadIdx.x == 0) {
-    err[0] = 0;
-    dmax[0] = 0;
-  }
-}
-
 __global__ void k_set(int32_t* p, int32_t v) {
   if (threadIdx.x == 0 && blockIdx.x == 0) p[0] = v;
 }
 
-// Step (1) of the degree sort, plus the row-pointer checks and the maximum
-// degree of each workgroup.
+// Step (1) of the degree sort, plus the row-pointer checks: the maximum
+// degree and the OR of the error flags of each workgroup.
 __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
                                                      const int32_t* __restrict__ rowptr,
-                                                     int32_t* __restrict__ deg, uint32_t* err,
-                                                     int32_t* __restrict__ block_max) {
+                                                     int32_t* __restrict__ deg,
+                                                     int32_t* __restrict__ block_max,
+                                                     uint32_t* __restrict__ block_err) {
   __shared__ int32_t s_max[kThreads / 64];
+  __shared__ uint32_t s_err[kThreads / 64];
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   uint32_t e = 0;
   int32_t d = 0;
@@ -189,31 +193,57 @@ __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
     if (i == n - 1 && (int64_t)b != nnz) e |= kErrRowptrEnd;
     deg[i] = d;
   }
-  if (e) atomicOr(err, e);
   const int32_t m = wave_max(d);
-  if ((threadIdx.x & 63) == 0) s_max[threadIdx.x >> 6] = m;
+  const uint32_t we = wave_or(e);
+  if ((threadIdx.x & 63) == 0) {
+    s_max[threadIdx.x >> 6] = m;
+    s_err[threadIdx.x >> 6] = we;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     int32_t t = 0;
-    for (int w = 0; w < kThreads / 64; ++w) t = max(t, s_max[w]);
+    uint32_t f = 0;
+    for (int w = 0; w < kThreads / 64; ++w) {
+      t = max(t, s_max[w]);
+      f |= s_err[w];
+    }
     block_max[blockIdx.x] = t;
+    block_err[blockIdx.x] = f;
   }
 }
 
-// Maximum of the per-workgroup maxima (one workgroup of kScanTopThreads).
+// Maximum of the per-workgroup maxima and OR of their error flags (one
+// workgroup of kScanTopThreads). It is the first writer of the plan's error
+// word and maximum degree (nb = 0: both become 0), so no clearing kernel runs
+// before it; every later kernel reads or ORs into them.
 __global__ __launch_bounds__(kScanTopThreads) void k_dmax(const int32_t* __restrict__ block_max,
-                                                          int32_t nb, int32_t* dmax,
+                                                          const uint32_t* __restrict__ block_err,
+                                                          int32_t nb, int32_t* dmax, uint32_t* err,
                                                           PlanSummary* host_sum) {
   __shared__ int32_t s_max[kScanTopThreads / 64];
+  __shared__ uint32_t s_err[kScanTopThreads / 64];
   int32_t m = 0;
-  for (int32_t i = threadIdx.x; i < nb; i += kScanTopThreads) m = max(m, block_max[i]);
+  uint32_t e = 0;
+  for (int32_t i = threadIdx.x; i < nb; i += kScanTopThreads) {
+    m = max(m, block_max[i]);
+    e |= block_err[i];
+  }
   m = wave_max(m);
-  if ((threadIdx.x & 63) == 0) s_max[threadIdx.x >> 6] = m;
+  e = wave_or(e);
+  if ((threadIdx.x & 63) == 0) {
+    s_max[threadIdx.x >> 6] = m;
+    s_err[threadIdx.x >> 6] = e;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     int32_t t = 0;
-    for (int w = 0; w < kScanTopThreads / 64; ++w) t = max(t, s_max[w]);
+    uint32_t f = 0;
+    for (int w = 0; w < kScanTopThreads / 64; ++w) {
+      t = max(t, s_max[w]);
+      f |= s_err[w];
+    }
     dmax[0] = t;
+    err[0] = f;
     host_sum->max_deg = t;
     __threadfence_system();
   }
@@ -600,15 +630,33 @@ __global__ __launch_bounds__(kThreads) void k_seg_count(int32_t n, const int32_t
   nb[s] = (int32_t)v;
 }
 
-// Alg. 2's entries, each computed independently from its segment.
-__global__ __launch_bounds__(kThreads) void k_meta_fill(
-    const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ deg_s,
+// The partition's outputs, one kernel after the segment scan (every part is
+// computed independently from the segment offsets and class starts):
+//   - Alg. 2's entries, each from its segment;
+//   - the first chunk of each hub row, and the summary read back by the host;
+//   - the SpMM launch order: hub chunks, then the other entries heaviest
+//     first (rewritten after the host synchronisation when hub chunks are
+//     launched in column order; it never changes a result).
+__global__ __launch_bounds__(kThreads) void k_partition_fill(
+    int32_t n, const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ deg_s,
     const int32_t* __restrict__ cls, const int32_t* __restrict__ seg_off, int32_t S, int32_t W,
-    int32_t Z, int32_t DB, int32_t H, int4* __restrict__ meta, int64_t cap, const uint32_t* err) {
-  if (failed(err)) return;
-  const int64_t total = seg_off[S];
-  for (int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x; b < total && b < cap;
-       b += (int64_t)gridDim.x * kThreads) {
+    int32_t Z, int32_t DB, int32_t H, int4* __restrict__ meta, int64_t cap, int32_t hub_ub,
+    int32_t* __restrict__ hub_chunk_off, int32_t* __restrict__ order, PlanSummary* sum,
+    const uint32_t* err) {
+  const int64_t t0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  const uint32_t e = err[0];
+  if (t0 == 0) {
+    sum->err = e;
+    if (e) __threadfence_system();
+  }
+  if (e) return;
+  const int32_t total = seg_off[S];
+  const int32_t hub_first_entry = seg_off[DB + 1];
+  const int32_t first_hub_row = cls[DB + 1];
+  const int32_t n_hub = n - first_hub_row;
+  const int32_t n_chunks = n_hub > 0 ? total - hub_first_entry : 0;
+  for (int64_t b = t0; b < total && b < cap; b += stride) {
     int32_t a = 0, c = S - 1;  // largest segment starting at or before b
     while (a < c) {
       const int32_t mid = (int32_t)(((int64_t)a + c + 1) >> 1);
@@ -630,28 +678,15 @@ __global__ __launch_bounds__(kThreads) void k_meta_fill(
       m = make_int4(d, rowptr_s[r] + off, r, left < H ? left : H);
     }
     meta[b] = m;
+    order[b] = b < n_chunks ? total - 1 - (int32_t)b : hub_first_entry - 1 - (int32_t)(b - n_chunks);
   }
-}
-
-__global__ __launch_bounds__(kThreads) void k_hub_offsets(
-    int32_t n, const int32_t* __restrict__ deg_s, const int32_t* __restrict__ cls,
-    const int32_t* __restrict__ seg_off, int32_t S, int32_t DB, int32_t hub_ub,
-    int32_t* __restrict__ hub_chunk_off, PlanSummary* sum, const uint32_t* err) {
-  const int64_t h = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const uint32_t e = err[0];
-  if (h == 0) {
-    sum->err = e;
-    if (e) __threadfence_system();
-  }
-  if (e) return;
-  const int32_t first = cls[DB + 1];
-  const int32_t n_hub = n - first;
-  if (h <= n_hub && h <= hub_ub) hub_chunk_off[h] = seg_off[DB + 1 + h] - seg_off[DB + 1];
-  if (h == 0) {
-    sum->n_entries = seg_off[S];
-    sum->hub_first_entry = seg_off[DB + 1];
+  for (int64_t h = t0; h <= n_hub && h <= hub_ub; h += stride)
+    hub_chunk_off[h] = seg_off[DB + 1 + h] - seg_off[DB + 1];
+  if (t0 == 0) {
+    sum->n_entries = total;
+    sum->hub_first_entry = hub_first_entry;
     sum->n_hub_rows = n_hub;
-    sum->hub_first_row = first;
+    sum->hub_first_row = first_hub_row;
     sum->max_deg = n > 0 ? deg_s[n - 1] : 0;
     __threadfence_system();
   }
@@ -886,7 +921,7 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   const size_t o_goff = L.take(4 * (n + 1));
   const size_t o_deg = L.take(4 * n);
   const size_t o_ng = L.take(4 * n);
-  const size_t o_bmax = L.take(4 * (ceil_div64(n, kThreads) + 1));
+  const size_t o_bmax = L.take(4 * 2 * (ceil_div64(n, kThreads) + 1));  // block maxima, error flags
   const size_t o_partials = L.take(4 * n_partials);
   const size_t o_err = L.take(64);
   const size_t o_dmax = L.take(64);
@@ -914,12 +949,11 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   if (hs == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "pinned host buffer allocation failed");
   *hs = PlanSummary{};
   const int64_t nb = ceil_div64(n, kThreads);
-  k_init<<<1, 64, 0, st>>>(err, dmax);
-  if (n > 0) {
-    k_degree<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err, bmax);
-    k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, (int32_t)nb, dmax, dsum);
-    k_wl_groups<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, deg, Z, ng, err);
-  }
+  uint32_t* berr = reinterpret_cast<uint32_t*>(bmax + nb + 1);
+  if (n > 0)
+    k_degree<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, bmax, berr);
+  k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, berr, (int32_t)nb, dmax, err, dsum);
+  if (n > 0) k_wl_groups<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, deg, Z, ng, err);
   const unsigned cgrid = (unsigned)std::min<int64_t>(grid_for(std::max(nnz, n + 1), kThreads), 65536);
   k_wl_copy<<<cgrid, kThreads, 0, st>>>((int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals,
                                         p->perm, p->rowptr_s, p->colidx_s, p->vals_s, err);
@@ -981,7 +1015,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   const size_t o_err = L.take(64);
   const size_t o_dmax = L.take(64);
   const int64_t n_deg_blocks = ceil_div64(n, kThreads);
-  const size_t o_bmax = L.take(4 * (n_deg_blocks + 1));
+  const size_t o_bmax = L.take(4 * 2 * (n_deg_blocks + 1));  // block maxima, error flags
   const size_t o_hsort = L.take(4 * 5 * chunk_ub);  // keys in, 2 x keys, 2 x ids
   const size_t o_hgate = L.take(64);
 
@@ -1019,22 +1053,27 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   if (hs == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "pinned host buffer allocation failed");
   *hs = PlanSummary{};  // no kernel of this thread's previous plan is still running
   hipError_t he;
-  k_init<<<1, 64, 0, st>>>(err, dmax);
+  uint32_t* berr = reinterpret_cast<uint32_t*>(bmax + n_deg_blocks + 1);
+  if (n > 0)
+    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, bmax,
+                                                         berr);
+  k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, berr, (int32_t)n_deg_blocks, dmax, err, dsum);
+  if ((rc = check_launch("k_degree"))) return rc;
   if (n > 0) {
-    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, err,
-                                                         bmax);
-    k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, (int32_t)n_deg_blocks, dmax, dsum);
-    if ((rc = check_launch("k_degree"))) return rc;
     // The maximum degree reaches the host while radix pass 0 (always needed)
     // runs; the host then launches exactly the passes it needs.
     hipEvent_t ev = plan_event();
     if (ev == nullptr || (he = hipEventRecord(ev, st)) != hipSuccess)
       return hip_fail(ev ? he : hipErrorOutOfMemory, "hipEventRecord(plan)");
 
-    // Stable LSD radix sort of row ids by degree, 8-bit digits.
+    // Stable LSD radix sort of row ids by degree, 8-bit digits. Passes 0 and
+    // 1 are queued before the host reads the maximum degree (pass 1 returns
+    // at once on the device when one pass suffices), so the GPU keeps busy
+    // while the read-back reaches the host; passes 2 and 3 follow if needed.
     const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
     const RadixBufs bufs{deg, {keys, keys2}, {p->perm, ids2}};
-    int passes = 1;
+    constexpr int kPassesBeforeReadback = 2;
+    int passes = kPassesBeforeReadback;
     for (int pass = 0; pass < passes; ++pass) {
       k_radix_hist<<<rgrid, kThreads, 0, st>>>((int32_t)n, bufs, pass, counts, (int32_t)n_tiles, err,
                                                dmax);
@@ -1044,12 +1083,12 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
       k_radix_scatter<<<rgrid, kThreads, 0, st>>>((int32_t)n, bufs, pass, counts, (int32_t)n_tiles,
                                                   err, dmax);
       if ((rc = check_launch("k_radix_scatter"))) return rc;
-      if (pass == 0) {
+      if (pass == kPassesBeforeReadback - 1) {
         if ((he = hipEventSynchronize(ev)) != hipSuccess) return hip_fail(he, "hipEventSynchronize");
         const int32_t md = hs->max_deg;
         int bits = 0;
         while (bits < 31 && (int64_t(1) << bits) <= md) ++bits;
-        passes = std::max(1, (bits + 7) / 8);
+        passes = std::max(kPassesBeforeReadback, (bits + 7) / 8);
       }
     }
   }
@@ -1067,10 +1106,9 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   if ((rc = check_launch("partition counts"))) return rc;
   if ((rc = scan_exclusive(nb, S, seg, seg + S, partials, err, st))) return rc;
   const unsigned mgrid = (unsigned)std::min<int64_t>(grid_for(ent_ub, kThreads), 16384);
-  k_meta_fill<<<mgrid, kThreads, 0, st>>>(p->rowptr_s, keys, cls, seg, (int32_t)S, W, Z, DB, H,
-                                          p->meta, ent_ub, err);
-  k_hub_offsets<<<grid_for(hub_ub + 1, kThreads), kThreads, 0, st>>>(
-      (int32_t)n, keys, cls, seg, (int32_t)S, DB, (int32_t)hub_ub, p->hub_chunk_off, dsum, err);
+  k_partition_fill<<<mgrid, kThreads, 0, st>>>((int32_t)n, p->rowptr_s, keys, cls, seg, (int32_t)S,
+                                               W, Z, DB, H, p->meta, ent_ub, (int32_t)hub_ub,
+                                               p->hub_chunk_off, p->order, dsum, err);
   if ((rc = check_launch("partition fill"))) return rc;
 
   he = hipStreamSynchronize(st);
@@ -1090,8 +1128,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   p->hub_first_row = hs->hub_first_row;
   p->max_deg = hs->max_deg;
 
-  // Launch order for the SpMM (does not change any result, only which
-  // entries run side by side). Queued after the synchronisation; agcn_spmm
+  // Hub chunks in column order: queued after the synchronisation; agcn_spmm
   // waits for the event recorded below.
   const int32_t n_chunks = p->n_hub_rows > 0 ? p->n_entries - p->hub_first_entry : 0;
   const int32_t* sorted_ids = nullptr;
@@ -1117,10 +1154,9 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
                                                   hgate);
     }
     sorted_ids = hb.ids[0];
-  }
-  if (p->n_entries > 0)
     k_order_fill<<<grid_for(p->n_entries, kThreads), kThreads, 0, st>>>(
         p->order, p->n_entries, p->hub_first_entry, n_chunks, sorted_ids);
+  }
   if ((rc = check_launch("launch order"))) return rc;
   if ((he = hipEventCreateWithFlags(&p->ready, hipEventDisableTiming)) != hipSuccess)
     return hip_fail(he, "hipEventCreate(plan ready)");
@@ -1132,6 +1168,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
 
 int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
                const float* d_vals, hipStream_t st) {
+  p->stream = st;
   return (p->flags & AGCN_PLAN_WARP_LEVEL) ? build_plan_warp_level(p, d_rowptr, d_colidx, d_vals, st)
                                           : build_plan_block(p, d_rowptr, d_colidx, d_vals, st);
 }

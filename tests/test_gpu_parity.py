@@ -301,16 +301,18 @@ def test_plan_memory_reused_across_plans():
     p3.destroy()
 
 
-def test_destroy_while_executing_then_reuse_on_another_stream():
+@pytest.mark.parametrize("plan_stream", ["exec", "other"])
+def test_destroy_while_executing_then_reuse_on_another_stream(plan_stream):
     """agcn_plan_destroy does not block; a plan that reuses the destroyed
     plan's cached memory on another stream must wait for the work still
     queued with the old plan (it would otherwise overwrite the sorted CSR the
-    running execute reads)."""
+    running execute reads). The executes run on the plan's own stream (marked
+    at release) or on another stream (marked by each call)."""
     g1 = _mixed(81, n=40000, hub_max=8000)
     g2 = _mixed(82, n=39000, hub_max=8000)
-    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1, s2, s0 = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     agcn.agcn_release_cached_memory()
-    p1 = _plan(g1, stream=s1)
+    p1 = _plan(g1, stream=s1 if plan_stream == "exec" else s0)
     F = 512
     X1 = np.random.default_rng(83).standard_normal((g1.n_cols, F)).astype(np.float32)
     X1d = _dev(X1)
