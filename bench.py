@@ -239,6 +239,17 @@ def rocsparse_compare(g, Fs, Xs, Ys, d_rowptr, d_colidx, d_vals, stream, reps):
 MFMA_FP32_PEAK_TFLOPS = 157.3
 
 
+def linear_kernel_name(fin, fout):
+    """Instantiation agcn_linear picks for compact, 16-byte aligned float32 X and
+    W (AGCN_LINEAR_RW=0 forces the tiled kernel)."""
+    vec = fin % 4 == 0 and fout % 4 == 0
+    if vec and 1 <= fin <= 128 and fout <= 128 and os.environ.get("AGCN_LINEAR_RW", "1") != "0":
+        nb = 2 if fout <= 32 else 4 if fout <= 64 else 8
+        ks = 2 if fin <= 32 else 4 if fin <= 64 else 8
+        return f"k_linear_rw<{nb}, {ks}>"
+    return f"k_linear<{32 if fout <= 32 else 64 if fout <= 64 else 128}, {'true' if vec else 'false'}>"
+
+
 def bench_layer(args):
     """One GCNConv forward per step over a plan built once."""
     import torch
@@ -305,7 +316,7 @@ def bench_layer(args):
     fl_lin = 2.0 * g.n_cols * fin * fout
     fl_agg = 2.0 * g.nnz * fout
     ach = fl_lin / (lin_ms * 1e-3) / 1e12
-    kname = f"k_linear<{32 if fout <= 32 else 64 if fout <= 64 else 128}, true>"
+    kname = linear_kernel_name(fin, fout)
     out = {
         "metric": "GCNConv layer forward GFLOP/s (2·N·fin·fout + 2·nnz·fout)",
         "value": round((fl_lin + fl_agg) / (ms_step * 1e-3) / 1e9, 3), "unit": "GFLOP/s",

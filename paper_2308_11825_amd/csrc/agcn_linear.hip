@@ -19,6 +19,7 @@
 // X is read once per column tile, and the column tiles of one row tile are
 // consecutive workgroups, so the second read of X hits L2.
 #include <algorithm>
+#include <cstdlib>
 
 #include "agcn_internal.hpp"
 
@@ -165,6 +166,176 @@ __global__ __launch_bounds__(kThreads) void k_linear(int64_t n, int32_t fin, int
   }
 }
 
+// --- W resident in LDS --------------------------------------------------------
+//
+// k_linear_rw: for fin <= 128 and fout <= 128 (128-bit path, X and H each
+// under 4 GiB), W^T stays in
+// LDS for the whole kernel and every wave works alone on 16-row tiles of X, so
+// the main loop has no workgroup barrier:
+//   1. each workgroup (4 waves) writes W^T into LDS once: NB * 16 rows (output
+//      columns) of KP floats (fin rounded up to KS * 16), zero outside W; the
+//      16-byte chunk c of row j sits at chunk c ^ (j & 7), so the 8 rows a
+//      group of lanes reads for one chunk fall in 8 different bank groups;
+//   2. wave v takes tiles v, v + waves, ... of 16 rows; the next tile's X is
+//      loaded into registers while the current one is multiplied;
+//   3. v_mfma_f32_16x16x4f32 (lane l supplies A[l % 16][l / 16] and
+//      B[l / 16][l % 16]; accumulator register r of lane l holds
+//      C[4 (l / 16) + r][l % 16]). The contraction order is permuted so that
+//      one 16-byte load per lane feeds four instructions: in k-step s, lane l
+//      loads X[row][16 s + 4 g .. + 3] (g = l / 16) and instruction t takes
+//      element t, paired with W^T[col][16 s + 4 g + t] from one 16-byte LDS
+//      read; the four instructions together cover k = 16 s .. 16 s + 15.
+constexpr int kRwThreads = 256;
+constexpr int kRwWaves = kRwThreads / 64;
+constexpr int kRwRows = 16;
+
+// Offset of a masked element. A raw buffer access is out of range when its
+// offset is >= the resource's byte count; every resource here covers at most
+// kRwOutOfRange - 16 bytes (checked by the host), so this offset is always
+// out of range: the load returns 0 and the store is dropped.
+constexpr uint32_t kRwOutOfRange = 0xFFFFFFF0u;
+
+__device__ inline __amdgpu_buffer_rsrc_t rw_resource(const void* base, uint32_t bytes) {
+  // Raw buffer (stride 0) of `bytes` bytes; dword3 = 32-bit data format (gfx9 family).
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+__device__ inline int wt_index(int j, int k, int kc) {  // float index of W^T[j][k]
+  return (j * kc + ((k >> 2) ^ (j & 7))) * 4 + (k & 3);
+}
+
+template <int NB, int KS>
+__global__ __launch_bounds__(kRwThreads) void k_linear_rw(int64_t n, int32_t fin, int32_t fout,
+                                                          const float* __restrict__ X, int64_t ldx,
+                                                          const float* __restrict__ W, int64_t ldw,
+                                                          float* __restrict__ H, int64_t ldh) {
+  constexpr int KP = KS * 16, KC = KP / 4, NJ = NB * 16;
+  __shared__ __attribute__((aligned(16))) float swt[NJ * KP];
+  // 1. W^T into LDS: W row k is read as float4 (4 output columns) and
+  //    scattered into 4 rows of W^T. Consecutive lanes take consecutive k, so
+  //    their LDS writes land in consecutive words of one W^T row.
+  for (int idx = threadIdx.x; idx < KP * (NJ / 4); idx += kRwThreads) {
+    const int j0 = (idx / KP) * 4, k = idx - (idx / KP) * KP;
+    f4 w = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (k < fin && j0 < fout) w = *reinterpret_cast<const f4*>(W + (int64_t)k * ldw + j0);
+    swt[wt_index(j0 + 0, k, KC)] = w.x;
+    swt[wt_index(j0 + 1, k, KC)] = w.y;
+    swt[wt_index(j0 + 2, k, KC)] = w.z;
+    swt[wt_index(j0 + 3, k, KC)] = w.w;
+  }
+  __syncthreads();
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int i = lane & 15, g = lane >> 4;
+  const int64_t n_tiles = (n + kRwRows - 1) / kRwRows;
+  const int64_t n_waves = (int64_t)gridDim.x * kRwWaves;
+  // X and H through buffer resources: a masked element gets an offset past
+  // the 4 GiB range, so its load returns 0 and its store is dropped, with no
+  // branch; the compiler then counts the memory operations in flight exactly
+  // and waits only for the loads it needs.
+  const __amdgpu_buffer_rsrc_t xr = rw_resource(X, (uint32_t)(n * ldx * 4));
+  const __amdgpu_buffer_rsrc_t hr = rw_resource(H, (uint32_t)(n * ldh * 4));
+  auto load_x = [&](int64_t tile, f4* xv) {
+    const int64_t row = tile * kRwRows + i;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int k = 16 * s + 4 * g;
+      const uint32_t off = (row < n && k < fin) ? (uint32_t)((row * ldx + k) * 4) : kRwOutOfRange;
+      xv[s] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, 0));
+    }
+  };
+  // H stores of one tile, branch-free (masked rows and columns get the
+  // out-of-range offset).
+  const uint32_t ldh4 = (uint32_t)(ldh * 4);
+  auto store_h = [&](int64_t tile, const f4* acc) {
+    const int64_t rbase = tile * kRwRows + 4 * g;
+    const uint32_t base = (uint32_t)(rbase * ldh4) + (uint32_t)(4 * i);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bool row_ok = rbase + r < n;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const bool ok = row_ok && 16 * b + i < fout;
+        const uint32_t off = ok ? base + (uint32_t)r * ldh4 + (uint32_t)(64 * b) : kRwOutOfRange;
+        const float v = acc[b][r];  // a scalar first: bit_cast of a vector element is not one
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), hr, (int)off, 0, 0);
+      }
+    }
+  };
+  f4 xa[KS], xb[KS];
+  int64_t tile = (int64_t)blockIdx.x * kRwWaves + wave;
+  load_x(tile, xa);
+  for (; tile < n_tiles; tile += n_waves) {
+    load_x(tile + n_waves, xb);  // past the last tile: rows >= n, zeros
+    f4 acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[b] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      f4 wv[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        wv[b] = *reinterpret_cast<const f4*>(swt + wt_index(16 * b + i, 16 * s + 4 * g, KC));
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[s][t], wv[b][t], acc[b], 0, 0, 0);
+    }
+    store_h(tile, acc);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) xa[s] = xb[s];
+  }
+}
+
+// AGCN_LINEAR_RW=0 selects the tiled kernel for every shape (for measurements).
+bool rw_disabled() {
+  static const bool v = [] {
+    const char* e = std::getenv("AGCN_LINEAR_RW");
+    return e != nullptr && std::atoi(e) == 0;
+  }();
+  return v;
+}
+
+// Workgroups for k_linear_rw: as many as are resident at once on the device
+// (each loads W^T once and then loops over tiles), fewer when there are fewer
+// tiles.
+template <int NB, int KS>
+int rw_grid(int64_t n) {
+  static const int resident = [] {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_linear_rw<NB, KS>, kRwThreads, 0) !=
+            hipSuccess) {
+      (void)hipGetLastError();
+      cus = 256;
+      per_cu = 1;
+    }
+    return std::max(1, cus) * std::max(1, per_cu);
+  }();
+  const int64_t tiles = (n + kRwRows - 1) / kRwRows;
+  return (int)std::max<int64_t>(1, std::min<int64_t>(resident, (tiles + kRwWaves - 1) / kRwWaves));
+}
+
+template <int NB, int KS>
+int launch_rw(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx, const float* W,
+              int64_t ldw, float* H, int64_t ldh, hipStream_t st) {
+  k_linear_rw<NB, KS><<<rw_grid<NB, KS>(n), kRwThreads, 0, st>>>(n, fin, fout, X, ldx, W, ldw, H,
+                                                                 ldh);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? AGCN_OK : hip_fail(e, "k_linear_rw launch");
+}
+
+template <int NB>
+int dispatch_rw(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx, const float* W,
+                int64_t ldw, float* H, int64_t ldh, hipStream_t st) {
+  if (fin <= 32) return launch_rw<NB, 2>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
+  if (fin <= 64) return launch_rw<NB, 4>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
+  return launch_rw<NB, 8>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
+}
+
 template <int BN>
 int launch_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx,
                   const float* W, int64_t ldw, float* H, int64_t ldh, hipStream_t st, bool vec) {
@@ -189,6 +360,15 @@ int run_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx
   if (n == 0 || fout == 0) return AGCN_OK;
   const bool vec = fin % 4 == 0 && fout % 4 == 0 && ldx % 4 == 0 && ldw % 4 == 0 &&
                    aligned16(X) && aligned16(W);
+  // k_linear_rw addresses X and H with 32-bit byte offsets, and its masked
+  // offset must lie past both (see kRwOutOfRange).
+  const int64_t lim = (int64_t)kRwOutOfRange - 16;
+  const bool rw_fits = n * ldx * 4 <= lim && n * ldh * 4 <= lim;
+  if (vec && rw_fits && fin >= 1 && fin <= 128 && fout <= 128 && !rw_disabled()) {
+    if (fout <= 32) return dispatch_rw<2>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
+    if (fout <= 64) return dispatch_rw<4>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
+    return dispatch_rw<8>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
+  }
   if (fout <= 32) return launch_linear<32>(n, fin, fout, X, ldx, W, ldw, H, ldh, st, vec);
   if (fout <= 64) return launch_linear<64>(n, fin, fout, X, ldx, W, ldw, H, ldh, st, vec);
   return launch_linear<128>(n, fin, fout, X, ldx, W, ldw, H, ldh, st, vec);

@@ -42,3 +42,12 @@ def test_kernel_names_match_the_library_dispatch():
     assert bench.spmm_kernel_name(17) == "k_spmm<1, 17>"
     assert bench.spmm_kernel_name(64, "column_loop") == "k_spmm_colloop"
     assert bench.spmm_kernel_name(64, "warp_level") == "k_spmm_wl<4, 8>"
+
+
+def test_linear_kernel_names_match_the_library_dispatch():
+    assert bench.linear_kernel_name(128, 128) == "k_linear_rw<8, 8>"
+    assert bench.linear_kernel_name(32, 16) == "k_linear_rw<2, 2>"
+    assert bench.linear_kernel_name(64, 100) == "k_linear_rw<8, 4>"
+    assert bench.linear_kernel_name(256, 128) == "k_linear<128, true>"
+    assert bench.linear_kernel_name(128, 200) == "k_linear<128, true>"
+    assert bench.linear_kernel_name(30, 64) == "k_linear<64, false>"
