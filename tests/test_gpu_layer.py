@@ -215,3 +215,30 @@ def test_layer_captured_in_a_hip_graph_replays_like_eager():
             _check_layer(plan, g, Xr, W.cpu().numpy(), "relu", Yg=Y.cpu().numpy())
     del graph
     plan.destroy()
+
+
+def test_linear_padded_strides_and_x_past_4_gib():
+    """The resident-W kernel (fin, fout <= 128, 16-byte aligned rows) with
+    padded leading dimensions: X's padding columns hold infinities that must
+    never be read, H's padding columns stay untouched. X spanning 4 GiB or
+    more takes the tiled kernel: same tolerance."""
+    rng = np.random.default_rng(11)
+    n, fin, fout = 2051, 100, 44
+    X = rng.standard_normal((n, fin)).astype(np.float32)
+    W = graphgen.weights(fin, fout, seed=12)
+    Xp = torch.full((n, fin + 8), float("inf"), device=DEV)
+    Xp[:, :fin] = _dev(X)
+    Wp = torch.full((fin, fout + 4), float("inf"), device=DEV)
+    Wp[:, :fout] = _dev(W)
+    Hp = torch.full((n, fout + 12), 7.0, device=DEV)
+    agcn.linear(Xp[:, :fin], Wp[:, :fout], out=Hp[:, :fout])
+    _check_linear(X, W, Hp[:, :fout].cpu().numpy(), "padded strides")
+    assert torch.all(Hp[:, fout:] == 7.0)
+    n2, ld2 = 60_000, 18_000                  # n2 * ld2 * 4 bytes > 4 GiB
+    X2 = rng.standard_normal((n2, 64)).astype(np.float32)
+    W2 = graphgen.weights(64, 128, seed=13)
+    big = torch.empty((n2, ld2), device=DEV)
+    big[:, :64] = _dev(X2)
+    H2 = agcn.linear(big[:, :64], _dev(W2)).cpu().numpy()
+    del big
+    _check_linear(X2, W2, H2, "X past 4 GiB")
