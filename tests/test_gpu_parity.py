@@ -181,6 +181,49 @@ def test_row_permutation_equivariance_bit_exact():
     pb.destroy()
 
 
+def test_symmetric_relabel_within_tolerance():
+    """Relabelling the nodes, (P A P^T)(P X) = P (A X): the relabelled graph
+    has other degrees per position, other columns and so another partition
+    and summation order, so the two agree within the tolerance (twice the
+    bound: each side carries its own rounding)."""
+    g = _mixed(24, n=7000, hub_max=5000)
+    p = np.random.default_rng(25).permutation(g.n_rows)
+    pinv = np.empty_like(p)
+    pinv[p] = np.arange(p.size)
+    gp = graphgen.permute_rows(g, p)
+    gp.colidx[:] = pinv[gp.colidx].astype(np.int32)      # column j of A is column pinv[j] of P A P^T
+    X = np.random.default_rng(26).standard_normal((g.n_cols, 64)).astype(np.float32)
+    Y, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, want_scale=True)
+    pb = _plan(gp)
+    Yb = pb.spmm(_dev(X[p])).cpu().numpy()
+    assert_close(Yb, Y[p], 2 * S[p], "P A P^T P X against P (A X)")
+    pb.destroy()
+
+
+def test_linearity_within_tolerance(mixed_plan):
+    """A (a X1 + b X2) = a (A X1) + b (A X2): each of the three products is
+    within the bound of its own scale, so the two sides differ by at most
+    the sum of the bounds."""
+    g, plan = mixed_plan
+    rng = np.random.default_rng(27)
+    F, a, b = 32, np.float32(0.75), np.float32(-1.5)
+    X1 = rng.standard_normal((g.n_cols, F)).astype(np.float32)
+    X2 = rng.standard_normal((g.n_cols, F)).astype(np.float32)
+    Z = a * X1 + b * X2
+    _, S1 = oracle.spmm(g.rowptr, g.colidx, g.vals, X1, want_scale=True)
+    _, S2 = oracle.spmm(g.rowptr, g.colidx, g.vals, X2, want_scale=True)
+    _, SZ = oracle.spmm(g.rowptr, g.colidx, g.vals, Z, want_scale=True)
+    lhs = plan.spmm(_dev(Z)).cpu().numpy()
+    rhs = (a * plan.spmm(_dev(X1)) + b * plan.spmm(_dev(X2))).cpu().numpy()
+    # Bound of |lhs - rhs| in units of the tolerance's 1e-5: the three products'
+    # bounds (each with its 1e-7 absolute term), plus the float32 roundings of
+    # a * y1, b * y2 and their sum (2^-24 relative each).
+    u = 2.0 ** -24 / 1e-5
+    S = (SZ + (abs(a) * S1 + abs(b) * S2) * (1 + u) + 2 * u * np.abs(rhs).astype(np.float64)
+         + (abs(a) + abs(b)) * 1e-7 / 1e-5)
+    assert_close(lhs, rhs, S, "linearity")
+
+
 def test_non_finite_features_propagate_like_the_oracle(mixed_plan):
     """NaN and infinite X rows reach exactly the Y elements the definition
     says (NaN anywhere -> NaN, +inf with -inf -> NaN, +inf alone -> +inf),
