@@ -12,6 +12,7 @@ import os
 import numpy as np
 import pytest
 import scipy.sparse as sp
+from hypothesis import given, settings, strategies as st
 
 import graphgen
 import oracle
@@ -343,6 +344,26 @@ def test_partition_invariants_and_replay(W, Z, H, seed):
     assert np.all(cover == 1)                                             # I1
     # Replaying visits each row's nnz in ascending order, so the float64 sums
     # match the definition exactly.
+    assert np.array_equal(Y, oracle.spmm(g.rowptr, g.colidx, g.vals, X))
+
+
+@settings(max_examples=60, deadline=None, derandomize=True)
+@given(W=st.integers(1, 32), zf=st.floats(0.0, 1.0), H=st.integers(0, 4096),
+       degs=st.lists(st.integers(0, 600), min_size=0, max_size=60))
+def test_partition_invariants_for_any_parameters(W, zf, H, degs):
+    """I1-I7 and the replay cover for parameters drawn over the whole
+    accepted range (1 <= W <= 32, W * Z <= 4096, 0 <= H <= 4096) and
+    arbitrary degree lists, including empty ones and rows far above
+    deg_bound."""
+    Z = 1 + int(zf * (4096 // W - 1))
+    n = len(degs)
+    g = graphgen.random_csr(n, 700, np.array(degs, dtype=np.int64), seed=n + W, dupes=True)
+    p = oracle.plan(g.rowptr, g.colidx, g.vals, W, Z, H)
+    _check_partition(p["rowptr_s"], p["meta"], W, Z, H)
+    X = np.random.default_rng(n).standard_normal((g.n_cols, 3)).astype(np.float32)
+    Y, cover, _, _ = oracle.replay_meta(
+        p["rowptr_s"], p["colidx_s"], p["vals_s"], p["perm"], p["meta"], W, Z, X)
+    assert np.all(cover == 1)
     assert np.array_equal(Y, oracle.spmm(g.rowptr, g.colidx, g.vals, X))
 
 
