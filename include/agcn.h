@@ -57,7 +57,11 @@ enum agcn_status {
  * vwarp holding at most Z = max_wave_nzs nnz; deg_bound = W * Z. Rows of
  * degree > deg_bound are cut into chunks of hub_chunk_nnz nnz (the paper
  * uses deg_bound; 0 selects deg_bound).
- * Limits: 1 <= W <= 32; 1 <= Z; W * Z <= 4096; 0 <= hub_chunk_nnz <= 4096.
+ * Limits: 1 <= W <= 32; 1 <= Z; W * Z <= 4096; 0 <= hub_chunk_nnz <= 4096;
+ * and one entry must fit the aggregation kernel's 64 KiB of LDS: the staged
+ * (column, value) pairs of the largest entry (max(W * Z, H), one pad word per
+ * 32) plus W * 64 float4 partial sums (one pad per 8). W = 32 with
+ * W * Z = 4096 exceeds it; agcn_plan_create then returns INVALID_ARGUMENT.
  * flags: 0 for the method itself, or one of the two baselines of the paper's
  * ablation study (Table II):
  *   AGCN_PLAN_WARP_LEVEL   no degree sort; each row in original order is cut

@@ -53,6 +53,30 @@ def test_plan_bit_exact_random(kw, seed):
     plan.destroy()
 
 
+def test_plan_bit_exact_drawn_parameters():
+    """Device plan against the oracle, and the SpMM, for 24 (W, Z, H) drawn
+    over the whole accepted range (1 <= W <= 32, W * Z <= 4096,
+    0 <= H <= 4096) on small graphs with empty, short and hub rows."""
+    rng = np.random.default_rng(2024)
+    ran = 0
+    for i in range(24):
+        W = int(rng.integers(1, 33))
+        Z = int(rng.integers(1, 4096 // W + 1))
+        H = int(rng.choice([0, int(rng.integers(1, 4097))]))
+        g = _mixed(100 + i, n=int(rng.integers(50, 3000)), hub_max=6000, dupes=bool(i % 2))
+        print(f"[drawn] W={W} Z={Z} H={H} n={g.n_rows} nnz={g.nnz}", flush=True)
+        try:
+            plan = _plan(g, max_block_waves=W, max_wave_nzs=Z, hub_chunk_nnz=H)
+        except agcn.AgcnError as e:   # the one further limit: one entry's staging in 64 KiB of LDS
+            assert e.status == agcn.AGCN_ERR_INVALID_ARGUMENT and "LDS" in str(e), str(e)
+            continue
+        assert_plan_matches_oracle(plan, g)
+        _spmm_check(plan, g, int(rng.choice([3, 16, 40])), seed=i)
+        plan.destroy()
+        ran += 1
+    assert ran >= 12
+
+
 @pytest.mark.parametrize("case", ["one_row", "all_empty", "deg_eq_bound", "deg_multiple_bound",
                                   "deg_bound_plus_one", "single_hub", "no_nnz_cols", "rect"])
 def test_plan_and_spmm_edge_cases(case):
