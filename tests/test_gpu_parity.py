@@ -286,6 +286,31 @@ def test_plan_reused_across_streams(mixed_plan):
     assert np.array_equal(Y.cpu().numpy(), ref)
 
 
+def test_concurrent_executes_of_one_plan_on_two_streams(mixed_plan):
+    """The plan is read-only during an execute: two executes of one plan
+    queued on two streams at once (each with its own Y and workspace, the
+    second with another F) both match their single-stream results bit for
+    bit."""
+    g, plan = mixed_plan
+    rng = np.random.default_rng(31)
+    Xa = _dev(rng.standard_normal((g.n_cols, 64)).astype(np.float32))
+    Xb = _dev(rng.standard_normal((g.n_cols, 96)).astype(np.float32))
+    ref_a, ref_b = plan.spmm(Xa).cpu().numpy(), plan.spmm(Xb).cpu().numpy()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    wsa, wsb = plan.workspace(64), plan.workspace(96)
+    Ya = torch.empty((g.n_rows, 64), device=DEV)
+    Yb = torch.empty((g.n_rows, 96), device=DEV)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        with torch.cuda.stream(sa):
+            plan.spmm(Xa, out=Ya, ws=wsa, stream=sa)
+        with torch.cuda.stream(sb):
+            plan.spmm(Xb, out=Yb, ws=wsb, stream=sb)
+    torch.cuda.synchronize()
+    assert np.array_equal(Ya.cpu().numpy().view(np.uint32), ref_a.view(np.uint32))
+    assert np.array_equal(Yb.cpu().numpy().view(np.uint32), ref_b.view(np.uint32))
+
+
 # ---------------------------------------------------------------------------
 # Input validation on the device and host-side errors with a live plan
 # ---------------------------------------------------------------------------
