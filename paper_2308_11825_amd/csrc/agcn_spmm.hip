@@ -10,7 +10,8 @@
 // halves, so the slice never drops below 128 bytes.
 //   1. The entry {deg, loc, row, info} is read once (uniform, scalar load).
 //   2. Its column indices and values -- contiguous in the sorted CSR -- are
-//      staged into LDS with non-temporal loads, 4 pairs per thread in flight.
+//      staged into LDS with plain loads (measured: non-temporal ones were
+//      2-6% slower), 4 pairs per thread in flight.
 //      The LDS index is padded by one word per 32 so the vwarps of a wave,
 //      which read slices a fixed stride apart, fall in different banks.
 //   3. Virtual warps (the paper's warps): a row of degree d is covered by
@@ -156,8 +157,8 @@ __global__ __launch_bounds__(1024) void k_spmm(
     for (int u = 0; u < kStageUnroll; ++u) {
       const int i = i0 + u * T + threadIdx.x;
       if (i < n_e) {
-        c[u] = __builtin_nontemporal_load(colidx_s + loc + i);
-        v[u] = __builtin_nontemporal_load(vals_s + loc + i);
+        c[u] = colidx_s[loc + i];
+        v[u] = vals_s[loc + i];
       }
     }
 #pragma unroll
@@ -307,8 +308,8 @@ __global__ __launch_bounds__(1024) void k_spmm_wl(
     for (int u = 0; u < kStageUnroll; ++u) {
       const int i = i0 + u * T + threadIdx.x;
       if (i < n_e) {
-        c[u] = __builtin_nontemporal_load(colidx_s + base + i);
-        v[u] = __builtin_nontemporal_load(vals_s + base + i);
+        c[u] = colidx_s[base + i];
+        v[u] = vals_s[base + i];
       }
     }
 #pragma unroll
@@ -409,8 +410,8 @@ __global__ __launch_bounds__(1024) void k_spmm_colloop(
   const int32_t rows = info & 0xFFFF;
   const int32_t n_e = hub ? info : rows * deg;
   for (int i = threadIdx.x; i < n_e; i += T) {
-    s_col[pad_idx(i)] = __builtin_nontemporal_load(colidx_s + loc + i);
-    s_val[pad_idx(i)] = __builtin_nontemporal_load(vals_s + loc + i);
+    s_col[pad_idx(i)] = colidx_s[loc + i];
+    s_val[pad_idx(i)] = vals_s[loc + i];
   }
   __syncthreads();
   const int32_t wn = (int32_t)((uint32_t)info >> 16);
