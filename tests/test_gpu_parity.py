@@ -77,6 +77,19 @@ def test_plan_bit_exact_drawn_parameters():
     assert ran >= 12
 
 
+@pytest.mark.parametrize("n", [64 * 4096 - 1, 64 * 4096, 64 * 4096 + 1])
+def test_plan_at_the_single_pass_scan_limit(n):
+    """The row-pointer scan has n values: up to 64 tiles of 4096 run in one
+    pass (decoupled look-back), more in two passes. Both sides of the limit
+    give the oracle's plan bit for bit and a matching SpMM."""
+    deg = np.random.default_rng(n).integers(0, 6, size=n)
+    g = graphgen.random_csr(n, n, deg, seed=n % 1000)
+    plan = _plan(g)
+    assert_plan_matches_oracle(plan, g)
+    _spmm_check(plan, g, 32, seed=3)
+    plan.destroy()
+
+
 @pytest.mark.parametrize("case", ["one_row", "all_empty", "deg_eq_bound", "deg_multiple_bound",
                                   "deg_bound_plus_one", "single_hub", "no_nnz_cols", "rect"])
 def test_plan_and_spmm_edge_cases(case):
