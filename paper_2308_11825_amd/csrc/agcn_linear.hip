@@ -28,6 +28,7 @@ namespace {
 
 typedef float f16v __attribute__((ext_vector_type(16)));
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 128;
 constexpr int kBK = 32;
@@ -176,15 +177,25 @@ __global__ __launch_bounds__(kThreads) void k_linear(int64_t n, int32_t fin, int
 //      columns) of KP floats (fin rounded up to KS * 16), zero outside W; the
 //      16-byte chunk c of row j sits at chunk c ^ (j & 7), so the 8 rows a
 //      group of lanes reads for one chunk fall in 8 different bank groups;
-//   2. wave v takes tiles v, v + waves, ... of 16 rows; the next tile's X is
-//      loaded into registers while the current one is multiplied;
-//   3. v_mfma_f32_16x16x4f32 (lane l supplies A[l % 16][l / 16] and
-//      B[l / 16][l % 16]; accumulator register r of lane l holds
-//      C[4 (l / 16) + r][l % 16]). The contraction order is permuted so that
-//      one 16-byte load per lane feeds four instructions: in k-step s, lane l
-//      loads X[row][16 s + 4 g .. + 3] (g = l / 16) and instruction t takes
-//      element t, paired with W^T[col][16 s + 4 g + t] from one 16-byte LDS
-//      read; the four instructions together cover k = 16 s .. 16 s + 15.
+//   2. wave v takes tiles v, v + waves, ... of 16 rows while every wave has a
+//      whole round left; the next tile's X is loaded into registers while the
+//      current one is multiplied. The tiles of the last, partial round are
+//      cut by output columns into as many ranges (1, 2, 4 or 8) as still give
+//      each range a wave of its own, so that round takes a fraction of a
+//      tile's time instead of a whole one;
+//   3. v_mfma_f32_16x16x4f32 with W^T as the left operand, so one instruction
+//      computes (X W)^T for 16 rows and 16 output columns (lane l supplies
+//      A[l % 16][l / 16] = W^T[col][k] and B[l / 16][l % 16] = X[row][k];
+//      accumulator register r of lane l holds C[4 (l / 16) + r][l % 16], that
+//      is H[row l % 16][4 (l / 16) + r]: four consecutive columns of one row,
+//      written with one 16-byte store). The contraction order is permuted so
+//      that one 16-byte load per lane feeds four instructions: in k-step s,
+//      lane l loads X[row][16 s + 4 g .. + 3] (g = l / 16) and instruction t
+//      takes element t, paired with W^T[col][16 s + 4 g + t] from one 16-byte
+//      LDS read; the four instructions together cover k = 16 s .. 16 s + 15.
+//      The compiler keeps all of W^T in registers across the tile loop (one
+//      wave per SIMD); re-reading it from LDS at two waves per SIMD measured
+//      no faster.
 constexpr int kRwThreads = 256;
 constexpr int kRwWaves = kRwThreads / 64;
 constexpr int kRwRows = 16;
@@ -245,29 +256,27 @@ __global__ __launch_bounds__(kRwThreads) void k_linear_rw(int64_t n, int32_t fin
       xv[s] = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, 0));
     }
   };
-  // H stores of one tile, branch-free (masked rows and columns get the
-  // out-of-range offset).
+  // H stores of one tile: lane (i, g) holds H[row i][16 b + 4 g .. + 3] of
+  // every column block b, one 16-byte store each.
   const uint32_t ldh4 = (uint32_t)(ldh * 4);
   auto store_h = [&](int64_t tile, const f4* acc) {
-    const int64_t rbase = tile * kRwRows + 4 * g;
-    const uint32_t base = (uint32_t)(rbase * ldh4) + (uint32_t)(4 * i);
+    const int64_t row = tile * kRwRows + i;
+    const uint32_t base = (uint32_t)(row * ldh4) + (uint32_t)(16 * g);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const bool row_ok = rbase + r < n;
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const bool ok = row_ok && 16 * b + i < fout;
-        const uint32_t off = ok ? base + (uint32_t)r * ldh4 + (uint32_t)(64 * b) : kRwOutOfRange;
-        const float v = acc[b][r];  // a scalar first: bit_cast of a vector element is not one
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), hr, (int)off, 0, 0);
-      }
+    for (int b = 0; b < NB; ++b) {
+      const bool ok = row < n && 16 * b + 4 * g < fout;
+      const uint32_t off = ok ? base + (uint32_t)(64 * b) : kRwOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, acc[b]), hr, (int)off, 0, 0);
     }
   };
+  // Full rounds: every wave takes n_tiles / n_waves tiles.
+  const int64_t wid = (int64_t)blockIdx.x * kRwWaves + wave;
+  const int64_t n_full = (n_tiles / n_waves) * n_waves;
   f4 xa[KS], xb[KS];
-  int64_t tile = (int64_t)blockIdx.x * kRwWaves + wave;
-  load_x(tile, xa);
-  for (; tile < n_tiles; tile += n_waves) {
-    load_x(tile + n_waves, xb);  // past the last tile: rows >= n, zeros
+  int64_t tile = wid;
+  if (tile < n_full) load_x(tile, xa);
+  for (; tile < n_full; tile += n_waves) {
+    if (tile + n_waves < n_full) load_x(tile + n_waves, xb);  // uniform
     f4 acc[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[b] = f4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -281,11 +290,39 @@ __global__ __launch_bounds__(kRwThreads) void k_linear_rw(int64_t n, int32_t fin
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int b = 0; b < NB; ++b)
-          acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[s][t], wv[b][t], acc[b], 0, 0, 0);
+          acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[b][t], xa[s][t], acc[b], 0, 0, 0);
     }
     store_h(tile, acc);
 #pragma unroll
     for (int s = 0; s < KS; ++s) xa[s] = xb[s];
+  }
+  // The last, partial round: its tiles are cut into `split` column ranges of
+  // NB / split blocks each, as many as keep every unit on its own wave.
+  const int64_t rem = n_tiles - n_full;
+  if (rem == 0) return;
+  int split = 1;
+  while (split < NB && rem * split * 2 <= n_waves) split *= 2;
+  const int per = NB / split;
+  for (int64_t u = wid; u < rem * split; u += n_waves) {
+    const int64_t t2 = n_full + u / split;
+    const int b0 = (int)(u % split) * per;
+    load_x(t2, xa);
+    const int64_t row = t2 * kRwRows + i;
+    for (int bb = 0; bb < per; ++bb) {
+      const int b = b0 + bb;
+      f4 acc = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const f4 wv = *reinterpret_cast<const f4*>(swt + wt_index(16 * b + i, 16 * s + 4 * g, KC));
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(wv[t], xa[s][t], acc, 0, 0, 0);
+      }
+      const bool ok = row < n && 16 * b + 4 * g < fout;
+      const uint32_t off = ok ? (uint32_t)(row * ldh4) + (uint32_t)(16 * g) + (uint32_t)(64 * b)
+                              : kRwOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, acc), hr, (int)off, 0, 0);
+    }
   }
 }
 

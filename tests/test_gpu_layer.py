@@ -50,6 +50,43 @@ def test_linear_matches_oracle(n, fin, fout):
     _check_linear(X, W, H, f"n={n} fin={fin} fout={fout}")
 
 
+def _resident_waves():
+    # Waves the W-resident kernel runs at the widths below: one workgroup of 4
+    # waves per compute unit.
+    return torch.cuda.get_device_properties(0).multi_processor_count * 4
+
+
+_LAST_ROUND = {"one": lambda w: 1, "eighth": lambda w: w // 8, "eighth+1": lambda w: w // 8 + 1,
+               "quarter+1": lambda w: w // 4 + 1, "half+1": lambda w: w // 2 + 1,
+               "all-3": lambda w: w - 3}
+
+
+@pytest.mark.parametrize("last,fin,fout,short", [("one", 128, 128, 3), ("eighth", 128, 128, 5),
+                                                 ("eighth+1", 128, 128, 0), ("eighth", 100, 60, 7),
+                                                 ("quarter+1", 128, 128, 1), ("quarter+1", 32, 32, 0),
+                                                 ("half+1", 128, 128, 2), ("all-3", 64, 128, 9)])
+def test_linear_last_round_split_by_columns(last, fin, fout, short):
+    """16-row tiles past the last whole round of waves are cut by output
+    columns (1, 2, 4 or 8 ranges, depending on how many are left). Every
+    output row stays within the oracle's bound, and is bit-identical to the
+    same row computed inside a whole round: the rows are rotated so that the
+    last round's rows come first and the outputs compared row by row."""
+    waves = _resident_waves()
+    rem = _LAST_ROUND[last](waves)
+    tiles = 2 * waves + rem
+    n = 16 * tiles - short
+    rng = np.random.default_rng(tiles + fin + fout + short)
+    X = rng.standard_normal((n, fin)).astype(np.float32)
+    W = graphgen.weights(fin, fout, seed=fin * 7 + fout)
+    print(f"[linear tail] n={n} tiles={tiles} rem={rem} fin={fin} fout={fout}", flush=True)
+    H = agcn.linear(_dev(X), _dev(W)).cpu().numpy()
+    _check_linear(X, W, H, f"n={n} fin={fin} fout={fout}")
+    cut = 16 * 2 * waves
+    Xr = np.ascontiguousarray(np.concatenate([X[cut:], X[:cut]]))
+    Hr = agcn.linear(_dev(Xr), _dev(W)).cpu().numpy()
+    assert np.array_equal(np.concatenate([H[cut:], H[:cut]]), Hr)
+
+
 def test_linear_strided_unaligned_and_deterministic():
     rng = np.random.default_rng(3)
     n, fin, fout = 3001, 64, 48
