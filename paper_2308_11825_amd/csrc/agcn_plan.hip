@@ -455,12 +455,16 @@ __global__ __launch_bounds__(kThreads) void k_scan_down(const int32_t* __restric
 // new for every scan, so words left by earlier scans read as not ready and
 // the status array needs no clearing. The wait is bounded; running out of it
 // raises the internal-error flag instead of hanging.
+// The status word is the only data one workgroup reads from another, and it
+// carries its value, so its loads and stores are relaxed device-scope atomics
+// (coherent past the per-XCD L2s): acquire and release would add an L2
+// invalidate to every poll and an L2 write-back to every publish.
 constexpr uint32_t kLookBackSpins = 1u << 22;
 
 __device__ inline void publish(unsigned long long* w, uint32_t state, uint32_t epoch, int32_t v) {
   const unsigned long long x = ((unsigned long long)state << 62) |
                                ((unsigned long long)(epoch & 0x3FFFFFFFu) << 32) | (uint32_t)v;
-  __hip_atomic_store(w, x, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(w, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __global__ __launch_bounds__(kThreads) void k_scan_chained(
@@ -508,7 +512,7 @@ __global__ __launch_bounds__(kThreads) void k_scan_chained(
         uint32_t state = 0;
         int32_t val = 0;
         if (j >= 0) {
-          const unsigned long long w = __hip_atomic_load(status + j, __ATOMIC_ACQUIRE,
+          const unsigned long long w = __hip_atomic_load(status + j, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT);
           if ((uint32_t)(w >> 32 & 0x3FFFFFFFu) == (epoch & 0x3FFFFFFFu)) state = (uint32_t)(w >> 62);
           val = (int32_t)(uint32_t)w;
