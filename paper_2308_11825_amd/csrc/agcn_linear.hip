@@ -398,9 +398,10 @@ int run_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx
   const bool vec = fin % 4 == 0 && fout % 4 == 0 && ldx % 4 == 0 && ldw % 4 == 0 &&
                    aligned16(X) && aligned16(W);
   // k_linear_rw addresses X and H with 32-bit byte offsets, and its masked
-  // offset must lie past both (see kRwOutOfRange).
+  // offset must lie past both (see kRwOutOfRange); it writes H in 16-byte
+  // pieces, so H's rows must be 16-byte aligned too.
   const int64_t lim = (int64_t)kRwOutOfRange - 16;
-  const bool rw_fits = n * ldx * 4 <= lim && n * ldh * 4 <= lim;
+  const bool rw_fits = n * ldx * 4 <= lim && n * ldh * 4 <= lim && ldh % 4 == 0 && aligned16(H);
   if (vec && rw_fits && fin >= 1 && fin <= 128 && fout <= 128 && !rw_disabled()) {
     if (fout <= 32) return dispatch_rw<2>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
     if (fout <= 64) return dispatch_rw<4>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);

@@ -109,6 +109,24 @@ def test_linear_strided_unaligned_and_deterministic():
     assert torch.all(Hs[:, fout:] == 9.0)
 
 
+@pytest.mark.parametrize("offset,pad", [(1, 4), (0, 3), (1, 3)])
+def test_linear_output_rows_not_16_byte_aligned(offset, pad):
+    """fin, fout <= 128 with X and W aligned, but H's rows not all 16-byte
+    aligned (H one float past an aligned address, or a row stride that is not
+    a multiple of 4): the resident-W kernel writes 16-byte pieces, so the
+    tiled kernel runs instead. Within the bound; padding untouched."""
+    rng = np.random.default_rng(21 + offset + pad)
+    n, fin, fout = 3001, 128, 128
+    X = rng.standard_normal((n, fin)).astype(np.float32)
+    W = graphgen.weights(fin, fout, seed=22)
+    ld = fout + pad
+    buf = torch.full((n * ld + offset,), 5.0, device=DEV)
+    Hs = buf[offset:].view(n, ld)
+    agcn.linear(_dev(X), _dev(W), out=Hs[:, :fout])
+    _check_linear(X, W, Hs[:, :fout].cpu().numpy(), f"offset={offset} ldh={ld}")
+    assert torch.all(Hs[:, fout:] == 5.0) and torch.all(buf[:offset] == 5.0)
+
+
 def test_linear_identity_is_exact():
     X = np.random.default_rng(5).standard_normal((1000, 96)).astype(np.float32)
     H = agcn.linear(_dev(X), _dev(np.eye(96, dtype=np.float32))).cpu().numpy()
