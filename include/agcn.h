@@ -117,10 +117,14 @@ void agcn_default_params(agcn_plan_params* p);
  * Inputs: d_rowptr[n_rows + 1], d_colidx[nnz], d_vals[nnz] on the current
  * device; params NULL = defaults. The plan copies what it needs (sorted
  * permutation, sorted CSR copy, metadata); the inputs may be freed once the
- * call returns. Work is ordered on `stream`; the call synchronises that
- * stream once (to read back the number of metadata entries). `stream` must
- * remain valid until the plan is destroyed (agcn_plan_destroy marks the
- * plan's last work on it).
+ * call returns (every kernel that reads them has finished by then). Work is
+ * ordered on `stream`. The call waits on the host, by polling pinned memory,
+ * for two results the device writes there: the maximum degree and the number
+ * of metadata entries. The plan's last kernels may still run on `stream` when
+ * it returns; later work on that stream comes after them, and agcn_spmm* on
+ * another stream waits for them. The warp-level plan (AGCN_PLAN_WARP_LEVEL)
+ * synchronises `stream` instead. `stream` must remain valid until the plan is
+ * destroyed (agcn_plan_destroy marks the plan's last work on it).
  *
  * The CSR is validated on the device: rowptr[0] == 0, non-decreasing,
  * rowptr[n_rows] == nnz, 0 <= colidx[e] < n_cols. A violation returns
@@ -225,7 +229,8 @@ int agcn_gcn_layer(agcn_plan_t plan, int32_t fin, int32_t fout, const float* d_X
 /* Fills *out. Host-only, no HIP call. */
 int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* out);
 
-/* Copies the plan to host memory (synchronous).
+/* Copies the plan to host memory (synchronous: waits for the plan's kernels
+ * first).
  * Any pointer may be NULL to skip that array. Sizes: h_perm[n_rows] (sorted
  * position -> original row), h_rowptr_s[n_rows + 1], h_colidx_s[nnz],
  * h_vals_s[nnz] (the CSR with rows in sorted order), h_meta[4 * n_entries]

@@ -54,21 +54,23 @@ int hip_fail(hipError_t e, const char* what) {
 // cached, one block per device, and the next plan on that device reuses it
 // when it fits without wasting more than half of it. The block travels with
 // events marking its previous owner's last work on every stream; the reusing
-// plan's stream waits on them, so nothing blocks on the host.
+// plan's stream waits on those of the other streams (on its own stream, stream
+// order already does it, and a wait would add a barrier packet, around which
+// the GPU idles for microseconds), so nothing blocks on the host.
 namespace {
 struct CachedBlock {
   void* ptr = nullptr;
   size_t bytes = 0;
-  std::vector<hipEvent_t> pending;
+  std::vector<StreamEvent> pending;
 };
 std::mutex g_cache_mu;
 std::map<int, CachedBlock> g_cache;
 
 // Frees a block no plan will reuse (the caller has made its device current).
 void free_block(CachedBlock& b) {
-  for (hipEvent_t ev : b.pending) {
-    (void)hipEventSynchronize(ev);
-    (void)hipEventDestroy(ev);
+  for (const StreamEvent& se : b.pending) {
+    (void)hipEventSynchronize(se.ev);
+    (void)hipEventDestroy(se.ev);
   }
   b.pending.clear();
   if (b.ptr) (void)hipFree(b.ptr);
@@ -96,12 +98,12 @@ int device_alloc(int device, size_t bytes, hipStream_t stream, void** out, size_
     }
   }
   if (reuse.ptr != nullptr) {
-    for (hipEvent_t ev : reuse.pending) {
-      if (hipStreamWaitEvent(stream, ev, 0) != hipSuccess) {
+    for (const StreamEvent& se : reuse.pending) {
+      if (se.stream != stream && hipStreamWaitEvent(stream, se.ev, 0) != hipSuccess) {
         (void)hipGetLastError();
-        (void)hipEventSynchronize(ev);
+        (void)hipEventSynchronize(se.ev);
       }
-      (void)hipEventDestroy(ev);
+      (void)hipEventDestroy(se.ev);
     }
     *out = reuse.ptr;
     *got = reuse.bytes;
@@ -132,7 +134,7 @@ int device_alloc(int device, size_t bytes, hipStream_t stream, void** out, size_
   return AGCN_OK;
 }
 
-void device_release(int device, void* ptr, size_t bytes, std::vector<hipEvent_t> pending) {
+void device_release(int device, void* ptr, size_t bytes, std::vector<StreamEvent> pending) {
   int prev = 0;
   if (with_device(device, &prev) != AGCN_OK) return;
   CachedBlock incoming{ptr, bytes, std::move(pending)};
@@ -205,9 +207,9 @@ const char* agcn_last_error(void) { return agcn::g_last_error.c_str(); }
 
 static void plan_free(agcn_plan* p) {
   if (p == nullptr) return;
-  std::vector<hipEvent_t> pending;
-  if (p->ready != nullptr) pending.push_back(p->ready);
-  for (auto& u : p->uses) pending.push_back(u.second);
+  std::vector<agcn::StreamEvent> pending;
+  if (p->ready != nullptr) pending.push_back({p->ready, p->stream});
+  for (auto& u : p->uses) pending.push_back({u.second, u.first});
   // Calls on the plan's own stream record no event of their own: one event
   // recorded now on that stream follows all of them (and the plan's kernels).
   if (p->base != nullptr) {
@@ -216,7 +218,7 @@ static void plan_free(agcn_plan* p) {
     if (agcn::with_device(p->device, &prev) == AGCN_OK) {
       if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess &&
           hipEventRecord(ev, p->stream) == hipSuccess) {
-        pending.push_back(ev);
+        pending.push_back({ev, p->stream});
       } else {
         (void)hipGetLastError();
         if (ev) (void)hipEventDestroy(ev);
@@ -516,6 +518,10 @@ int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s, int
   if (he != hipSuccess) return agcn::hip_fail(he, "hipGetDevice");
   if (dev != plan->device)
     return fail(AGCN_ERR_INVALID_ARGUMENT, "current device differs from the plan's device");
+  // The plan's last kernels may still run on its stream, which the copies
+  // below (on the null stream) need not wait for.
+  if (plan->ready != nullptr && (he = hipEventSynchronize(plan->ready)) != hipSuccess)
+    return agcn::hip_fail(he, "hipEventSynchronize(plan ready)");
   for (const Item& it : items) {
     if (it.dst == nullptr || it.bytes == 0) continue;
     he = hipMemcpy(it.dst, it.src, it.bytes, hipMemcpyDeviceToHost);

@@ -22,7 +22,9 @@ enum : uint32_t {
   kErrColumn = 1u << 3,        // a column index outside [0, n_cols)
 };
 
-// Facts the device computes while partitioning; read back once.
+// Facts the device computes while partitioning, written into pinned host
+// memory. dmax_ready and done are set (after a system-scope fence) once
+// max_deg, and then everything else, can be read.
 struct PlanSummary {
   int32_t n_entries;
   int32_t hub_first_entry;
@@ -30,7 +32,8 @@ struct PlanSummary {
   int32_t hub_first_row;
   int32_t max_deg;
   uint32_t err;
-  int32_t pad[2];
+  uint32_t dmax_ready;
+  uint32_t done;
 };
 
 // Largest number of (column, value) pairs one metadata entry stages in LDS.
@@ -97,13 +100,20 @@ int run_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx
 // Dynamic LDS bytes the SpMM kernel needs for a plan (worst case over F).
 size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz);
 
+// An event and the stream it was recorded on.
+struct StreamEvent {
+  hipEvent_t ev;
+  hipStream_t stream;
+};
+
 // Plan memory. device_alloc may hand back the block a destroyed plan left in
 // the per-device cache (*got receives its size, >= bytes); `stream` then
-// waits (device-side) on the events that mark the previous owner's last work.
-// device_release keeps the block cached (one per device) with those events and
-// takes ownership of them; it does not block.
+// waits (device-side) on the events that mark the previous owner's last work
+// on other streams; on `stream` itself its own order already puts that work
+// first. device_release keeps the block cached (one per device) with those
+// events and takes ownership of them; it does not block.
 int device_alloc(int device, size_t bytes, hipStream_t stream, void** out, size_t* got);
-void device_release(int device, void* ptr, size_t bytes, std::vector<hipEvent_t> pending);
+void device_release(int device, void* ptr, size_t bytes, std::vector<StreamEvent> pending);
 
 // Records, on `stream`, the event that marks the plan's last work there.
 void note_use(agcn_plan* p, hipStream_t stream);

@@ -1,9 +1,9 @@
 // Device-side preprocessing: degree sort and block-level partition
 // (Sec. III-C "Degree Sorting" and "Block-level Partition", Alg. 1 and Alg. 2).
 //
-// Pipeline (all on one stream; the host waits twice: on an event once the
-// maximum degree is known -- radix passes 0 and 1 are already queued -- and on
-// the stream after the partition):
+// Pipeline (all on one stream; the host waits twice: for the maximum degree
+// -- radix passes 0 and 1 are already queued -- and for the partition's
+// summary):
 //   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
 //                   per-workgroup maximum degree and error flags
 //   k_dmax          maximum degree (one workgroup); written to pinned host
@@ -23,14 +23,17 @@
 //                   order; first chunk of each hub row; summary for the host;
 //                   launch order: hub chunks, then the other entries
 //                   heaviest first
-//   (host sync)     entry counts read back
+//   (host wait)     entry counts read back
 //   launch order    when hub rows are long: hub-chunk entries re-sorted by a
 //                   16-bit key of their first column (two radix passes), then
 //                   the other entries; an event marks the plan ready
 //
 // The two read-backs (maximum degree, summary) are written by the kernels
-// straight into pinned, host-coherent memory; the host reads them after the
-// event or stream synchronisation, with no copy launched.
+// straight into pinned, host-coherent memory, each followed by a ready flag
+// that the host polls, with no copy launched. Polling keeps event markers out
+// of the stream (the GPU idles several microseconds around each) and avoids a
+// blocking synchronisation's wake-up (about 30 us from the partition's last
+// kernel to the next launch).
 //
 // Stability of the radix sort comes from giving each 64-lane wave a tile of
 // consecutive rows that it walks in order, ranking equal digits inside a
@@ -45,7 +48,8 @@
 #include <climits>
 #include <cstdlib>
 #include <atomic>
-#include <map>
+#include <string>
+#include <thread>
 
 #include "agcn_internal.hpp"
 
@@ -249,6 +253,8 @@ __global__ __launch_bounds__(kScanTopThreads) void k_dmax(const int32_t* __restr
     dmax[0] = t;
     err[0] = f;
     host_sum->max_deg = t;
+    __threadfence_system();
+    host_sum->dmax_ready = 1;
     __threadfence_system();
   }
 }
@@ -749,7 +755,7 @@ __global__ __launch_bounds__(kThreads) void k_seg_count(int32_t n, const int32_t
 //   - Alg. 2's entries, each from its segment;
 //   - the first chunk of each hub row, and the summary read back by the host;
 //   - the SpMM launch order: hub chunks, then the other entries heaviest
-//     first (rewritten after the host synchronisation when hub chunks are
+//     first (rewritten after the host has read the summary when hub chunks are
 //     launched in column order; it never changes a result).
 __global__ __launch_bounds__(kThreads) void k_partition_fill(
     int32_t n, const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ deg_s,
@@ -762,7 +768,11 @@ __global__ __launch_bounds__(kThreads) void k_partition_fill(
   const uint32_t e = err[0];
   if (t0 == 0) {
     sum->err = e;
-    if (e) __threadfence_system();
+    if (e) {
+      __threadfence_system();
+      sum->done = 1;
+      __threadfence_system();
+    }
   }
   if (e) return;
   const int32_t total = seg_off[S];
@@ -802,6 +812,8 @@ __global__ __launch_bounds__(kThreads) void k_partition_fill(
     sum->n_hub_rows = n_hub;
     sum->hub_first_row = first_hub_row;
     sum->max_deg = n > 0 ? deg_s[n - 1] : 0;
+    __threadfence_system();
+    sum->done = 1;
     __threadfence_system();
   }
 }
@@ -1016,20 +1028,22 @@ PlanSummary* pinned_summary(PlanSummary** dev) {
   return buf;
 }
 
-// Per-thread, per-device event marking the maximum-degree read-back.
-hipEvent_t plan_event() {
-  thread_local std::map<int, hipEvent_t> events;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
-  auto it = events.find(dev);
-  if (it != events.end()) return it->second;
-  hipEvent_t e = nullptr;
-  if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
-    (void)hipGetLastError();
-    return nullptr;
+// Waits until the device sets *flag, a word of the pinned summary, polling
+// it; every 64 polls the stream is queried, so a failed launch or a stream
+// that finished without setting the flag ends the wait with an error.
+int wait_flag(const uint32_t* flag, hipStream_t st, const char* what) {
+  for (uint32_t it = 1;; ++it) {
+    if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) != 0) return AGCN_OK;
+    if ((it & 63) == 0) {
+      const hipError_t q = hipStreamQuery(st);
+      if (q == hipSuccess) {
+        if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) != 0) return AGCN_OK;
+        return fail(AGCN_ERR_HIP, std::string(what) + ": the stream finished without the result");
+      }
+      if (q != hipErrorNotReady) return hip_fail(q, what);
+    }
+    std::this_thread::yield();
   }
-  events[dev] = e;
-  return e;
 }
 
 struct Layout {
@@ -1202,7 +1216,9 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   PlanSummary* dsum = nullptr;
   PlanSummary* hs = pinned_summary(&dsum);
   if (hs == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "pinned host buffer allocation failed");
-  *hs = PlanSummary{};  // no kernel of this thread's previous plan is still running
+  // No kernel of this thread's previous plan writes the summary any more: its
+  // last write came before the flag that plan waited for.
+  *hs = PlanSummary{};
   hipError_t he;
   uint32_t* berr = reinterpret_cast<uint32_t*>(bmax + n_deg_blocks + 1);
   if (n > 0)
@@ -1218,10 +1234,6 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   if (n > 0) {
     // The maximum degree reaches the host while radix pass 0 (always needed)
     // runs; the host then launches exactly the passes it needs.
-    hipEvent_t ev = plan_event();
-    if (ev == nullptr || (he = hipEventRecord(ev, st)) != hipSuccess)
-      return hip_fail(ev ? he : hipErrorOutOfMemory, "hipEventRecord(plan)");
-
     // Stable LSD radix sort of row ids by degree, 8-bit digits. Passes 0 and
     // 1 are queued before the host reads the maximum degree (pass 1 returns
     // at once on the device when one pass suffices), so the GPU keeps busy
@@ -1241,7 +1253,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
                                                   err, dmax);
       if ((rc = check_launch("k_radix_scatter"))) return rc;
       if (pass == kPassesBeforeReadback - 1) {
-        if ((he = hipEventSynchronize(ev)) != hipSuccess) return hip_fail(he, "hipEventSynchronize");
+        if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
         const int32_t md = hs->max_deg;
         int bits = 0;
         while (bits < 31 && (int64_t(1) << bits) <= md) ++bits;
@@ -1270,8 +1282,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
                                                p->hub_chunk_off, p->order, dsum, err);
   if ((rc = check_launch("partition fill"))) return rc;
 
-  he = hipStreamSynchronize(st);
-  if (he != hipSuccess) return hip_fail(he, "hipStreamSynchronize(plan)");
+  if ((rc = wait_flag(&hs->done, st, "plan summary read-back"))) return rc;
   if (hs->err) {
     std::string why;
     if (hs->err & kErrRowptrStart) why += " rowptr[0] != 0;";
@@ -1287,7 +1298,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   p->hub_first_row = hs->hub_first_row;
   p->max_deg = hs->max_deg;
 
-  // Hub chunks in column order: queued after the synchronisation; agcn_spmm
+  // Hub chunks in column order: queued after the summary read-back; agcn_spmm
   // waits for the event recorded below.
   const int32_t n_chunks = p->n_hub_rows > 0 ? p->n_entries - p->hub_first_entry : 0;
   const int32_t* sorted_ids = nullptr;

@@ -324,6 +324,44 @@ def test_concurrent_executes_of_one_plan_on_two_streams(mixed_plan):
     assert np.array_equal(Yb.cpu().numpy().view(np.uint32), ref_b.view(np.uint32))
 
 
+def test_plan_on_a_side_stream_used_at_once():
+    """agcn_plan_create returns once the device has written the plan's
+    summary; its last kernels may still run on the plan's stream. An export
+    right away, an execute on another stream, and the next plans that reuse
+    the cached plan memory (on the same stream, then on another) all see the
+    finished plan: bit-exact plans, executes equal bit for bit."""
+    g = _mixed(77, n=6000, hub_max=4000)
+    rng = np.random.default_rng(78)
+    X = _dev(rng.standard_normal((g.n_cols, 64)).astype(np.float32))
+    Y, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X.cpu().numpy(), want_scale=True)
+    rp, ci, va = _dev(g.rowptr), _dev(g.colidx), _dev(g.vals)
+    side, other = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    first = None
+    for rep in range(3):
+        print(f"[side stream] rep {rep}", flush=True)
+        p1 = agcn.Plan(rp, ci, va, n_cols=g.n_cols, stream=side)
+        assert_plan_matches_oracle(p1, g)
+        with torch.cuda.stream(other):
+            Y1 = p1.spmm(X, stream=other)
+        other.synchronize()
+        Y1 = Y1.cpu().numpy()
+        assert_close(Y1, Y, S, "execute on another stream")
+        first = Y1 if first is None else first
+        assert np.array_equal(Y1.view(np.uint32), first.view(np.uint32))
+        p1.destroy()
+        p2 = agcn.Plan(rp, ci, va, n_cols=g.n_cols, stream=side)
+        with torch.cuda.stream(side):
+            Y2 = p2.spmm(X, stream=side)
+        side.synchronize()
+        assert np.array_equal(Y2.cpu().numpy().view(np.uint32), first.view(np.uint32))
+        p2.destroy()
+        p3 = agcn.Plan(rp, ci, va, n_cols=g.n_cols, stream=other)
+        assert_plan_matches_oracle(p3, g)
+        p3.destroy()
+    torch.cuda.synchronize()
+
+
 # ---------------------------------------------------------------------------
 # Input validation on the device and host-side errors with a live plan
 # ---------------------------------------------------------------------------
