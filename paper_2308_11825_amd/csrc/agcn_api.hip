@@ -155,6 +155,25 @@ void device_release(int device, void* ptr, size_t bytes, std::vector<StreamEvent
   if (prev != device) (void)hipSetDevice(prev);
 }
 
+// Recorded only when needed: an execute on another stream, or a host copy.
+// Recording it at the end of every plan cost about 5 us of host time on the
+// way to the first execute, which usually runs on the plan's own stream.
+int plan_ready_event(agcn_plan* p, hipEvent_t* out) {
+  std::lock_guard<std::mutex> lk(p->use_mu);
+  if (p->ready == nullptr) {
+    hipEvent_t ev = nullptr;
+    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreate(plan ready)");
+    if ((e = hipEventRecord(ev, p->stream)) != hipSuccess) {
+      (void)hipEventDestroy(ev);
+      return hip_fail(e, "hipEventRecord(plan ready)");
+    }
+    p->ready = ev;
+  }
+  *out = p->ready;
+  return AGCN_OK;
+}
+
 void note_use(agcn_plan* p, hipStream_t stream) {
   std::lock_guard<std::mutex> lk(p->use_mu);
   for (auto& u : p->uses) {
@@ -370,6 +389,14 @@ int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
                       agcn::ranges_overlap(d_ws, ws_need, d_X, xb)))
     return fail(AGCN_ERR_INVALID_ARGUMENT, "workspace overlaps X or Y");
   if (int rc = check_device(plan)) return rc;
+  // The plan's last kernels may still run on its stream: order another
+  // stream after them (on the plan's own stream they already come first).
+  if (static_cast<hipStream_t>(stream) != plan->stream) {
+    hipEvent_t ready = nullptr;
+    if (int rc = agcn::plan_ready_event(plan, &ready)) return rc;
+    const hipError_t e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), ready, 0);
+    if (e != hipSuccess) return agcn::hip_fail(e, "hipStreamWaitEvent(plan ready)");
+  }
   const int rc = agcn::run_spmm(plan, F, d_X, ldx, d_Y, ldy, static_cast<float*>(d_ws),
                                 static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(ev_begin),
                                 static_cast<hipEvent_t>(ev_mid), static_cast<hipEvent_t>(ev_end),
@@ -520,7 +547,9 @@ int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s, int
     return fail(AGCN_ERR_INVALID_ARGUMENT, "current device differs from the plan's device");
   // The plan's last kernels may still run on its stream, which the copies
   // below (on the null stream) need not wait for.
-  if (plan->ready != nullptr && (he = hipEventSynchronize(plan->ready)) != hipSuccess)
+  hipEvent_t ready = nullptr;
+  if (int rc = agcn::plan_ready_event(plan, &ready)) return rc;
+  if ((he = hipEventSynchronize(ready)) != hipSuccess)
     return agcn::hip_fail(he, "hipEventSynchronize(plan ready)");
   for (const Item& it : items) {
     if (it.dst == nullptr || it.bytes == 0) continue;

@@ -61,7 +61,7 @@ struct agcn_plan {
   int32_t* hub_chunk_off = nullptr; // [hub rows upper bound + 1] first chunk of each hub row
   int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
   int32_t* group_off = nullptr;     // warp-level plans: [n_rows + 1] first group of each row
-  hipEvent_t ready = nullptr;       // recorded after the launch order is built
+  hipEvent_t ready = nullptr;       // the plan's kernels done (plan_ready_event; use_mu)
   hipStream_t stream = nullptr;     // the stream the plan was built on (valid until destroy)
   // Last work of the plan on each stream other than its own that ran an
   // execute with it (one event per stream, re-recorded by every call; guarded
@@ -117,6 +117,10 @@ void device_release(int device, void* ptr, size_t bytes, std::vector<StreamEvent
 
 // Records, on `stream`, the event that marks the plan's last work there.
 void note_use(agcn_plan* p, hipStream_t stream);
+
+// The event after the plan's kernels, recorded on the plan's stream on the
+// first call (so it also covers work queued there since) and reused after.
+int plan_ready_event(agcn_plan* p, hipEvent_t* out);
 
 inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; }

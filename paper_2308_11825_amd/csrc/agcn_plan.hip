@@ -26,7 +26,7 @@
 //   (host wait)     entry counts read back
 //   launch order    when hub rows are long: hub-chunk entries re-sorted by a
 //                   16-bit key of their first column (two radix passes), then
-//                   the other entries; an event marks the plan ready
+//                   the other entries
 //
 // The two read-backs (maximum degree, summary) are written by the kernels
 // straight into pinned, host-coherent memory, each followed by a ready flag
@@ -1219,7 +1219,6 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   // No kernel of this thread's previous plan writes the summary any more: its
   // last write came before the flag that plan waited for.
   *hs = PlanSummary{};
-  hipError_t he;
   uint32_t* berr = reinterpret_cast<uint32_t*>(bmax + n_deg_blocks + 1);
   if (n > 0)
     k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, bmax,
@@ -1298,8 +1297,9 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   p->hub_first_row = hs->hub_first_row;
   p->max_deg = hs->max_deg;
 
-  // Hub chunks in column order: queued after the summary read-back; agcn_spmm
-  // waits for the event recorded below.
+  // Hub chunks in column order: queued after the summary read-back (an
+  // execute on another stream waits for the plan's kernels, see
+  // plan_ready_event).
   const int32_t n_chunks = p->n_hub_rows > 0 ? p->n_entries - p->hub_first_entry : 0;
   const int32_t* sorted_ids = nullptr;
   // Only long rows have chunks with narrow column ranges: sort when the hub
@@ -1328,11 +1328,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     k_order_fill<<<grid_for(p->n_entries, kThreads), kThreads, 0, st>>>(
         p->order, p->n_entries, p->hub_first_entry, n_chunks, sorted_ids);
   }
-  if ((rc = check_launch("launch order"))) return rc;
-  if ((he = hipEventCreateWithFlags(&p->ready, hipEventDisableTiming)) != hipSuccess)
-    return hip_fail(he, "hipEventCreate(plan ready)");
-  if ((he = hipEventRecord(p->ready, st)) != hipSuccess) return hip_fail(he, "hipEventRecord(plan ready)");
-  return AGCN_OK;
+  return check_launch("launch order");
 }
 
 }  // namespace

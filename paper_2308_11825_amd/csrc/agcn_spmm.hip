@@ -692,11 +692,6 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
                    aligned16(Y) && (ws == nullptr || aligned16(ws));
   const SpmmArgs a{p, F, X, ldx, Y, ldy, ws, st, act};
   hipError_t e;
-  // The plan's last kernels (the launch order) were queued on the plan's
-  // stream after its host synchronisation; order another stream after them
-  // (on the plan's own stream they already come first).
-  if (p->ready && st != p->stream && (e = hipStreamWaitEvent(st, p->ready, 0)) != hipSuccess)
-    return hip_fail(e, "hipStreamWaitEvent(plan ready)");
   if (p->n_entries == 0) {  // no rows (hub rows need entries): keep the marks meaningful
     for (hipEvent_t ev : {ev_begin, ev_mid, ev_end})
       if (ev && (e = hipEventRecord(ev, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
