@@ -1336,8 +1336,12 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
 int build_plan(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
                const float* d_vals, hipStream_t st) {
   p->stream = st;
-  return (p->flags & AGCN_PLAN_WARP_LEVEL) ? build_plan_warp_level(p, d_rowptr, d_colidx, d_vals, st)
-                                          : build_plan_block(p, d_rowptr, d_colidx, d_vals, st);
+  if (p->flags & AGCN_PLAN_WARP_LEVEL) return build_plan_warp_level(p, d_rowptr, d_colidx, d_vals, st);
+  const int rc = build_plan_block(p, d_rowptr, d_colidx, d_vals, st);
+  // A plan that failed after launching kernels lets them finish first: they
+  // write this thread's pinned summary, which the next plan polls.
+  if (rc != AGCN_OK) (void)hipStreamSynchronize(st);
+  return rc;
 }
 
 }  // namespace agcn

@@ -378,6 +378,10 @@ def test_invalid_csr_rejected_on_device():
     with pytest.raises(agcn.AgcnError) as ei:
         agcn.Plan(_dev(rp), _dev(g.colidx), _dev(g.vals), n_cols=100)
     assert ei.value.status == agcn.AGCN_ERR_INVALID_INPUT
+    # the next plan on this thread reads its own results, not the failed ones'
+    ok = _plan(g)
+    assert_plan_matches_oracle(ok, g)
+    ok.destroy()
     rp = g.rowptr.copy()
     rp[-1] -= 1
     with pytest.raises(agcn.AgcnError) as ei:
