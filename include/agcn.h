@@ -196,10 +196,10 @@ int agcn_spmm_ex(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
  * floats, stride ldw >= fout; d_H: n rows of fout floats, stride ldh >= fout.
  * All row-major, device memory owned by the caller; H must not overlap X or
  * W. fin = 0 gives H = 0. fp32 products and sums (matrix-core accumulation,
- * fin terms per element). Kernel choice: with fin and fout at most 128, fin,
- * fout, ldx, ldw and ldh multiples of 4, X, W and H 16-byte aligned and X and
- * H each under 4 GiB, W stays resident on chip while X streams past once;
- * otherwise a tiled kernel runs (128-bit loads when fin, fout, ldx and ldw are
+ * fin terms per element). Kernel choice: with fin at most 128, fin, fout,
+ * ldx, ldw and ldh multiples of 4, X, W and H 16-byte aligned and X and H
+ * each under 4 GiB, W stays resident on chip while X streams past (once per
+ * 128 output columns); otherwise a tiled kernel runs (128-bit loads when fin, fout, ldx and ldw are
  * multiples of 4 and X, W are 16-byte aligned, else 32-bit loads with the
  * same results). The two kernels add the fin products in different orders,
  * so their results may differ in the last bits; each is deterministic.

@@ -169,8 +169,8 @@ __global__ __launch_bounds__(kThreads) void k_linear(int64_t n, int32_t fin, int
 
 // --- W resident in LDS --------------------------------------------------------
 //
-// k_linear_rw: for fin <= 128 and fout <= 128 (128-bit path, X and H each
-// under 4 GiB), W^T stays in
+// k_linear_rw: for fin <= 128 and fout <= 128 (wider outputs: one launch per
+// 128 columns; 128-bit path, X and H each under 4 GiB), W^T stays in
 // LDS for the whole kernel and every wave works alone on 16-row tiles of X, so
 // the main loop has no workgroup barrier:
 //   1. each workgroup (4 waves) writes W^T into LDS once: NB * 16 rows (output
@@ -402,10 +402,22 @@ int run_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx
   // pieces, so H's rows must be 16-byte aligned too.
   const int64_t lim = (int64_t)kRwOutOfRange - 16;
   const bool rw_fits = n * ldx * 4 <= lim && n * ldh * 4 <= lim && ldh % 4 == 0 && aligned16(H);
-  if (vec && rw_fits && fin >= 1 && fin <= 128 && fout <= 128 && !rw_disabled()) {
-    if (fout <= 32) return dispatch_rw<2>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
-    if (fout <= 64) return dispatch_rw<4>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
-    return dispatch_rw<8>(n, fin, fout, X, ldx, W, ldw, H, ldh, st);
+  if (vec && rw_fits && fin >= 1 && fin <= 128 && !rw_disabled()) {
+    // Wider outputs run as one launch per 128 columns of W and H, each
+    // streaming X again (measured at 230,000 x 128 -> 256: two launches take
+    // less time than the tiled kernel). Every column's sum is the same as in
+    // a single launch.
+    for (int32_t c0 = 0; c0 < fout; c0 += 128) {
+      const int32_t w = std::min<int32_t>(128, fout - c0);
+      const float* Wc = W + c0;
+      float* Hc = H + c0;
+      int rc;
+      if (w <= 32) rc = dispatch_rw<2>(n, fin, w, X, ldx, Wc, ldw, Hc, ldh, st);
+      else if (w <= 64) rc = dispatch_rw<4>(n, fin, w, X, ldx, Wc, ldw, Hc, ldh, st);
+      else rc = dispatch_rw<8>(n, fin, w, X, ldx, Wc, ldw, Hc, ldh, st);
+      if (rc) return rc;
+    }
+    return AGCN_OK;
   }
   if (fout <= 32) return launch_linear<32>(n, fin, fout, X, ldx, W, ldw, H, ldh, st, vec);
   if (fout <= 64) return launch_linear<64>(n, fin, fout, X, ldx, W, ldw, H, ldh, st, vec);

@@ -40,7 +40,8 @@ def _check_linear(X, W, H, what=""):
 
 @pytest.mark.parametrize("n,fin,fout", [(1000, 128, 128), (777, 33, 17), (5000, 64, 16),
                                         (130, 1, 1), (300, 256, 300), (2000, 100, 40),
-                                        (129, 32, 32), (64, 0, 8), (4097, 12, 200)])
+                                        (129, 32, 32), (64, 0, 8), (4097, 12, 200),
+                                        (20011, 128, 256), (5003, 64, 300), (3000, 128, 132)])
 def test_linear_matches_oracle(n, fin, fout):
     rng = np.random.default_rng(n + fin + fout)
     X = rng.standard_normal((n, fin)).astype(np.float32)
@@ -125,6 +126,23 @@ def test_linear_output_rows_not_16_byte_aligned(offset, pad):
     agcn.linear(_dev(X), _dev(W), out=Hs[:, :fout])
     _check_linear(X, W, Hs[:, :fout].cpu().numpy(), f"offset={offset} ldh={ld}")
     assert torch.all(Hs[:, fout:] == 5.0) and torch.all(buf[:offset] == 5.0)
+
+
+def test_linear_wide_output_in_column_launches():
+    """fin <= 128 and fout > 128 run as one W-resident launch per 128 output
+    columns: within the bound, padding columns of a strided H untouched, and
+    each column bit-identical to the same column computed alone."""
+    rng = np.random.default_rng(41)
+    n, fin, fout = 3001, 96, 260
+    X = rng.standard_normal((n, fin)).astype(np.float32)
+    W = graphgen.weights(fin, fout, seed=42)
+    Hp = torch.full((n, fout + 12), 3.0, device=DEV)
+    agcn.linear(_dev(X), _dev(W), out=Hp[:, :fout])
+    H = Hp[:, :fout].cpu().numpy()
+    _check_linear(X, W, H, "wide output")
+    assert torch.all(Hp[:, fout:] == 3.0)
+    Hc = agcn.linear(_dev(X), _dev(np.ascontiguousarray(W[:, 128:256]))).cpu().numpy()
+    assert np.array_equal(H[:, 128:256].view(np.uint32), Hc.view(np.uint32))
 
 
 def test_linear_identity_is_exact():
