@@ -13,8 +13,6 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB_PATH = os.path.join(PKG, "libagcn.so")
 CSRC = os.path.join(PKG, "csrc")
-PROBE_SRC = os.path.join(PKG, "probe", "gather_probe.hip")
-PROBE_PATH = os.path.join(PKG, "probe", "gather_probe")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -49,11 +47,8 @@ def _hipcc(args, out_path, verbose):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every HIP source into libagcn.so, and the memory-ceiling probe
-    (probe/gather_probe, a standalone executable the library does not use).
-    Always recompiles."""
+    """Compile every HIP source into libagcn.so. Always recompiles."""
     _hipcc(["-shared", *sources()], LIB_PATH, verbose)
-    _hipcc([PROBE_SRC], PROBE_PATH, verbose)
     return LIB_PATH
 
 
