@@ -134,7 +134,16 @@ void agcn_default_params(agcn_plan_params* p);
  * Errors: INVALID_ARGUMENT (null out, negative sizes, null arrays with
  * n_rows > 0 or nnz > 0, parameters outside the limits), UNSUPPORTED
  * (nnz >= 2^31 or n_rows + nnz / H + 1 >= 2^31), OUT_OF_MEMORY, HIP.
- * On any error *out is set to NULL. */
+ * On any error *out is set to NULL and the device memory the call allocated
+ * is released (it may stay in the library's plan-memory cache, which
+ * agcn_release_cached_memory empties).
+ *
+ * Fault injection for tests (environment variables, read on every call;
+ * leave them unset in normal use): AGCN_TEST_FAIL_ALLOC=k makes the k-th
+ * memory allocation attempt of each agcn_plan_create call on the calling
+ * thread fail with OUT_OF_MEMORY; AGCN_TEST_FAIL_ORDER_SORT=1 raises the
+ * internal-error flag before the hub-chunk launch-order sort, which then
+ * keeps the plain heaviest-first order (the plan stays valid). */
 int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t nnz,
                      const int32_t* d_rowptr, const int32_t* d_colidx, const float* d_vals,
                      const agcn_plan_params* params, void* stream);

@@ -2,6 +2,7 @@
 // Every check that can be made on the host runs before the first HIP call.
 #include <algorithm>
 #include <climits>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -33,6 +34,24 @@ bool span_bytes(int64_t rows, int64_t ld, int64_t F, size_t* out) {
   return true;
 }
 }  // namespace
+
+namespace {
+thread_local int g_alloc_attempts = 0;
+
+int env_int(const char* name) {
+  const char* v = std::getenv(name);
+  return v ? std::atoi(v) : 0;
+}
+}  // namespace
+
+void test_alloc_reset() { g_alloc_attempts = 0; }
+
+bool test_alloc_fails() {
+  const int k = env_int("AGCN_TEST_FAIL_ALLOC");
+  return ++g_alloc_attempts == k && k > 0;
+}
+
+bool test_order_sort_fails() { return env_int("AGCN_TEST_FAIL_ORDER_SORT") != 0; }
 
 void set_error(const std::string& msg) { g_last_error = msg; }
 
@@ -110,8 +129,9 @@ int device_alloc(int device, size_t bytes, hipStream_t stream, void** out, size_
     return AGCN_OK;
   }
   void* p = nullptr;
-  hipError_t e = hipMalloc(&p, bytes);
-  if (e == hipErrorOutOfMemory) {
+  const bool injected = test_alloc_fails();  // the attempt fails, retry included
+  hipError_t e = injected ? hipErrorOutOfMemory : hipMalloc(&p, bytes);
+  if (e == hipErrorOutOfMemory && !injected) {
     // Give the cached block back to the device and try once more.
     (void)hipGetLastError();
     CachedBlock old;
@@ -312,6 +332,7 @@ int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t n
   hipError_t he = hipGetDevice(&dev);
   if (he != hipSuccess) return agcn::hip_fail(he, "hipGetDevice");
 
+  agcn::test_alloc_reset();
   agcn_plan* p = new (std::nothrow) agcn_plan();
   if (p == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "host allocation failed");
   p->device = dev;

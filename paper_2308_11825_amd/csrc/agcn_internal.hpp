@@ -74,6 +74,19 @@ struct agcn_plan {
 
 namespace agcn {
 
+// Fault injection for the error-path tests, read from the environment on
+// every call (unset in normal use):
+//   AGCN_TEST_FAIL_ALLOC=k       the k-th memory allocation attempt (device
+//                                block, pinned read-back buffer) of each
+//                                agcn_plan_create call on the calling thread
+//                                fails as if the memory were exhausted;
+//   AGCN_TEST_FAIL_ORDER_SORT=1  the launch-order sort of hub chunks starts
+//                                with the internal-error flag raised, as when
+//                                one of its scans gives up its bounded wait.
+void test_alloc_reset();    // start of agcn_plan_create
+bool test_alloc_fails();    // counts one allocation attempt; true: fail it
+bool test_order_sort_fails();
+
 // Thread-local error text (set by the failing call).
 void set_error(const std::string& msg);
 int fail(int status, const std::string& msg);

@@ -177,6 +177,11 @@ __global__ void k_set(int32_t* p, int32_t v) {
   if (threadIdx.x == 0 && blockIdx.x == 0) p[0] = v;
 }
 
+// Raises error flags from the host's side (fault injection for tests).
+__global__ void k_raise(uint32_t* err, uint32_t bits) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) atomicOr(err, bits);
+}
+
 // Step (1) of the degree sort, plus the row-pointer checks: the maximum
 // degree and the OR of the error flags of each workgroup.
 __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
@@ -837,15 +842,21 @@ __global__ __launch_bounds__(kThreads) void k_hub_keys(const int4* __restrict__ 
 
 // order[i] = entry launched by workgroup i: the n_chunks hub entries first
 // (sorted ids, or in reverse entry order without them), then the remaining
-// entries from the heaviest down.
+// entries from the heaviest down. This sort runs after the host has read the
+// plan's summary, so nothing reads the error word again: if a scan of the sort
+// gave up its bounded wait (or any earlier step failed), the sorted ids were
+// never written, and the plain order -- a permutation of every entry whatever
+// happened -- is written instead.
 __global__ __launch_bounds__(kThreads) void k_order_fill(int32_t* __restrict__ order,
                                                          int32_t n_entries, int32_t hub_first,
                                                          int32_t n_chunks,
-                                                         const int32_t* __restrict__ sorted_ids) {
+                                                         const int32_t* __restrict__ sorted_ids,
+                                                         const uint32_t* err) {
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (i >= n_entries) return;
+  const bool use_sorted = sorted_ids != nullptr && !failed(err);
   if (i < n_chunks)
-    order[i] = sorted_ids ? hub_first + sorted_ids[i] : n_entries - 1 - (int32_t)i;
+    order[i] = use_sorted ? hub_first + sorted_ids[i] : n_entries - 1 - (int32_t)i;
   else
     order[i] = hub_first - 1 - (int32_t)(i - n_chunks);
 }
@@ -1008,6 +1019,7 @@ PlanSummary* pinned_summary(PlanSummary** dev) {
   thread_local PlanSummary* dbuf = nullptr;
   if (buf == nullptr) {
     void* q = nullptr;
+    if (test_alloc_fails()) return nullptr;
     // Portable: one buffer serves plans built on any device from this thread.
     if (hipHostMalloc(&q, sizeof(PlanSummary),
                       hipHostMallocMapped | hipHostMallocCoherent | hipHostMallocPortable) !=
@@ -1309,6 +1321,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   if (n_chunks > 0 && hub_order_setting() &&
       ((int64_t)n_chunks >= (int64_t)kOrderMinChunks * p->n_hub_rows ||
        n_chunks >= kOrderMinTotalChunks)) {
+    if (test_order_sort_fails()) k_raise<<<1, 64, 0, st>>>(err, kErrInternal);
     const int64_t ct = ceil_div64(n_chunks, kRadixTile);
     int32_t* hk_in = hsort;
     const RadixBufs hb{hk_in, {hsort + chunk_ub, hsort + 2 * chunk_ub},
@@ -1326,7 +1339,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     }
     sorted_ids = hb.ids[0];
     k_order_fill<<<grid_for(p->n_entries, kThreads), kThreads, 0, st>>>(
-        p->order, p->n_entries, p->hub_first_entry, n_chunks, sorted_ids);
+        p->order, p->n_entries, p->hub_first_entry, n_chunks, sorted_ids, err);
   }
   return check_launch("launch order");
 }
