@@ -5,7 +5,7 @@
 // Nothing here is shared with the device library. The readings R1-R9 of the
 // paper that this file follows are listed in agcn_oracle.h.
 //
-// Style: single-threaded, straight loops in the paper's order, float64
+// Style: single-threaded, straight loops following the paper's definitions, float64
 // accumulation. Built with -O2 -ffp-contract=off.
 #include "agcn_oracle.h"
 
@@ -26,27 +26,20 @@ bool rowptr_ok(int32_t n_rows, const int32_t* rowptr) {
   return true;
 }
 
-// Alg. 1 written out: walk the factors of max_block_warps in ascending order;
-// a degree takes the first factor whose warps (each holding max_warp_nzs
-// nnz) can cover it. Degrees run 1..deg_bound inclusive (R4).
+// Alg. 1 by its definition (R4): for a degree d in 1..W*Z, f(d) is the
+// smallest divisor f of W for which f warps of Z nnz hold d nnz (f * Z >= d).
+// A block then holds W / f rows of that degree, and each of a row's f warps
+// ceil(d / f) of its nnz. f = W always qualifies, since W * Z = deg_bound >= d.
 void patterns(int32_t W, int32_t Z, std::vector<int32_t>& block_rows,
               std::vector<int32_t>& warp_nzs) {
   const int32_t deg_bound = W * Z;
-  std::vector<int32_t> factors;
-  for (int32_t f = 1; f <= W; ++f)
-    if (W % f == 0) factors.push_back(f);
   block_rows.assign(deg_bound + 1, 0);
   warp_nzs.assign(deg_bound + 1, 0);
-  size_t i = 0;
-  int32_t deg = 1;
-  while (deg <= deg_bound) {
-    if ((int64_t)factors[i] * Z >= deg) {
-      block_rows[deg] = W / factors[i];
-      warp_nzs[deg] = (int32_t)ceil_div(deg, factors[i]);
-      ++deg;
-    } else {
-      ++i;  // the last factor is W itself and W * Z = deg_bound, so i stays in range
-    }
+  for (int32_t d = 1; d <= deg_bound; ++d) {
+    int32_t f = 1;
+    while (W % f != 0 || (int64_t)f * Z < d) ++f;
+    block_rows[d] = W / f;
+    warp_nzs[d] = (int32_t)ceil_div(d, f);
   }
 }
 
@@ -106,7 +99,14 @@ int oracle_patterns(int32_t max_block_warps, int32_t max_warp_nzs, int32_t* bloc
   return 0;
 }
 
-// Alg. 2: one pass over the degree classes of the sorted rows, ascending.
+// Alg. 2 by its definition. The degree sort leaves the rows of each degree as
+// one run of consecutive sorted rows; runs are taken in ascending degree and
+// each is cut on its own (R3, R5-R8):
+//   d <= deg_bound: ceil(c / b) entries of b = block_rows(d) consecutive rows
+//                   (b = W for d = 0), the last one holding what remains;
+//   d >  deg_bound: every row of the run, in sorted order, becomes
+//                   ceil(d / H) entries of H consecutive nnz, the last one
+//                   holding what remains.
 int64_t oracle_partition(int32_t n_rows, const int32_t* rowptr_s, int32_t max_block_warps,
                          int32_t max_warp_nzs, int32_t hub_chunk_nnz, int32_t* meta,
                          int64_t cap) {
@@ -130,43 +130,27 @@ int64_t oracle_partition(int32_t n_rows, const int32_t* rowptr_s, int32_t max_bl
     ++count;
     return true;
   };
+  auto degree = [&](int64_t r) { return (int64_t)rowptr_s[r + 1] - rowptr_s[r]; };
 
-  int64_t r = 0;  // cursor over sorted rows
-  while (r < n_rows) {
-    const int64_t deg = rowptr_s[r + 1] - rowptr_s[r];
-    int64_t rows_of_deg = 0;  // size of this degree class (sorted => contiguous)
-    while (r + rows_of_deg < n_rows &&
-           rowptr_s[r + rows_of_deg + 1] - rowptr_s[r + rows_of_deg] == deg)
-      ++rows_of_deg;
-    if (deg <= deg_bound) {
-      // Degree 0 (R7): rows of W, nothing to gather.
-      const int64_t br = deg == 0 ? W : block_rows[deg];
-      const int64_t wn = deg == 0 ? 0 : warp_nzs[deg];
-      int64_t rows_remaining = rows_of_deg;
-      while (rows_remaining >= br) {
-        if (!emit(deg, rowptr_s[r], r, (wn << 16) | br)) return -2;
-        r += br;
-        rows_remaining -= br;
-      }
-      if (rows_remaining > 0) {  // R6: no empty residual entry
-        if (!emit(deg, rowptr_s[r], r, (wn << 16) | rows_remaining)) return -2;
-        r += rows_remaining;
+  for (int64_t r0 = 0; r0 < n_rows;) {
+    const int64_t d = degree(r0);
+    int64_t r1 = r0 + 1;  // the run of rows of degree d is [r0, r1)
+    while (r1 < n_rows && degree(r1) == d) ++r1;
+    const int64_t c = r1 - r0;
+    if (d <= deg_bound) {
+      const int64_t b = d == 0 ? W : block_rows[d];
+      const int64_t wn = d == 0 ? 0 : warp_nzs[d];
+      for (int64_t k = 0; k < ceil_div(c, b); ++k) {
+        const int64_t row = r0 + k * b;
+        const int64_t rows = std::min(b, c - k * b);
+        if (!emit(d, rowptr_s[row], row, (wn << 16) | rows)) return -2;
       }
     } else {
-      // R8: every row of this degree is cut into chunks of H nnz.
-      for (int64_t k = 0; k < rows_of_deg; ++k, ++r) {
-        int64_t loc = rowptr_s[r];
-        int64_t deg_remaining = deg;
-        while (deg_remaining >= H) {
-          if (!emit(deg, loc, r, H)) return -2;
-          loc += H;
-          deg_remaining -= H;
-        }
-        if (deg_remaining > 0) {
-          if (!emit(deg, loc, r, deg_remaining)) return -2;
-        }
-      }
+      for (int64_t row = r0; row < r1; ++row)
+        for (int64_t k = 0; k < ceil_div(d, H); ++k)
+          if (!emit(d, rowptr_s[row] + k * H, row, std::min(H, d - k * H))) return -2;
     }
+    r0 = r1;
   }
   return count;
 }

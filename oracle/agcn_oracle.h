@@ -56,14 +56,17 @@ int oracle_relayout(int32_t n_rows, const int32_t* rowptr, const int32_t* colidx
                     const float* vals, const int32_t* perm, int32_t* rowptr_s,
                     int32_t* colidx_s, float* vals_s);
 
-/* Alg. 1 (partition patterns) with R4: for d = 1..W*Z writes
- * block_rows[d] = W / f and warp_nzs[d] = ceil(d / f), f being the first
- * factor of W (ascending) with f * Z >= d. Index 0 is set to 0. Both arrays
+/* Alg. 1 (partition patterns) with R4, by its definition: for d = 1..W*Z
+ * writes block_rows[d] = W / f and warp_nzs[d] = ceil(d / f), f being the
+ * smallest divisor of W with f * Z >= d. Index 0 is set to 0. Both arrays
  * hold W*Z + 1 entries. */
 int oracle_patterns(int32_t max_block_warps, int32_t max_warp_nzs,
                     int32_t* block_rows, int32_t* warp_nzs);
 
-/* Alg. 2 (block-level partitioning) with R3-R9 over the sorted row pointer.
+/* Alg. 2 (block-level partitioning) with R3-R9 over the sorted row pointer,
+ * by its definition: each run of equal-degree sorted rows, in ascending
+ * degree, gives ceil(count / block_rows) entries (degree <= deg_bound) or,
+ * per row, ceil(degree / hub_chunk_nnz) chunk entries (degree > deg_bound).
  * hub_chunk_nnz <= 0 means deg_bound. meta receives 4 int32 per entry
  * {deg, loc, row, info}; pass meta = NULL to count only. Returns the number
  * of entries, or -1 on a bad argument, or -2 if cap is too small. */
