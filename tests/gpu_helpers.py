@@ -1,6 +1,9 @@
 """Shared helpers of the GPU tests: device copies, plan creation, and the
 oracle comparisons (plan bit-exact, Y within 1e-5 * S + 1e-7 per element,
 S = sum_e |a_e| |x|)."""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 
@@ -107,3 +110,34 @@ def _sample_rows(g, plan, k=3000, seed=0):
         rows.append(rng.choice(hub, size=min(300, hub.size), replace=False))
     rows.append(np.argsort(d)[-20:])
     return np.unique(np.concatenate(rows)).astype(np.int32)
+
+
+def _host_workers():
+    """Worker threads for the oracle checks: the host's CPU share, at most 16."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def assert_all_rows_close(g, X, Yg, what="", block=32768):
+    """Every element of Yg (n_rows x F, original row order) against the
+    oracle's definition of A X, within RTOL * S + ATOL. The oracle itself is
+    the plain single-threaded function; disjoint blocks of rows are handed to
+    it from several host threads (the C call releases the GIL), so that the
+    full-size workloads are checked in seconds."""
+    n = g.n_rows
+    assert Yg.shape == (n, X.shape[1]), (what, Yg.shape)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+
+    def check(s):
+        rows = np.arange(s, min(n, s + block), dtype=np.int32)
+        Yr, Sr = oracle.spmm_rows(g.rowptr, g.colidx, g.vals, X, rows, n_cols=g.n_cols)
+        assert_close(Yg[s:s + rows.size], Yr, Sr, f"{what} rows {s}..{s + rows.size - 1}")
+        return rows.size
+
+    with ThreadPoolExecutor(_host_workers()) as ex:
+        done = sum(f.result() for f in [ex.submit(check, s) for s in range(0, n, block)])
+    assert done == n
+    return done

@@ -15,7 +15,7 @@ pytestmark = pytest.mark.gpu
 
 import paper_2308_11825_amd as agcn  # noqa: E402
 
-from gpu_helpers import (DEV, _dev, _mixed, _plan, _sample_rows, _spmm_check,  # noqa: E402
+from gpu_helpers import (DEV, _dev, _mixed, _plan, _sample_rows, _spmm_check, assert_all_rows_close,  # noqa: E402
                          _workload, assert_close, assert_plan_matches_oracle)
 
 
@@ -410,7 +410,8 @@ def test_spmm_argument_errors(mixed_plan):
 
 # ---------------------------------------------------------------------------
 # Full-size workloads (default parameters, the launch configuration the
-# benchmark times): plan bit-exact, Y on sampled rows.
+# benchmark times): plan bit-exact, and every element of Y against the oracle
+# at every feature width of the workload.
 # ---------------------------------------------------------------------------
 
 @pytest.mark.slow
@@ -419,14 +420,11 @@ def test_workload_parity(name):
     g = _workload(name)
     plan = _plan(g)
     assert_plan_matches_oracle(plan, g)
-    rows = _sample_rows(g, plan)
     for F in graphgen.CONFIGS[name]["F"]:
         X = graphgen.workload_features(name, g, F)
         Yg = plan.spmm(_dev(X)).cpu().numpy()
-        Yr, Sr = oracle.spmm_rows(g.rowptr, g.colidx, g.vals, X, rows)
-        assert_close(Yg[rows], Yr, Sr, f"{name} F={F}")
-        assert np.all(np.isfinite(Yg))
-        print(f"[parity] {name} F={F} ok ({rows.size} rows checked)", flush=True)
+        n = assert_all_rows_close(g, X, Yg, f"{name} F={F}")
+        print(f"[parity] {name} F={F} ok (all {n} rows x {F} columns checked)", flush=True)
     plan.destroy()
 
 
@@ -504,8 +502,8 @@ def test_long_hub_rows_column_ordered_launch():
 def test_nnz_just_below_the_int32_limit(flags):
     """The largest matrix the int32 format holds: nnz = 2^31 - 3 over about
     1.9 M rows of mixed degree (empty, small, the deg_bound edges, hubs of
-    several chunks). Entry counts checked against the closed forms, Y on
-    sampled rows (first, last, every degree) against the oracle."""
+    several chunks). Entry counts checked against the closed forms, every
+    element of Y against the oracle."""
     pattern = np.array([0, 1, 7, 64, 511, 512, 513, 2000, 4000], np.int64)
     n_cols = 1 << 20
     target = (1 << 31) - 3
@@ -535,11 +533,8 @@ def test_nnz_just_below_the_int32_limit(flags):
     F = 8
     X = rng.standard_normal((n_cols, F)).astype(np.float32)
     Yg = plan.spmm(_dev(X)).cpu().numpy()
-    rows = np.unique(np.concatenate([np.arange(len(pattern)), np.arange(n - 20, n),
-                                     rng.choice(n, 400, replace=False)])).astype(np.int32)
     g = graphgen.Graph("max", n, n_cols, rowptr, colidx, vals)
-    Yr, Sr = oracle.spmm_rows(g.rowptr, g.colidx, g.vals, X, rows, n_cols=n_cols)
-    assert_close(Yg[rows], Yr, Sr, f"nnz=2^31-3 flags={flags}")
-    print(f"[max] ok ({rows.size} rows checked)", flush=True)
+    checked = assert_all_rows_close(g, X, Yg, f"nnz=2^31-3 flags={flags}", block=65536)
+    print(f"[max] ok (all {checked} rows checked)", flush=True)
     plan.destroy()
     agcn.agcn_release_cached_memory()
