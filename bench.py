@@ -42,6 +42,12 @@ import graphgen  # noqa: E402
 
 METRIC = "SpMM GFLOP/s (2·nnz·F) and % of HBM roofline, F=16..256"
 HBM_PEAK_GBPS = 8000.0
+# Rates of random 128-byte gathers on this GPU (profiles/gather_ceiling_probe.md):
+# served by L2 (working set within one XCD's 4 MB) 26-28 TB/s, served past L2
+# (Infinity Cache or HBM) 6.8-7.3 TB/s; 64-byte gathers run at the same
+# request rates. In requests per second for the whole GPU:
+L2_GATHER_REQ_PER_S = 220e9
+PAST_L2_GATHER_REQ_PER_S = 55e9
 KERNEL_SRC = os.path.join(ROOT, "paper_2308_11825_amd", "csrc", "agcn_spmm.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_traffic.json")
 
@@ -70,6 +76,13 @@ def kernel_bytes(st, F, n_ref, variant="block"):
           + 4 * F * st.n_hub_chunks)
     k8 = 4 * F * st.n_hub_chunks + 4 * F * st.n_hub_rows + 8 * st.n_hub_rows
     return k7, k8
+
+
+def gather_requests(st, F):
+    """Gather requests one aggregation launch issues for X: every nonzero
+    loads its X row's piece of every column slice of 32 floats (one 128-byte
+    line; a single 64-byte piece when F = 16)."""
+    return st.nnz * ((F + 31) // 32)
 
 
 def spmm_kernel_name(F, variant="block"):
@@ -140,27 +153,38 @@ def cache_protocol(agcn, plan, Fs, Xs, Ys, ws, stream, reps, dev):
     """Execute timings per F in the two cache states: cold (a 1 GiB buffer is
     written before every rep, outside the events, so X, the CSR and Y start
     outside L2 and the Infinity Cache) and warm (reps back to back).
-    Median, p10 and p90 of the per-rep times, in ms."""
+    Median, p10 and p90 of the per-rep times, in ms: the whole execute, and
+    the aggregation kernel alone (the events the library attaches to it)."""
     import torch
     flush = torch.empty(256 * 2**20, dtype=torch.float32, device=dev)
     sh = stream.cuda_stream
-    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)  # creates the underlying hipEvent_t
+        return e
+
+    def stats(t):
+        return {"median_ms": round(float(np.median(t)), 5),
+                "p10_ms": round(float(np.percentile(t, 10)), 5),
+                "p90_ms": round(float(np.percentile(t, 90)), 5)}
+
     out = {}
     for F in Fs:
         res = {}
         for mode in ("cold", "warm"):
-            marks = [(ev(), ev()) for _ in range(reps)]
-            for a, b in marks:
+            marks = [(ev(), ev(), ev(), ev()) for _ in range(reps)]
+            torch.cuda.synchronize()
+            for a, b, m, c in marks:
                 if mode == "cold":
                     flush.fill_(float(len(res)))
                 a.record(stream)
-                agcn.agcn_spmm(plan, F, Xs[F].data_ptr(), F, Ys[F].data_ptr(), F, ws.data_ptr(), sh)
-                b.record(stream)
+                agcn.agcn_spmm_timed(plan, F, Xs[F].data_ptr(), F, Ys[F].data_ptr(), F,
+                                     ws.data_ptr(), sh, b.cuda_event, m.cuda_event, None)
+                c.record(stream)
             torch.cuda.synchronize()
-            t = np.array([a.elapsed_time(b) for a, b in marks])
-            res[mode] = {"median_ms": round(float(np.median(t)), 5),
-                         "p10_ms": round(float(np.percentile(t, 10)), 5),
-                         "p90_ms": round(float(np.percentile(t, 90)), 5)}
+            res[mode] = stats(np.array([a.elapsed_time(c) for a, _, _, c in marks]))
+            res[mode]["spmm"] = stats(np.array([b.elapsed_time(m) for _, b, m, _ in marks]))
         out[F] = res
     del flush
     return out
@@ -485,24 +509,35 @@ def main():
     mean_bytes = float(np.mean([per_f[F]["spmm_bytes"] for F in dom_F]))
     mean_ms = float(np.mean([per_f[F]["spmm_ms"] for F in dom_F]))
     ach = mean_bytes / (mean_ms * 1e-3) / 1e9
+    # traffic: calibrated FETCH_SIZE + WRITE_SIZE per launch, i.e. the bytes
+    # moved between L2 and the memory side; gfx950 has no counter that tells
+    # Infinity Cache hits from HBM accesses, so part of it may never reach HBM.
     traffic = None
     try:
         with open(TRAFFIC_FILE) as f:
             tr = json.load(f)
         if (tr.get("source_hash") == source_hash() and tr.get("workload") == name
                 and tr.get("F") == dom_F and tr.get("kernel") == dom):
-            traffic = tr.get("hbm_bytes_per_launch")
+            traffic = tr.get("past_l2_bytes_per_launch")
     except (OSError, ValueError):
         pass
+    # Model ceiling of any kernel that gathers X rows per nonzero: its gather
+    # requests all served by L2 at the measured L2 gather rate.
+    req = float(np.mean([gather_requests(st, F) for F in dom_F]))
+    cap_ms = req / L2_GATHER_REQ_PER_S * 1e3
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "kernel": dom, "launches_per_step": len(dom_F), "F": dom_F,
-                "alg_bytes_per_launch": int(mean_bytes), "avg_launch_ms": round(mean_ms, 5)}
+                "alg_bytes_per_launch": int(mean_bytes), "avg_launch_ms": round(mean_ms, 5),
+                "l2_gather_cap": {"requests_per_launch": int(req), "cap_ms": round(cap_ms, 5),
+                                  "frac_at_cap": round(mean_bytes / (cap_ms * 1e-3) / 1e9
+                                                       / HBM_PEAK_GBPS, 4),
+                                  "achieved_over_cap": round(cap_ms / mean_ms, 4)}}
     if traffic is not None:
-        # the counter-measured bytes past L2 (Infinity Cache hits included) over the same time
+        # counter-measured bytes past L2 (Infinity Cache hits included) over the same time
         tg = traffic / (mean_ms * 1e-3) / 1e9
-        roofline["traffic_GBps"] = round(tg, 1)
-        roofline["traffic_frac"] = round(tg / HBM_PEAK_GBPS, 4)
+        roofline["past_l2_GBps"] = round(tg, 1)
+        roofline["past_l2_frac_of_hbm_peak"] = round(tg / HBM_PEAK_GBPS, 4)
 
     # A measured streaming ceiling beside the 8 TB/s peak: a 1 GiB device copy
     # (read + write), timed after the timed region; with --copy-probe it is
@@ -542,9 +577,14 @@ def main():
         log("cold / warm execute protocol ...")
         plan = agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
                                      d_colidx.data_ptr(), d_vals.data_ptr(), prm, sh)
-        out["execute_cold_warm"] = cache_protocol(agcn, plan, Fs, Xs, Ys, ws, stream,
-                                                  args.cache_reps, dev)
+        cw = cache_protocol(agcn, plan, Fs, Xs, Ys, ws, stream, args.cache_reps, dev)
+        out["execute_cold_warm"] = cw
         agcn.agcn_plan_destroy(plan)
+        # the dominant kernel's roofline fraction from its cold launches (X, the
+        # CSR and Y outside L2 and the Infinity Cache when each launch starts)
+        cold_ms = float(np.mean([cw[F]["cold"]["spmm"]["median_ms"] for F in dom_F]))
+        roofline["frac_cold"] = round(mean_bytes / (cold_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)
+        roofline["avg_launch_ms_cold"] = round(cold_ms, 5)
     if args.rocsparse:
         log("rocSPARSE comparison ...")
         rs = rocsparse_compare(g, Fs, Xs, Ys, d_rowptr, d_colidx, d_vals, stream, reps=10)
