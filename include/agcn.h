@@ -198,6 +198,25 @@ int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, 
 int agcn_spmm_ex(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
                  int64_t ldy, void* d_ws, void* stream, int32_t epilogue);
 
+/* agcn_spmm_ex for callers that cannot allocate memory: code being captured
+ * into a HIP graph, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, kernels and results (bit for bit) as agcn_spmm_ex, without
+ * d_ws: the hub-row partial sums go to a fixed workspace the library keeps in
+ * device memory, AGCN_NOALLOC_MAX_WORKSPACE bytes on every GPU it runs on,
+ * held until the process ends. The call allocates nothing (no device or host
+ * memory, no HIP event): on a stream other than the plan's own on which the
+ * plan has not run agcn_spmm / agcn_spmm_ex before, it marks the plan so that
+ * agcn_plan_destroy waits for the device instead of tracking the stream with
+ * an event. All calls on one GPU share the workspace, and each call writes
+ * every part of it that it reads, so nothing needs clearing between calls;
+ * calls that may overlap in time on one GPU (different streams, or graph
+ * replays running concurrently) race on it and must be ordered by the caller.
+ * Errors: those of agcn_spmm_ex, plus UNSUPPORTED when
+ * agcn_spmm_workspace_size(plan, F) exceeds AGCN_NOALLOC_MAX_WORKSPACE. */
+#define AGCN_NOALLOC_MAX_WORKSPACE ((size_t)64 << 20)
+int agcn_spmm_noalloc(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+                      int64_t ldy, void* stream, int32_t epilogue);
+
 /* H = X W, the linear transformation of a GCNConv layer (Sec. II-A), on the
  * fp32 matrix cores. Asynchronous on `stream`; no plan needed.
  *

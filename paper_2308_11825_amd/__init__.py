@@ -19,7 +19,8 @@ __all__ = [
     "agcn_spmm_workspace_size", "agcn_spmm", "agcn_spmm_timed", "agcn_plan_info",
     "agcn_plan_export", "agcn_plan_destroy", "agcn_status_string", "agcn_last_error",
     "agcn_release_cached_memory", "agcn_spmm_ex", "agcn_linear", "agcn_gcn_workspace_size",
-    "agcn_gcn_layer", "Plan", "linear", "PlanParams", "PlanStats", "EXPORTED_SYMBOLS",
+    "agcn_gcn_layer", "agcn_spmm_noalloc", "AGCN_NOALLOC_MAX_WORKSPACE", "Plan", "linear",
+    "PlanParams", "PlanStats", "EXPORTED_SYMBOLS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -29,7 +30,7 @@ EXPORTED_SYMBOLS = [
     "agcn_default_params", "agcn_plan_create", "agcn_spmm_workspace_size", "agcn_spmm",
     "agcn_spmm_timed", "agcn_plan_info", "agcn_plan_export", "agcn_plan_destroy",
     "agcn_status_string", "agcn_last_error", "agcn_release_cached_memory", "agcn_spmm_ex",
-    "agcn_linear", "agcn_gcn_workspace_size", "agcn_gcn_layer",
+    "agcn_linear", "agcn_gcn_workspace_size", "agcn_gcn_layer", "agcn_spmm_noalloc",
 ]
 
 AGCN_OK = 0
@@ -41,6 +42,8 @@ AGCN_ERR_HIP = 5
 
 AGCN_PLAN_WARP_LEVEL = 0x1
 AGCN_PLAN_COLUMN_LOOP = 0x2
+
+AGCN_NOALLOC_MAX_WORKSPACE = 64 << 20
 
 AGCN_EPILOGUE_NONE = 0
 AGCN_EPILOGUE_RELU = 1
@@ -127,6 +130,9 @@ def load_library(path: str | None = None):
     lib.agcn_spmm_ex.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, ctypes.c_int64,
                                  _vp, _vp, ctypes.c_int32]
     lib.agcn_spmm_ex.restype = ctypes.c_int
+    lib.agcn_spmm_noalloc.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp,
+                                      ctypes.c_int64, _vp, ctypes.c_int32]
+    lib.agcn_spmm_noalloc.restype = ctypes.c_int
     lib.agcn_linear.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _vp,
                                 ctypes.c_int64, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp]
     lib.agcn_linear.restype = ctypes.c_int
@@ -191,6 +197,10 @@ def agcn_spmm_timed(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, ev_begin, ev_mid,
 
 def agcn_spmm_ex(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, epilogue):
     _check(load_library().agcn_spmm_ex(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, epilogue))
+
+
+def agcn_spmm_noalloc(plan, F, d_X, ldx, d_Y, ldy, stream, epilogue=AGCN_EPILOGUE_NONE):
+    _check(load_library().agcn_spmm_noalloc(plan, F, d_X, ldx, d_Y, ldy, stream, epilogue))
 
 
 def agcn_linear(n, fin, fout, d_X, ldx, d_W, ldw, d_H, ldh, stream=0):

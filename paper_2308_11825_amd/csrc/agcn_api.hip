@@ -180,18 +180,28 @@ void device_release(int device, void* ptr, size_t bytes, std::vector<StreamEvent
 // way to the first execute, which usually runs on the plan's own stream.
 int plan_ready_event(agcn_plan* p, hipEvent_t* out) {
   std::lock_guard<std::mutex> lk(p->use_mu);
-  if (p->ready == nullptr) {
-    hipEvent_t ev = nullptr;
-    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-    if (e != hipSuccess) return hip_fail(e, "hipEventCreate(plan ready)");
-    if ((e = hipEventRecord(ev, p->stream)) != hipSuccess) {
-      (void)hipEventDestroy(ev);
-      return hip_fail(e, "hipEventRecord(plan ready)");
-    }
-    p->ready = ev;
+  if (p->ready == nullptr) return fail(AGCN_ERR_HIP, "the plan has no readiness event");
+  if (!p->ready_recorded) {
+    const hipError_t e = hipEventRecord(p->ready, p->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord(plan ready)");
+    p->ready_recorded = true;
   }
   *out = p->ready;
   return AGCN_OK;
+}
+
+void note_use_noalloc(agcn_plan* p, hipStream_t stream) {
+  std::lock_guard<std::mutex> lk(p->use_mu);
+  for (auto& u : p->uses) {
+    if (u.first == stream) {
+      if (hipEventRecord(u.second, stream) != hipSuccess) {
+        (void)hipGetLastError();
+        p->sync_on_release = true;
+      }
+      return;
+    }
+  }
+  p->sync_on_release = true;
 }
 
 void note_use(agcn_plan* p, hipStream_t stream) {
@@ -247,7 +257,10 @@ const char* agcn_last_error(void) { return agcn::g_last_error.c_str(); }
 static void plan_free(agcn_plan* p) {
   if (p == nullptr) return;
   std::vector<agcn::StreamEvent> pending;
-  if (p->ready != nullptr) pending.push_back({p->ready, p->stream});
+  if (p->ready != nullptr) {
+    if (p->ready_recorded) pending.push_back({p->ready, p->stream});
+    else (void)hipEventDestroy(p->ready);
+  }
   for (auto& u : p->uses) pending.push_back({u.second, u.first});
   // Calls on the plan's own stream record no event of their own: one event
   // recorded now on that stream follows all of them (and the plan's kernels).
@@ -346,7 +359,15 @@ int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t n
   p->flags = prm.flags;
   int rc;
   try {
-    rc = agcn::build_plan(p, d_rowptr, d_colidx, d_vals, static_cast<hipStream_t>(stream));
+    // The readiness event is created now and recorded only when first needed
+    // (an execute on another stream, an export), so no execute allocates it.
+    he = hipEventCreateWithFlags(&p->ready, hipEventDisableTiming);
+    if (he != hipSuccess) {
+      p->ready = nullptr;
+      rc = agcn::hip_fail(he, "hipEventCreate(plan ready)");
+    } else {
+      rc = agcn::build_plan(p, d_rowptr, d_colidx, d_vals, static_cast<hipStream_t>(stream));
+    }
   } catch (const std::bad_alloc&) {
     rc = fail(AGCN_ERR_OUT_OF_MEMORY, "host allocation failed");
   } catch (...) {
@@ -386,9 +407,11 @@ int check_device(const agcn_plan* plan) {
   return AGCN_OK;
 }
 
+// noalloc: the workspace is the library's fixed device array (d_ws unused),
+// and the call creates no event either.
 int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
                  int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
-                 void* ev_end, int32_t epilogue) {
+                 void* ev_end, int32_t epilogue, bool noalloc = false) {
   if (plan == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "plan is NULL");
   if (epilogue != AGCN_EPILOGUE_NONE && epilogue != AGCN_EPILOGUE_RELU)
     return fail(AGCN_ERR_INVALID_ARGUMENT, "epilogue must be AGCN_EPILOGUE_NONE or AGCN_EPILOGUE_RELU");
@@ -398,6 +421,23 @@ int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
   if (plan->nnz > 0 && d_X == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "X is NULL");
   size_t ws_need = 0;
   agcn_spmm_workspace_size(plan, F, &ws_need);
+  if (noalloc) {
+    if (ws_need > agcn::kNoallocScratchBytes)
+      return fail(AGCN_ERR_UNSUPPORTED,
+                  "agcn_spmm_noalloc: this plan needs " + std::to_string(ws_need) +
+                      " bytes of workspace at F = " + std::to_string(F) + ", above the " +
+                      std::to_string(agcn::kNoallocScratchBytes) +
+                      "-byte fixed workspace (use agcn_spmm with a workspace)");
+    d_ws = nullptr;
+    if (ws_need > 0) {
+      int dev = -1;
+      hipError_t he = hipGetDevice(&dev);
+      if (he != hipSuccess) return agcn::hip_fail(he, "hipGetDevice");
+      float* scratch = nullptr;
+      if (int rc = agcn::noalloc_scratch(dev, &scratch)) return rc;
+      d_ws = scratch;
+    }
+  }
   if (ws_need > 0 && d_ws == nullptr)
     return fail(AGCN_ERR_INVALID_ARGUMENT, "this plan has hub rows: a workspace is required");
   size_t xb = 0, yb = 0;
@@ -424,8 +464,10 @@ int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
                                 epilogue);
   // Last use on a stream other than the plan's own (also after a failed
   // launch); uses on the plan's stream are covered at release.
-  if (static_cast<hipStream_t>(stream) != plan->stream)
-    agcn::note_use(plan, static_cast<hipStream_t>(stream));
+  if (static_cast<hipStream_t>(stream) != plan->stream) {
+    if (noalloc) agcn::note_use_noalloc(plan, static_cast<hipStream_t>(stream));
+    else agcn::note_use(plan, static_cast<hipStream_t>(stream));
+  }
   return rc;
 }
 
@@ -476,6 +518,12 @@ int agcn_spmm_ex(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
                  int64_t ldy, void* d_ws, void* stream, int32_t epilogue) {
   return spmm_checked(plan, F, d_X, ldx, d_Y, ldy, d_ws, stream, nullptr, nullptr, nullptr,
                       epilogue);
+}
+
+int agcn_spmm_noalloc(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
+                      int64_t ldy, void* stream, int32_t epilogue) {
+  return spmm_checked(plan, F, d_X, ldx, d_Y, ldy, nullptr, stream, nullptr, nullptr, nullptr,
+                      epilogue, /*noalloc=*/true);
 }
 
 int agcn_linear(int64_t n, int32_t fin, int32_t fout, const float* d_X, int64_t ldx,

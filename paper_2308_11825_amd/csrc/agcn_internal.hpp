@@ -61,7 +61,9 @@ struct agcn_plan {
   int32_t* hub_chunk_off = nullptr; // [hub rows upper bound + 1] first chunk of each hub row
   int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
   int32_t* group_off = nullptr;     // warp-level plans: [n_rows + 1] first group of each row
-  hipEvent_t ready = nullptr;       // the plan's kernels done (plan_ready_event; use_mu)
+  hipEvent_t ready = nullptr;       // the plan's kernels done (created with the plan,
+                                    // recorded on first need: plan_ready_event; use_mu)
+  bool ready_recorded = false;
   hipStream_t stream = nullptr;     // the stream the plan was built on (valid until destroy)
   // Last work of the plan on each stream other than its own that ran an
   // execute with it (one event per stream, re-recorded by every call; guarded
@@ -110,6 +112,13 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
 int run_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx, const float* W,
                int64_t ldw, float* H, int64_t ldh, hipStream_t stream);
 
+// agcn_spmm_noalloc's workspace: a fixed device array of this many bytes in
+// agcn_spmm.hip; noalloc_scratch returns its address on `device` (the
+// current device), looked up on the first call for that device.
+constexpr size_t kNoallocScratchBytes = AGCN_NOALLOC_MAX_WORKSPACE;
+constexpr int kMaxDevices = 64;
+int noalloc_scratch(int device, float** out);
+
 // Dynamic LDS bytes the SpMM kernel needs for a plan (worst case over F).
 size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz);
 
@@ -133,7 +142,12 @@ void note_use(agcn_plan* p, hipStream_t stream);
 
 // The event after the plan's kernels, recorded on the plan's stream on the
 // first call (so it also covers work queued there since) and reused after.
+// The event object itself is created with the plan, so this allocates nothing.
 int plan_ready_event(agcn_plan* p, hipEvent_t* out);
+
+// Like note_use, but creates no event: a stream that has no event yet marks
+// the plan to wait for the device when it is released.
+void note_use_noalloc(agcn_plan* p, hipStream_t stream);
 
 inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline bool aligned16(const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; }

@@ -45,6 +45,7 @@
 #include <algorithm>
 #include <climits>
 #include <cstdlib>
+#include <mutex>
 
 #include <hip/hip_ext.h>
 
@@ -684,6 +685,35 @@ int run_colloop(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
 }
 
 }  // namespace
+
+// Workspace of agcn_spmm_noalloc: a fixed device array (every GPU the
+// library runs on holds its own copy until the process ends). Host code must
+// not use the name `scratch` as an address -- in host code it is only a
+// stand-in symbol; noalloc_scratch() returns the device's real address, looked
+// up once per device. The kernels write every partial they later read within
+// one call (hub-chunk partials, rows cut by warp-level workgroups), so the
+// array needs no clearing; calls that overlap on one GPU share it and race.
+namespace {
+__device__ __align__(256) float scratch[kNoallocScratchBytes / sizeof(float)];
+
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+int noalloc_scratch(int device, float** out) {
+  if (device < 0 || device >= kMaxDevices)
+    return fail(AGCN_ERR_UNSUPPORTED, "device ordinal beyond the library's table");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[device] == nullptr) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (ptr == nullptr) return fail(AGCN_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[device] = static_cast<float*>(ptr);
+  }
+  *out = g_scratch_ptr[device];
+  return AGCN_OK;
+}
 
 int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,
              float* ws, hipStream_t st, hipEvent_t ev_begin, hipEvent_t ev_mid,
