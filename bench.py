@@ -85,11 +85,22 @@ def gather_requests(st, F):
     return st.nnz * ((F + 31) // 32)
 
 
-def spmm_kernel_name(F, variant="block"):
+def small_path(st):
+    """Plans the library aggregates with k_spmm_rows (one vwarp per row, no
+    staging): no hub rows, every degree <= min(Z, 32), nnz <= 2^18, rows <= 2^16."""
+    return (st.n_hub_rows == 0 and st.max_deg <= min(st.max_wave_nzs, 32) and st.nnz <= 1 << 18
+            and st.n_rows <= 1 << 16)
+
+
+def spmm_kernel_name(F, variant="block", st=None):
     """Instantiation the library picks for an aligned float32 X: 32-column
     slices (AGCN_SLICE_COLS overrides), lanes = slice columns / 4."""
     if variant == "column_loop":
         return "k_spmm_colloop"
+    if variant == "block" and st is not None and small_path(st):
+        sc = min(F, 32) if F % 4 == 0 else min(F, 64)
+        L = sc // 4 if F % 4 == 0 else sc
+        return f"k_spmm_rows<{4 if F % 4 == 0 else 1}, {L if L in (4, 8) else 0}>"
     sc = int(os.environ.get("AGCN_SLICE_COLS", "32"))
     sc = sc if (4 <= sc <= 256 and sc % 4 == 0) else 32
     sc = min(F, sc)
@@ -503,7 +514,7 @@ def main():
     # launch duration over that group's launches.
     groups = {}
     for F in Fs:
-        groups.setdefault(spmm_kernel_name(F, args.variant), []).append(F)
+        groups.setdefault(spmm_kernel_name(F, args.variant, st), []).append(F)
     dom = max(groups, key=lambda k: sum(per_f[F]["spmm_ms"] for F in groups[k]))
     dom_F = groups[dom]
     mean_bytes = float(np.mean([per_f[F]["spmm_bytes"] for F in dom_F]))

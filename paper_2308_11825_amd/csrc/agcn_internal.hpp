@@ -60,6 +60,7 @@ struct agcn_plan {
   int4* meta = nullptr;             // [entries upper bound] {deg, loc, row, info}
   int32_t* hub_chunk_off = nullptr; // [hub rows upper bound + 1] first chunk of each hub row
   int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
+  bool hub_wide = false;            // hub chunks of long rows launched in column order
   int32_t* group_off = nullptr;     // warp-level plans: [n_rows + 1] first group of each row
   hipEvent_t ready = nullptr;       // the plan's kernels done (created with the plan,
                                     // recorded on first need: plan_ready_event; use_mu)

@@ -1318,9 +1318,9 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   // rows average at least kOrderMinChunks chunks, or when there are so many
   // chunks that even a small gain per chunk repays the ~20 us sort (measured:
   // 2.4% off the 2.4 M-row graph's execute; a net loss on a 2.4 M-nnz graph).
-  if (n_chunks > 0 && hub_order_setting() &&
-      ((int64_t)n_chunks >= (int64_t)kOrderMinChunks * p->n_hub_rows ||
-       n_chunks >= kOrderMinTotalChunks)) {
+  const bool long_hubs = (int64_t)n_chunks >= (int64_t)kOrderMinChunks * p->n_hub_rows;
+  if (n_chunks > 0 && hub_order_setting() && (long_hubs || n_chunks >= kOrderMinTotalChunks)) {
+    p->hub_wide = long_hubs;
     if (test_order_sort_fails()) k_raise<<<1, 64, 0, st>>>(err, kErrInternal);
     const int64_t ct = ceil_div64(n_chunks, kRadixTile);
     int32_t* hk_in = hsort;

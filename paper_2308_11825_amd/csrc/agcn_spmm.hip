@@ -68,6 +68,8 @@ struct VecOf<1> {
 };
 
 constexpr int kDefaultSliceCols = 32;  // one 128-byte line per X row per pass
+// Slice width of column-ordered hub chunks of long hub rows (two lines).
+constexpr int kHubSliceCols = 64;
 constexpr int kStageUnroll = 4;
 constexpr int kGatherUnroll = 8;
 
@@ -267,6 +269,58 @@ __global__ __launch_bounds__(1024) void k_hub_reduce(const int32_t* __restrict__
     V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[hub_first_row + h] * ldy + col0);
     __builtin_nontemporal_store(act_v(s_acc[l], act), yr + l);
   }
+}
+
+// Small plans (no hub rows, every degree <= min(Z, kSmallMaxDeg), few rows):
+// the whole launch is a chain of dependent memory round trips on a mostly idle
+// GPU, so this path drops the two that k_spmm adds before its gathers (the
+// launch-order / metadata reads and the LDS staging with its barrier). One
+// vwarp of L lanes (one float4 or float each, laid across the slice as in
+// k_spmm) takes one sorted row, heaviest rows first: it reads the row's
+// bounds, loads all of its (column, value) pairs at once, issues every gather
+// before the first FMA, and adds in nnz order. With every degree <= Z each
+// row is one vwarp of the block-level partition, so Y equals k_spmm's bit for
+// bit.
+constexpr int kSmallMaxDeg = 32;
+constexpr int kSmallThreads = 256;  // measured: 64-thread workgroups (every CU busy) were slower
+
+template <int VW, int LT>
+__global__ __launch_bounds__(kSmallThreads) void k_spmm_rows(
+    int32_t n_rows, const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ colidx_s,
+    const float* __restrict__ vals_s, const int32_t* __restrict__ perm, const float* __restrict__ X,
+    int64_t ldx, float* __restrict__ Y, int64_t ldy, int32_t col_base, int32_t slice_cols,
+    int32_t L_rt, int32_t act) {
+  using V = typename VecOf<VW>::T;
+  const int L = LT > 0 ? LT : L_rt;
+  const int64_t t = (int64_t)blockIdx.x * kSmallThreads + threadIdx.x;
+  const int64_t v = t / L;
+  const int lane = (int)(t - v * L);
+  if (v >= n_rows) return;
+  const int32_t r = n_rows - 1 - (int32_t)v;  // heaviest first
+  const int32_t a = rowptr_s[r];
+  const int32_t d = rowptr_s[r + 1] - a;
+  const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
+  const V* __restrict__ Xv = reinterpret_cast<const V*>(X + col0);
+  const int64_t ldxv = ldx / VW;
+  int32_t c[kSmallMaxDeg];
+  float w[kSmallMaxDeg];
+#pragma unroll
+  for (int k = 0; k < kSmallMaxDeg; ++k) {
+    if (k < d) {
+      c[k] = colidx_s[a + k];
+      w[k] = vals_s[a + k];
+    }
+  }
+  V x[kSmallMaxDeg];
+#pragma unroll
+  for (int k = 0; k < kSmallMaxDeg; ++k)
+    if (k < d) x[k] = Xv[(int64_t)c[k] * ldxv + lane];
+  V acc = V(0.0f);
+#pragma unroll
+  for (int k = 0; k < kSmallMaxDeg; ++k)
+    if (k < d) acc = fma_v(w[k], x[k], acc);
+  V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[r] * ldy + col0);
+  __builtin_nontemporal_store(act_v(acc, act), yr + lane);
 }
 
 // --- ablation baselines (the paper's Table II) ------------------------------
@@ -501,9 +555,15 @@ struct Marks {
   hipEvent_t stop = nullptr;
 };
 
+// Launch positions [e_begin, e_end) of the plan's launch order, every column
+// slice of one width.
+struct EntryRange {
+  int32_t begin, end;
+};
+
 template <int VW, int LT>
 void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols,
-                 Marks& mk, bool last_part) {
+                 Marks& mk, bool last_part, EntryRange er) {
   const agcn_plan* p = a.p;
   const int cap_pad = stage_words(std::max(p->deg_bound, p->H));
   const int want = p->W * L;
@@ -511,10 +571,10 @@ void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice
   const int rounds = (want + T - 1) / T;
   const size_t lds = (size_t)2 * cap_pad * 4 + (size_t)part_floats(VW, p->W, L) * 4;
   const int64_t max_grid = (int64_t)(UINT32_MAX / (uint32_t)T);
-  for (int64_t e0 = 0; e0 < p->n_entries; e0 += max_grid) {
-    const int64_t cnt = std::min<int64_t>(max_grid, p->n_entries - e0);
+  for (int64_t e0 = er.begin; e0 < er.end; e0 += max_grid) {
+    const int64_t cnt = std::min<int64_t>(max_grid, er.end - e0);
     dim3 grid((unsigned)cnt, (unsigned)n_slices);
-    const hipEvent_t stop = (last_part && e0 + cnt >= p->n_entries) ? mk.stop : nullptr;
+    const hipEvent_t stop = (last_part && e0 + cnt >= er.end) ? mk.stop : nullptr;
     if (mk.start || stop) {
       hipExtLaunchKernelGGL(k_spmm<VW, LT>, grid, dim3(T), (uint32_t)lds, a.st, mk.start, stop, 0,
                             p->meta, p->order, (int32_t)e0, p->hub_first_entry, p->deg_bound, p->W,
@@ -532,16 +592,16 @@ void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice
 
 template <int VW>
 void dispatch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols, Marks& mk,
-                   bool last_part) {
+                   bool last_part, EntryRange er) {
   switch (L) {
-    case 1: return launch_spmm<VW, 1>(a, L, n_slices, col_base, slice_cols, mk, last_part);
-    case 2: return launch_spmm<VW, 2>(a, L, n_slices, col_base, slice_cols, mk, last_part);
-    case 4: return launch_spmm<VW, 4>(a, L, n_slices, col_base, slice_cols, mk, last_part);
-    case 8: return launch_spmm<VW, 8>(a, L, n_slices, col_base, slice_cols, mk, last_part);
-    case 16: return launch_spmm<VW, 16>(a, L, n_slices, col_base, slice_cols, mk, last_part);
-    case 32: return launch_spmm<VW, 32>(a, L, n_slices, col_base, slice_cols, mk, last_part);
-    case 64: return launch_spmm<VW, 64>(a, L, n_slices, col_base, slice_cols, mk, last_part);
-    default: return launch_spmm<VW, 0>(a, L, n_slices, col_base, slice_cols, mk, last_part);
+    case 1: return launch_spmm<VW, 1>(a, L, n_slices, col_base, slice_cols, mk, last_part, er);
+    case 2: return launch_spmm<VW, 2>(a, L, n_slices, col_base, slice_cols, mk, last_part, er);
+    case 4: return launch_spmm<VW, 4>(a, L, n_slices, col_base, slice_cols, mk, last_part, er);
+    case 8: return launch_spmm<VW, 8>(a, L, n_slices, col_base, slice_cols, mk, last_part, er);
+    case 16: return launch_spmm<VW, 16>(a, L, n_slices, col_base, slice_cols, mk, last_part, er);
+    case 32: return launch_spmm<VW, 32>(a, L, n_slices, col_base, slice_cols, mk, last_part, er);
+    case 64: return launch_spmm<VW, 64>(a, L, n_slices, col_base, slice_cols, mk, last_part, er);
+    default: return launch_spmm<VW, 0>(a, L, n_slices, col_base, slice_cols, mk, last_part, er);
   }
 }
 
@@ -557,11 +617,12 @@ void launch_hub(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_
                                            a.Y, a.ldy, col_base, slice_cols, L, G, a.act);
 }
 
-// Runs one phase (aggregation or hub reduction) over all column slices: the
-// full slices in one launch, a narrower last slice in a second one.
+// Runs one phase (aggregation or hub reduction) over all column slices of
+// width sc_max (at most F): the full slices in one launch, a narrower last
+// slice in a second one. The aggregation covers the launch positions `er`.
 template <int VW>
-int run_phase(const SpmmArgs& a, bool hub_phase, Marks& mk) {
-  const int sc_max = VW == 4 ? slice_cols_setting() : std::min(64, slice_cols_setting());
+int run_phase(const SpmmArgs& a, bool hub_phase, Marks& mk, int sc_max, EntryRange er,
+              bool last_range) {
   const int sc = std::min(a.F, sc_max);
   const int n_full = a.F / sc;
   const int tail = a.F - n_full * sc;
@@ -571,13 +632,82 @@ int run_phase(const SpmmArgs& a, bool hub_phase, Marks& mk) {
     const int cols = part == 0 ? sc : tail;
     const int L = cols / VW;
     const int col_base = part == 0 ? 0 : n_full * sc;
-    const bool last_part = part == 1 || tail == 0;
+    const bool last_part = last_range && (part == 1 || tail == 0);
     if (hub_phase) launch_hub<VW>(a, L, n_slices, col_base, sc);
-    else dispatch_spmm<VW>(a, L, n_slices, col_base, sc, mk, last_part);
+    else dispatch_spmm<VW>(a, L, n_slices, col_base, sc, mk, last_part, er);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, hub_phase ? "k_hub_reduce launch" : "k_spmm launch");
   }
   return AGCN_OK;
+}
+
+// Plans small enough that k_spmm_rows runs instead of k_spmm.
+constexpr int64_t kSmallMaxNnz = (int64_t)1 << 18;
+constexpr int32_t kSmallMaxRows = 1 << 16;
+
+bool small_path(const agcn_plan* p) {
+  return p->flags == 0 && p->n_hub_rows == 0 && p->max_deg <= std::min(p->Z, kSmallMaxDeg) &&
+         p->nnz <= kSmallMaxNnz && p->n_rows <= kSmallMaxRows;
+}
+
+template <int VW, int LT>
+void launch_rows(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols, Marks& mk,
+                 bool last_part) {
+  const agcn_plan* p = a.p;
+  const int64_t threads = (int64_t)p->n_rows * L;
+  dim3 grid((unsigned)ceil_div64(threads, kSmallThreads), (unsigned)n_slices);
+  const hipEvent_t stop = last_part ? mk.stop : nullptr;
+  hipExtLaunchKernelGGL(k_spmm_rows<VW, LT>, grid, dim3(kSmallThreads), 0, a.st, mk.start, stop, 0,
+                        p->n_rows, p->rowptr_s, p->colidx_s, p->vals_s, p->perm, a.X, a.ldx, a.Y,
+                        a.ldy, col_base, slice_cols, L, a.act);
+  mk.start = nullptr;
+}
+
+template <int VW>
+int run_small(const SpmmArgs& a, Marks& mk) {
+  const int sc = std::min(a.F, VW == 4 ? kDefaultSliceCols : 64);
+  const int n_full = a.F / sc;
+  const int tail = a.F - n_full * sc;
+  for (int part = 0; part < 2; ++part) {
+    const int n_slices = part == 0 ? n_full : (tail > 0 ? 1 : 0);
+    if (n_slices == 0) continue;
+    const int L = (part == 0 ? sc : tail) / VW;
+    const int col_base = part == 0 ? 0 : n_full * sc;
+    const bool last_part = part == 1 || tail == 0;
+    switch (L) {
+      case 4: launch_rows<VW, 4>(a, L, n_slices, col_base, sc, mk, last_part); break;
+      case 8: launch_rows<VW, 8>(a, L, n_slices, col_base, sc, mk, last_part); break;
+      default: launch_rows<VW, 0>(a, L, n_slices, col_base, sc, mk, last_part); break;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "k_spmm_rows launch");
+  }
+  return AGCN_OK;
+}
+
+template <int VW>
+int default_slice_cols() {
+  return VW == 4 ? slice_cols_setting() : std::min(64, slice_cols_setting());
+}
+
+// The aggregation over every entry. When the hub chunks run in column order
+// and hub rows are long (plan flag hub_wide), the chunks in flight gather
+// from a narrow column range, so one XCD's L2 holds that range for several
+// 128-byte slices at once: the hub chunks then take slices of
+// kHubSliceCols columns (staging their CSR pairs once per wide slice instead
+// of once per 128-byte slice) and the other entries the default slices.
+template <int VW>
+int run_aggregation(const SpmmArgs& a, Marks& mk) {
+  const agcn_plan* p = a.p;
+  const int sc = default_slice_cols<VW>();
+  const int32_t n_chunks = p->n_hub_rows > 0 ? p->n_entries - p->hub_first_entry : 0;
+  const int wide = VW == 4 ? kHubSliceCols : std::min(64, kHubSliceCols);
+  if (p->hub_wide && n_chunks > 0 && std::min(a.F, wide) > std::min(a.F, sc)) {
+    int rc = run_phase<VW>(a, false, mk, wide, EntryRange{0, n_chunks}, n_chunks == p->n_entries);
+    if (rc || n_chunks == p->n_entries) return rc;
+    return run_phase<VW>(a, false, mk, sc, EntryRange{n_chunks, p->n_entries}, true);
+  }
+  return run_phase<VW>(a, false, mk, sc, EntryRange{0, p->n_entries}, true);
 }
 
 
@@ -731,10 +861,19 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
   if (p->flags & AGCN_PLAN_WARP_LEVEL)
     return vec ? run_warp_level<4>(a, mk, ev_end) : run_warp_level<1>(a, mk, ev_end);
   if (p->flags & AGCN_PLAN_COLUMN_LOOP) return run_colloop(a, mk, ev_end);
-  int rc = vec ? run_phase<4>(a, false, mk) : run_phase<1>(a, false, mk);
+  if (small_path(p)) {
+    const int rc = vec ? run_small<4>(a, mk) : run_small<1>(a, mk);
+    if (rc) return rc;
+    if (ev_end && (e = hipEventRecord(ev_end, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    return AGCN_OK;
+  }
+  int rc = vec ? run_aggregation<4>(a, mk) : run_aggregation<1>(a, mk);
   if (rc) return rc;
   Marks none{};
-  if (p->n_hub_rows > 0) rc = vec ? run_phase<4>(a, true, none) : run_phase<1>(a, true, none);
+  const EntryRange all{0, p->n_entries};
+  if (p->n_hub_rows > 0)
+    rc = vec ? run_phase<4>(a, true, none, default_slice_cols<4>(), all, true)
+             : run_phase<1>(a, true, none, default_slice_cols<1>(), all, true);
   if (rc) return rc;
   if (ev_end && (e = hipEventRecord(ev_end, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   return AGCN_OK;

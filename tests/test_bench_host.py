@@ -51,3 +51,22 @@ def test_linear_kernel_names_match_the_library_dispatch():
     assert bench.linear_kernel_name(256, 128) == "k_linear<128, true>"
     assert bench.linear_kernel_name(128, 200) == "k_linear<128, true>"
     assert bench.linear_kernel_name(30, 64) == "k_linear<64, false>"
+
+
+def test_small_path_kernel_name():
+    class St:
+        n_hub_rows, max_deg, max_wave_nzs, nnz, n_rows = 0, 21, 32, 36844, 4096
+    assert bench.small_path(St)
+    assert bench.spmm_kernel_name(16, "block", St) == "k_spmm_rows<4, 4>"
+    assert bench.spmm_kernel_name(64, "block", St) == "k_spmm_rows<4, 8>"
+    St.max_deg = 33
+    assert not bench.small_path(St)
+    assert bench.spmm_kernel_name(16, "block", St) == "k_spmm<4, 4>"
+
+
+def test_gather_requests_model():
+    class St:
+        nnz = 1000
+    assert bench.gather_requests(St, 16) == 1000
+    assert bench.gather_requests(St, 32) == 1000
+    assert bench.gather_requests(St, 256) == 8000
