@@ -7,7 +7,9 @@ power-law graph, mean degree 50, F = 16, 32, 64, 128, 256), then the plan is
 released. Inputs (CSR and X for every F) are resident in HBM before timing.
 
 Prints ONE JSON line. value = whole-step throughput in GFLOP/s, FLOPs being
-2 * nnz * F summed over the F sweep (the plan adds time, not FLOPs).
+2 * nnz * F summed over the F sweep (the plan adds time, not FLOPs). Every step
+builds its own plan; --overlap-steps builds the next step's plan on a second
+stream while the current step's executes run.
 Extra keys: per-F execute timings, plan time, the roofline of the dominant
 kernel (measured with HIP events the library attaches to that kernel's
 launch; each timed step marks the executes of one F, rotating through the
@@ -392,6 +394,9 @@ def main():
                     help="reps per F for the cold/warm execute protocol (0 skips it)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-frac", type=float, default=0.4)
+    ap.add_argument("--overlap-steps", action="store_true",
+                    help="build the next step's plan on a second stream during the current "
+                         "step's executes (default: plan, executes, release in order on one stream)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="accepted for older profile commands: the 1 GiB device copy (counter "
                          "calibration, measured copy bandwidth) now always runs after timing")
@@ -454,21 +459,46 @@ def main():
     def timed_fs(k):
         return [Fs[k % len(Fs)]] if args.steps >= len(Fs) else list(Fs)
 
-    def step(evs):
+    # Every step builds its own plan and runs the five executes with it, plan,
+    # executes and release one after the other on one stream. With
+    # --overlap-steps the plan of step k+1 is built on a second stream
+    # (default priority) while the executes of step k run, as a pipeline that
+    # plans the next graph during the current aggregation would; the executes
+    # wait for their plan on the device (the library orders an execute on
+    # another stream after the plan's kernels).
+    serial = not args.overlap_steps
+    plan_stream = stream if serial else torch.cuda.Stream(dev)
+    psh = plan_stream.cuda_stream
+
+    def make_plan():
+        return agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
+                                     d_colidx.data_ptr(), d_vals.data_ptr(), prm, psh)
+
+    def executes(plan, evs):
         # evs: per marked F (k_spmm start, k_spmm end, after the execute); the
         # library records the first two on the launch stream.
-        plan = agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
-                                     d_colidx.data_ptr(), d_vals.data_ptr(), prm, sh)
         for F in Fs:
             b, m, a = evs[F] if evs is not None and F in evs else (None, None, None)
             agcn.agcn_spmm_timed(plan, F, Xs[F].data_ptr(), F, Ys[F].data_ptr(), F, ws.data_ptr(),
                                  sh, b.cuda_event if b else None, m.cuda_event if m else None, None)
             if a is not None:
                 a.record(stream)
-        agcn.agcn_plan_destroy(plan)
 
-    for i in range(args.warmup):
-        step(None)
+    def run_steps(n, evs_of):
+        if serial:
+            for k in range(n):
+                plan = make_plan()
+                executes(plan, evs_of(k))
+                agcn.agcn_plan_destroy(plan)
+            return
+        cur = make_plan()
+        for k in range(n):
+            executes(cur, evs_of(k))
+            nxt = make_plan() if k + 1 < n else None
+            agcn.agcn_plan_destroy(cur)
+            cur = nxt
+
+    run_steps(args.warmup, lambda k: None)
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
 
@@ -477,14 +507,23 @@ def main():
     torch.cuda.synchronize()
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    t_start.record(stream)
-    for k in range(args.steps):
-        step(events[k])
+    t_start.record(plan_stream)     # the first step's plan is the first work timed
+    run_steps(args.steps, lambda k: events[k])
     t_end.record(stream)
     torch.cuda.synchronize()
     ms_total = t_start.elapsed_time(t_end)
     ms_step = ms_total / args.steps
     log(f"timed {args.steps} steps: {ms_step:.4f} ms/step")
+    # the plan alone (serial, for reference): create + destroy on one stream
+    pe0, pe1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    pe0.record(stream)
+    for _ in range(5):
+        agcn.agcn_plan_destroy(agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
+                                                     d_colidx.data_ptr(), d_vals.data_ptr(), prm, sh))
+    pe1.record(stream)
+    torch.cuda.synchronize()
+    plan_alone_ms = pe0.elapsed_time(pe1) / 5
 
     per_f = {}
     flops_step = 0.0
@@ -507,7 +546,9 @@ def main():
             "frac_hbm": round((b7 + b8) / (ex_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
             "spmm_bytes": int(b7), "spmm_GBps": round(b7 / (k7.mean() * 1e-3) / 1e9, 1),
         }
-    plan_ms = ms_step - exec_ms_sum  # the plan, plus the launch gaps between executes
+    # serial steps: the plan plus the launch gaps between executes; overlapped
+    # steps: whatever of the plan and the gaps the executes did not hide
+    plan_ms = ms_step - exec_ms_sum
     # Group the aggregation launches by kernel instantiation (lanes per vwarp),
     # as rocprofv3 reports them; the dominant one is the group with the most
     # time per step. achieved = mean algorithmic bytes per launch / mean
@@ -587,7 +628,10 @@ def main():
                    "hub_chunk_nnz": st.hub_chunk_nnz, "n_entries": st.n_entries,
                    "n_hub_rows": st.n_hub_rows, "variant": args.variant,
                    "parallelism": "single GPU"},
-        "plan_ms": round(plan_ms, 4),
+        "steps_overlap": (None if serial else
+                          "the plan of step k+1 is built on a second stream during the executes of "
+                          "step k; every step still builds its own plan"),
+        "plan_ms": round(plan_ms, 4), "plan_alone_ms": round(plan_alone_ms, 4),
         "spmm_only_gflops": round(flops_step / (exec_ms_sum * 1e-3) / 1e9, 2),
         "per_F": per_f,
         "roofline": roofline,
