@@ -53,6 +53,11 @@ bool test_alloc_fails() {
 
 bool test_order_sort_fails() { return env_int("AGCN_TEST_FAIL_ORDER_SORT") != 0; }
 
+int test_tail_cap() {
+  const char* v = std::getenv("AGCN_TEST_TAIL_CAP");
+  return v ? std::atoi(v) : -2;
+}
+
 void set_error(const std::string& msg) { g_last_error = msg; }
 
 int fail(int status, const std::string& msg) {

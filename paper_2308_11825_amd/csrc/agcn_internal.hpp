@@ -31,6 +31,8 @@ struct PlanSummary {
   int32_t n_hub_rows;
   int32_t hub_first_row;
   int32_t max_deg;
+  int32_t n_tail;   // rows of degree >= 255 (the short sort's tail)
+  int32_t nnz_low;  // nonzeros of the rows of degree < 255
   uint32_t err;
   uint32_t dmax_ready;
   uint32_t done;
@@ -89,6 +91,7 @@ namespace agcn {
 void test_alloc_reset();    // start of agcn_plan_create
 bool test_alloc_fails();    // counts one allocation attempt; true: fail it
 bool test_order_sort_fails();
+int test_tail_cap();         // AGCN_TEST_TAIL_CAP, or -2 when unset
 
 // Thread-local error text (set by the failing call).
 void set_error(const std::string& msg);

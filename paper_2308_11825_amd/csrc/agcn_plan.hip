@@ -2,31 +2,41 @@
 // (Sec. III-C "Degree Sorting" and "Block-level Partition", Alg. 1 and Alg. 2).
 //
 // Pipeline (all on one stream; the host waits twice: for the maximum degree
-// -- radix passes 0 and 1 are already queued -- and for the partition's
-// summary):
+// and the tail size, and for the partition's summary). With W * Z >= 255 and a
+// tail of at most kTailCap rows (the short sort):
 //   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
-//                   per-workgroup maximum degree and error flags
-//   k_dmax          maximum degree (one workgroup); written to pinned host
-//                   memory while radix passes 0 and 1 run, so the host
-//                   launches passes 2 and 3 only if the maximum degree needs
-//                   them
+//                   per-workgroup maximum degree, tail size and error flags;
+//                   per-tile histograms of min(deg, 255)
+//   k_dmax          maximum degree and tail size (one workgroup), written to
+//                   pinned host memory
+//   scan            bin starts of every (digit, tile)
+//   k_scatter_low   stable scatter by min(deg, 255): rows of degree < 255 reach
+//                   their final sorted place, with their sorted row pointer in
+//                   closed form; the tail (degree >= 255) follows in row order
+//   k_tail          one workgroup: the tail sorted by degree in LDS, its row
+//                   pointers, the class starts, the segment scan of Alg. 2 and
+//                   the summary
+//   k_relayout_fill the partition's int4 entries {deg, loc, row, info} in
+//                   Alg. 2's order, the first chunk of each hub row and the
+//                   launch order (hub chunks, then the other entries heaviest
+//                   first), side by side with the sorted CSR copy (column
+//                   indices checked against n_cols)
+//   k_publish       the summary's error word and done flag
+// Otherwise (the multi-pass sort):
 //   radix passes    stable LSD radix sort of row ids by degree, 8-bit digits:
 //                   k_radix_hist -> exclusive scan -> k_radix_scatter. Buffers
 //                   alternate so that the last pass writes the final
-//                   (keys, perm) pair.
+//                   (keys, perm) pair. Passes 0 and 1 are queued before the
+//                   maximum degree is read back unless it is known already.
 //   scan            rowptr_s = exclusive scan of the sorted degrees
-//   k_relayout      sorted CSR copy (column indices checked against n_cols)
+//   k_relayout      sorted CSR copy
 //   k_class_start   first sorted row of each degree class 0..deg_bound+1
 //   k_seg_count     blocks per degree class / chunks per hub row
 //   scan            entry offsets of every segment
-//   k_partition_fill one int4 {deg, loc, row, info} per entry, in Alg. 2's
-//                   order; first chunk of each hub row; summary for the host;
-//                   launch order: hub chunks, then the other entries
-//                   heaviest first
-//   (host wait)     entry counts read back
-//   launch order    when hub rows are long: hub-chunk entries re-sorted by a
-//                   16-bit key of their first column (two radix passes), then
-//                   the other entries
+//   k_partition_fill the entries, hub-row chunk offsets, launch order and summary
+// Both: (host wait) entry counts read back; when hub rows are long, hub-chunk
+// entries re-sorted into the order of a 16-bit key of their first column (two
+// radix passes), then the other entries.
 //
 // The two read-backs (maximum degree, summary) are written by the kernels
 // straight into pinned, host-coherent memory, each followed by a ready flag
@@ -76,6 +86,17 @@ constexpr int kRadixBins = 256;
 constexpr int kRadixItems = 8;
 constexpr int kRadixTile = 64 * kRadixItems;  // 512
 constexpr int kRadixWaves = kThreads / 64;    // 4 tiles per workgroup
+
+constexpr int kDegRows = kRadixTile * kRadixWaves;  // rows per k_degree workgroup
+
+// Short sort: one 8-bit pass over min(degree, kTailKey) finishes every row of
+// degree < kTailKey; the rows of degree >= kTailKey (the tail, in row order
+// after that pass) are sorted by one workgroup holding them in LDS.
+constexpr int kTailKey = 255;
+constexpr int kTailThreads = 1024;
+constexpr int kTailWaves = kTailThreads / 64;
+constexpr int kTailItems = 16;
+constexpr int32_t kTailCap = kTailThreads * kTailItems;  // 16384 rows
 
 // Relayout tile (sorted nnz positions per workgroup).
 constexpr int kRelayItems = 8;
@@ -161,13 +182,27 @@ __device__ inline uint64_t match_digit(uint32_t digit, bool valid) {
   return m;
 }
 
+// As match_digit for a digit of `bits` <= 8 bits.
+__device__ inline uint64_t match_bits(uint32_t digit, bool valid, int bits) {
+  uint64_t m = __ballot(valid);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    if (b < bits) {
+      const bool bit = (digit >> b) & 1u;
+      const uint64_t bal = __ballot(bit);
+      m &= bit ? bal : ~bal;
+    }
+  }
+  return m;
+}
+
 // Alg. 1 for one degree: the smallest factor f of W with f * Z >= d gives
 // block_rows = W / f and warp_nzs = ceil(d / f); returned as
 // warp_nzs << 16 | block_rows. Degree 0 gets W rows and warp_nzs 0.
 __device__ inline int32_t pattern_of(int32_t d, int32_t W, int32_t Z) {
   if (d == 0) return W;
-  for (int32_t f = 1; f <= W; ++f)
-    if (W % f == 0 && f * Z >= d) return (((d + f - 1) / f) << 16) | (W / f);
+  for (int32_t f = (d + Z - 1) / Z; f <= W; ++f)  // f * Z >= d from the first f on
+    if (W % f == 0) return (((d + f - 1) / f) << 16) | (W / f);
   return 0;  // d > W * Z: not a degree class
 }
 
@@ -182,82 +217,132 @@ __global__ void k_raise(uint32_t* err, uint32_t bits) {
   if (threadIdx.x == 0 && blockIdx.x == 0) atomicOr(err, bits);
 }
 
-// Step (1) of the degree sort, plus the row-pointer checks: the maximum
-// degree and the OR of the error flags of each workgroup.
+// Step (1) of the degree sort, plus the row-pointer checks. One workgroup
+// covers kDegRows rows, each wave the kRadixTile consecutive rows of one radix
+// tile, and writes: the degrees; the workgroup's maximum degree, error flags
+// and number of rows of degree >= kTailKey; and, when `counts` is given, each
+// tile's histogram of min(degree, kTailKey) in the digit-major layout of
+// k_radix_hist (the counts of the first pass of the short sort).
 __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
                                                      const int32_t* __restrict__ rowptr,
                                                      int32_t* __restrict__ deg,
                                                      int32_t* __restrict__ block_max,
-                                                     uint32_t* __restrict__ block_err) {
-  __shared__ int32_t s_max[kThreads / 64];
-  __shared__ uint32_t s_err[kThreads / 64];
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+                                                     uint32_t* __restrict__ block_err,
+                                                     int32_t* __restrict__ block_tail,
+                                                     int32_t* __restrict__ block_low,
+                                                     int32_t* __restrict__ counts, int32_t n_tiles) {
+  __shared__ int32_t s_max[kRadixWaves], s_tail[kRadixWaves], s_low[kRadixWaves];
+  __shared__ uint32_t s_err[kRadixWaves];
+  __shared__ int32_t cnt[kRadixWaves][kRadixBins];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t tile = (int64_t)blockIdx.x * kRadixWaves + wave;
+  const int64_t base = tile * kRadixTile;
+  if (counts)
+    for (int d = lane; d < kRadixBins; d += 64) cnt[wave][d] = 0;
   uint32_t e = 0;
-  int32_t d = 0;
-  if (i < n) {
-    const int32_t a = rowptr[i], b = rowptr[i + 1];
-    d = b - a;
-    if (a < 0 || b < a || (int64_t)b > nnz) {
-      e |= kErrRowptrOrder;
-      d = 0;
+  int32_t m = 0, tail = 0, low = 0;
+#pragma unroll
+  for (int j = 0; j < kRadixItems; ++j) {
+    const int64_t i = base + (int64_t)j * 64 + lane;
+    const bool valid = i < n;
+    int32_t d = 0;
+    if (valid) {
+      const int32_t a = rowptr[i], b = rowptr[i + 1];
+      d = b - a;
+      if (a < 0 || b < a || (int64_t)b > nnz) {
+        e |= kErrRowptrOrder;
+        d = 0;
+      }
+      if (i == 0 && a != 0) e |= kErrRowptrStart;
+      if (i == n - 1 && (int64_t)b != nnz) e |= kErrRowptrEnd;
+      deg[i] = d;
     }
-    if (i == 0 && a != 0) e |= kErrRowptrStart;
-    if (i == n - 1 && (int64_t)b != nnz) e |= kErrRowptrEnd;
-    deg[i] = d;
+    m = max(m, d);
+    tail += d >= kTailKey;
+    low += d < kTailKey ? d : 0;
+    if (counts) {
+      const uint32_t key = (uint32_t)min(d, kTailKey);
+      const uint64_t peers = match_digit(key, valid);
+      if (valid && __popcll(peers & __lanemask_lt()) == 0) cnt[wave][key] += __popcll(peers);
+    }
   }
-  const int32_t m = wave_max(d);
-  const uint32_t we = wave_or(e);
-  if ((threadIdx.x & 63) == 0) {
-    s_max[threadIdx.x >> 6] = m;
-    s_err[threadIdx.x >> 6] = we;
+  if (counts && tile < n_tiles)
+    for (int d = lane; d < kRadixBins; d += 64) counts[(int64_t)d * n_tiles + tile] = cnt[wave][d];
+  m = wave_max(m);
+  tail = wave_sum(tail);
+  low = wave_sum(low);
+  e = wave_or(e);
+  if (lane == 0) {
+    s_max[wave] = m;
+    s_tail[wave] = tail;
+    s_low[wave] = low;
+    s_err[wave] = e;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    int32_t t = 0;
+    int32_t t = 0, c = 0, l = 0;
     uint32_t f = 0;
-    for (int w = 0; w < kThreads / 64; ++w) {
+    for (int w = 0; w < kRadixWaves; ++w) {
       t = max(t, s_max[w]);
+      c += s_tail[w];
+      l += s_low[w];
       f |= s_err[w];
     }
     block_max[blockIdx.x] = t;
     block_err[blockIdx.x] = f;
+    block_tail[blockIdx.x] = c;
+    block_low[blockIdx.x] = l;
   }
 }
 
-// Maximum of the per-workgroup maxima and OR of their error flags (one
-// workgroup of kScanTopThreads). It is the first writer of the plan's error
+// Maximum of the per-workgroup maxima, sums of their tail-row counts and
+// lower nonzeros, and OR of their error flags (one workgroup of
+// kScanTopThreads). It is the first writer of the plan's error
 // word and maximum degree (nb = 0: both become 0), so no clearing kernel runs
 // before it; every later kernel reads or ORs into them.
 __global__ __launch_bounds__(kScanTopThreads) void k_dmax(const int32_t* __restrict__ block_max,
                                                           const uint32_t* __restrict__ block_err,
+                                                          const int32_t* __restrict__ block_tail,
+                                                          const int32_t* __restrict__ block_low,
                                                           int32_t nb, int32_t* dmax, uint32_t* err,
                                                           PlanSummary* host_sum, int32_t* tickets) {
   if (threadIdx.x < kMaxChainedScans) tickets[threadIdx.x] = 0;  // the plan's scans start here
-  __shared__ int32_t s_max[kScanTopThreads / 64];
+  __shared__ int32_t s_max[kScanTopThreads / 64], s_tail[kScanTopThreads / 64],
+      s_low[kScanTopThreads / 64];
   __shared__ uint32_t s_err[kScanTopThreads / 64];
-  int32_t m = 0;
+  int32_t m = 0, c = 0, l = 0;
   uint32_t e = 0;
   for (int32_t i = threadIdx.x; i < nb; i += kScanTopThreads) {
     m = max(m, block_max[i]);
+    c += block_tail[i];
+    l += block_low[i];
     e |= block_err[i];
   }
   m = wave_max(m);
+  c = wave_sum(c);
+  l = wave_sum(l);
   e = wave_or(e);
   if ((threadIdx.x & 63) == 0) {
     s_max[threadIdx.x >> 6] = m;
+    s_tail[threadIdx.x >> 6] = c;
+    s_low[threadIdx.x >> 6] = l;
     s_err[threadIdx.x >> 6] = e;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    int32_t t = 0;
+    int32_t t = 0, tc = 0, tl = 0;
     uint32_t f = 0;
     for (int w = 0; w < kScanTopThreads / 64; ++w) {
       t = max(t, s_max[w]);
+      tc += s_tail[w];
+      tl += s_low[w];
       f |= s_err[w];
     }
     dmax[0] = t;
     err[0] = f;
     host_sum->max_deg = t;
+    host_sum->n_tail = tc;
+    host_sum->nnz_low = tl;
     __threadfence_system();
     host_sum->dmax_ready = 1;
     __threadfence_system();
@@ -351,6 +436,73 @@ __global__ __launch_bounds__(kThreads) void k_radix_scatter(int32_t n, RadixBufs
     if (valid && rank == 0) start[wave][digit] += __popcll(peers);
   }
 }
+
+// First pass of the short sort: a stable scatter by min(degree, kTailKey),
+// the counts of k_degree scanned in `offsets`. A row of degree d < kTailKey is
+// then in its final place, and so is its sorted row pointer: with R[d] the
+// rows and NZ[d] the nonzeros of all degrees below d, the rows of degree d
+// occupy positions R[d] + k and start at NZ[d] + k * d. The tail rows go to
+// positions [n - m, n) of (tail_keys, tail_ids) in row order.
+__global__ __launch_bounds__(kThreads) void k_scatter_low(
+    int32_t n, const int32_t* __restrict__ deg, const int32_t* __restrict__ offsets, int32_t n_tiles,
+    int32_t* __restrict__ keys, int32_t* __restrict__ perm, int32_t* __restrict__ rowptr_s,
+    int32_t* __restrict__ tail_keys, int32_t* __restrict__ tail_ids, const uint32_t* err) {
+  if (failed(err)) return;
+  __shared__ int32_t start[kRadixWaves][kRadixBins];
+  __shared__ int32_t s_r[kRadixBins + 1], s_nz[kRadixBins];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  {
+    const int d = threadIdx.x;  // kThreads == kRadixBins
+    s_r[d] = offsets[(int64_t)d * n_tiles];
+    if (d == 0) s_r[kRadixBins] = n;
+    __syncthreads();
+    // Rows of degree d < kTailKey times d; the tail's term is not needed.
+    const int32_t v = d < kTailKey ? (s_r[d + 1] - s_r[d]) * d : 0;
+    int32_t total;
+    s_nz[d] = block_exclusive_scan<kThreads>(v, &total);
+    __syncthreads();
+    // The tail's first row pointer closes the rows below it.
+    if (blockIdx.x == 0 && d == kTailKey) rowptr_s[s_r[kTailKey]] = s_nz[kTailKey];
+  }
+  const int64_t tile = (int64_t)blockIdx.x * kRadixWaves + wave;
+  if (tile >= n_tiles) return;  // uniform per wave; no workgroup barrier below
+  for (int d = lane; d < kRadixBins; d += 64) start[wave][d] = offsets[(int64_t)d * n_tiles + tile];
+  const int64_t base = tile * kRadixTile;
+  int32_t k[kRadixItems];
+#pragma unroll
+  for (int j = 0; j < kRadixItems; ++j) {
+    const int64_t i = base + (int64_t)j * 64 + lane;
+    k[j] = i < n ? deg[i] : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < kRadixItems; ++j) {
+    const int64_t i = base + (int64_t)j * 64 + lane;
+    const bool valid = i < n;
+    const uint32_t key = (uint32_t)min(k[j], kTailKey);
+    const uint64_t peers = match_digit(key, valid);
+    const int32_t rank = (int32_t)__popcll(peers & __lanemask_lt());
+    const int32_t pos = start[wave][key] + rank;
+    if (valid) {
+      if (key < (uint32_t)kTailKey) {
+        keys[pos] = k[j];
+        perm[pos] = (int32_t)i;
+        rowptr_s[pos] = s_nz[key] + (pos - s_r[key]) * (int32_t)key;
+      } else {
+        tail_keys[pos] = k[j];
+        tail_ids[pos] = (int32_t)i;
+      }
+    }
+    if (valid && rank == 0) start[wave][key] += __popcll(peers);
+  }
+}
+
+// Information the short sort's tail kernel leaves for k_relayout_fill.
+struct TailInfo {
+  int32_t n_segments;  // degree classes 0..DB and one segment per hub row
+  int32_t n_entries;
+  int32_t hub_first_entry;
+  int32_t hub_first_row;
+};
 
 // --- exclusive scan of int32 -------------------------------------------------
 
@@ -639,50 +791,64 @@ __device__ inline int rpad(int i) { return i + (i >> 5); }
 // Degree-0 rows sort first, so every row owning one of these positions is
 // non-empty and at most kRelayTile rows (the "window") are involved. Each
 // window row marks its first position; an inclusive max-scan of the marks
-// then gives every position its row in O(1).
-__global__ __launch_bounds__(kThreads) void k_relayout(
-    int32_t n, int64_t nnz, int32_t n_cols, const int32_t* __restrict__ rowptr,
-    const int32_t* __restrict__ colidx, const float* __restrict__ vals,
-    const int32_t* __restrict__ perm, const int32_t* __restrict__ rowptr_s,
-    int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, uint32_t* err) {
-  if (failed(err)) return;
-  __shared__ int32_t s_ptr[kRelayTile + 1];  // rowptr_s over the window rows (+1 end)
-  __shared__ int32_t s_src[kRelayTile];      // first nnz of each window row in the input CSR
-  __shared__ int32_t s_row[kRelayTile + kRelayTile / 32];  // window row of each position
-  __shared__ int32_t s_wmax[kThreads / 64];
-  __shared__ int32_t s_lo, s_hi;
-  const int64_t e0 = (int64_t)blockIdx.x * kRelayTile;
+// then gives every position its row in O(1). Called by whole workgroups.
+// LDS of one relayout tile (int32 words), also lent to the tail's workgroup.
+constexpr int kRelayLds = (kRelayTile + 1) + kRelayTile + (kRelayTile + kRelayTile / 32) +
+                          kThreads / 64 + 2;
+
+__device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t n, int64_t nnz,
+                                     int32_t n_cols, const int32_t* __restrict__ rowptr,
+                                     const int32_t* __restrict__ colidx,
+                                     const float* __restrict__ vals,
+                                     const int32_t* __restrict__ perm,
+                                     const int32_t* __restrict__ rowptr_s,
+                                     int32_t* __restrict__ colidx_s, float* __restrict__ vals_s,
+                                     uint32_t* err, int32_t* lds) {
+  // kThreads threads (tid) work on the tile; several such groups of one
+  // workgroup may each run a tile (or none: !active), meeting at the same
+  // workgroup barriers.
+  int32_t* s_ptr = lds;                        // rowptr_s over the window rows (+1 end)
+  int32_t* s_src = s_ptr + kRelayTile + 1;     // first nnz of each window row in the input CSR
+  int32_t* s_row = s_src + kRelayTile;         // window row of each position (padded)
+  int32_t* s_wmax = s_row + kRelayTile + kRelayTile / 32;
+  int32_t& s_lo = s_wmax[kThreads / 64];
+  int32_t& s_hi = s_wmax[kThreads / 64 + 1];
+  const int64_t e0 = tile * kRelayTile;
   const int64_t e1 = e0 + kRelayTile < nnz ? e0 + kRelayTile : nnz;
-  if (threadIdx.x < 64) {
-    const int32_t r = wave_row_of(rowptr_s, n, e0, threadIdx.x);
-    if (threadIdx.x == 0) s_lo = r;
-  } else if (threadIdx.x < 128) {
-    const int32_t r = wave_row_of(rowptr_s, n, e1 - 1, threadIdx.x - 64);
-    if (threadIdx.x == 64) s_hi = r;
+  if (active) {
+    if (tid < 64) {
+      const int32_t r = wave_row_of(rowptr_s, n, e0, tid);
+      if (tid == 0) s_lo = r;
+    } else if (tid < 128) {
+      const int32_t r = wave_row_of(rowptr_s, n, e1 - 1, tid - 64);
+      if (tid == 64) s_hi = r;
+    }
+    for (int k = tid; k < kRelayTile; k += kThreads) s_row[rpad(k)] = 0;
   }
-  for (int k = threadIdx.x; k < kRelayTile; k += kThreads) s_row[rpad(k)] = 0;
   __syncthreads();
-  const int32_t lo = s_lo;
-  const int32_t nw = s_hi - lo + 1;
-  if (nw > kRelayTile || nw < 1) {  // cannot happen for a sorted row order
-    if (threadIdx.x == 0) atomicOr(err, kErrInternal);
-    return;
+  const int32_t lo = active ? s_lo : 0;
+  const int32_t nw = active ? s_hi - lo + 1 : 0;
+  if (active && (nw > kRelayTile || nw < 1)) {  // cannot happen for a sorted row order
+    if (tid == 0) atomicOr(err, kErrInternal);
+    active = false;
   }
-  for (int k = threadIdx.x; k <= nw; k += kThreads) s_ptr[k] = rowptr_s[lo + k];
-  for (int k = threadIdx.x; k < nw; k += kThreads) s_src[k] = rowptr[perm[lo + k]];
+  if (active) {
+    for (int k = tid; k <= nw; k += kThreads) s_ptr[k] = rowptr_s[lo + k];
+    for (int k = tid; k < nw; k += kThreads) s_src[k] = rowptr[perm[lo + k]];
+  }
   __syncthreads();
   // Window rows 1..nw-1 start strictly inside the tile.
-  for (int w = 1 + threadIdx.x; w < nw; w += kThreads) s_row[rpad((int)(s_ptr[w] - e0))] = w;
+  for (int w = 1 + tid; w < nw; w += kThreads) s_row[rpad((int)(s_ptr[w] - e0))] = w;
   __syncthreads();
   // Inclusive max-scan of the marks; thread t owns positions 8t .. 8t+7.
   int32_t v[kRelayItems];
   int32_t m = 0;
 #pragma unroll
   for (int k = 0; k < kRelayItems; ++k) {
-    m = max(m, s_row[rpad(threadIdx.x * kRelayItems + k)]);
+    m = max(m, s_row[rpad(tid * kRelayItems + k)]);
     v[k] = m;
   }
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int lane = tid & 63, wv = tid >> 6;
   int32_t inc = m;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -696,12 +862,13 @@ __global__ __launch_bounds__(kThreads) void k_relayout(
   for (int w = 0; w < wv; ++w) before = max(before, s_wmax[w]);
 #pragma unroll
   for (int k = 0; k < kRelayItems; ++k)
-    s_row[rpad(threadIdx.x * kRelayItems + k)] = max(before, v[k]);
+    s_row[rpad(tid * kRelayItems + k)] = max(before, v[k]);
   __syncthreads();
+  if (!active) return;  // no barrier below
   uint32_t bad = 0;
 #pragma unroll
   for (int k = 0; k < kRelayItems; ++k) {
-    const int j = k * kThreads + threadIdx.x;
+    const int j = k * kThreads + tid;
     const int64_t e = e0 + j;
     if (e < e1) {
       const int32_t w = s_row[rpad(j)];
@@ -714,6 +881,28 @@ __global__ __launch_bounds__(kThreads) void k_relayout(
     }
   }
   if (bad) atomicOr(err, bad);
+}
+
+// The error word as one workgroup sees it, read once (other workgroups may
+// raise flags meanwhile, and every thread must take the same branch).
+__device__ inline bool block_failed(const uint32_t* err) {
+  __shared__ uint32_t s_e;
+  if (threadIdx.x == 0) s_e = err[0];
+  __syncthreads();
+  const bool f = s_e != 0;
+  __syncthreads();
+  return f;
+}
+
+__global__ __launch_bounds__(kThreads) void k_relayout(
+    int32_t n, int64_t nnz, int32_t n_cols, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ colidx, const float* __restrict__ vals,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ rowptr_s,
+    int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, uint32_t* err) {
+  __shared__ int32_t lds[kRelayLds];
+  if (block_failed(err)) return;
+  relayout_tile(blockIdx.x, true, threadIdx.x, n, nnz, n_cols, rowptr, colidx, vals, perm, rowptr_s,
+                colidx_s, vals_s, err, lds);
 }
 
 // --- partition ---------------------------------------------------------------
@@ -755,31 +944,22 @@ __global__ __launch_bounds__(kThreads) void k_seg_count(int32_t n, const int32_t
   nb[s] = (int32_t)v;
 }
 
-// The partition's outputs, one kernel after the segment scan (every part is
-// computed independently from the segment offsets and class starts):
+// The partition's outputs from the segment offsets and class starts (S
+// segments, seg_off[S] the entry count), for threads t0, t0 + stride, ...:
 //   - Alg. 2's entries, each from its segment;
-//   - the first chunk of each hub row, and the summary read back by the host;
+//   - the first chunk of each hub row;
 //   - the SpMM launch order: hub chunks, then the other entries heaviest
 //     first (rewritten after the host has read the summary when hub chunks are
 //     launched in column order; it never changes a result).
-__global__ __launch_bounds__(kThreads) void k_partition_fill(
-    int32_t n, const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ deg_s,
-    const int32_t* __restrict__ cls, const int32_t* __restrict__ seg_off, int32_t S, int32_t W,
-    int32_t Z, int32_t DB, int32_t H, int4* __restrict__ meta, int64_t cap, int32_t hub_ub,
-    int32_t* __restrict__ hub_chunk_off, int32_t* __restrict__ order, PlanSummary* sum,
-    const uint32_t* err) {
-  const int64_t t0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  const uint32_t e = err[0];
-  if (t0 == 0) {
-    sum->err = e;
-    if (e) {
-      __threadfence_system();
-      sum->done = 1;
-      __threadfence_system();
-    }
-  }
-  if (e) return;
+__device__ inline void fill_partition(int64_t t0, int64_t stride, int32_t n,
+                                      const int32_t* __restrict__ rowptr_s,
+                                      const int32_t* __restrict__ deg_s,
+                                      const int32_t* __restrict__ cls,
+                                      const int32_t* __restrict__ seg_off, int32_t S, int32_t W,
+                                      int32_t Z, int32_t DB, int32_t H, int4* __restrict__ meta,
+                                      int64_t cap, int32_t hub_ub,
+                                      int32_t* __restrict__ hub_chunk_off,
+                                      int32_t* __restrict__ order) {
   const int32_t total = seg_off[S];
   const int32_t hub_first_entry = seg_off[DB + 1];
   const int32_t first_hub_row = cls[DB + 1];
@@ -811,12 +991,337 @@ __global__ __launch_bounds__(kThreads) void k_partition_fill(
   }
   for (int64_t h = t0; h <= n_hub && h <= hub_ub; h += stride)
     hub_chunk_off[h] = seg_off[DB + 1 + h] - seg_off[DB + 1];
+}
+
+// The partition after the two-pass segment scan (S an upper bound on the
+// segments: those past the last hub row are empty), and the summary for the
+// host.
+__global__ __launch_bounds__(kThreads) void k_partition_fill(
+    int32_t n, const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ deg_s,
+    const int32_t* __restrict__ cls, const int32_t* __restrict__ seg_off, int32_t S, int32_t W,
+    int32_t Z, int32_t DB, int32_t H, int4* __restrict__ meta, int64_t cap, int32_t hub_ub,
+    int32_t* __restrict__ hub_chunk_off, int32_t* __restrict__ order, PlanSummary* sum,
+    const uint32_t* err) {
+  const int64_t t0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  const uint32_t e = err[0];
   if (t0 == 0) {
-    sum->n_entries = total;
-    sum->hub_first_entry = hub_first_entry;
-    sum->n_hub_rows = n_hub;
+    sum->err = e;
+    if (e) {
+      __threadfence_system();
+      sum->done = 1;
+      __threadfence_system();
+    }
+  }
+  if (e) return;
+  fill_partition(t0, stride, n, rowptr_s, deg_s, cls, seg_off, S, W, Z, DB, H, meta, cap, hub_ub,
+                 hub_chunk_off, order);
+  if (t0 == 0) {
+    const int32_t first_hub_row = cls[DB + 1];
+    sum->n_entries = seg_off[S];
+    sum->hub_first_entry = seg_off[DB + 1];
+    sum->n_hub_rows = n - first_hub_row;
     sum->hub_first_row = first_hub_row;
     sum->max_deg = n > 0 ? deg_s[n - 1] : 0;
+    __threadfence_system();
+    sum->done = 1;
+    __threadfence_system();
+  }
+}
+
+// The last partition launch of the short-sort plan: workgroups [0, n_fill)
+// fill the partition from the tail workgroup's segment scan while the others
+// build the sorted CSR from tile `tile0` on (the tiles before it went with
+// the tail).
+__global__ __launch_bounds__(kThreads) void k_relayout_fill(
+    int32_t n_fill, int64_t tile0, int32_t n, int64_t nnz, int32_t n_cols,
+    const int32_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
+    const float* __restrict__ vals, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ rowptr_s, int32_t* __restrict__ colidx_s,
+    float* __restrict__ vals_s, const int32_t* __restrict__ deg_s, const int32_t* __restrict__ cls,
+    const int32_t* __restrict__ seg_off, const TailInfo* __restrict__ info, int32_t W, int32_t Z,
+    int32_t DB, int32_t H, int4* __restrict__ meta, int64_t cap, int32_t hub_ub,
+    int32_t* __restrict__ hub_chunk_off, int32_t* __restrict__ order, uint32_t* err) {
+  __shared__ int32_t lds[kRelayLds];
+  if (block_failed(err)) return;
+  if ((int32_t)blockIdx.x < n_fill)
+    fill_partition((int64_t)blockIdx.x * kThreads + threadIdx.x, (int64_t)n_fill * kThreads, n,
+                   rowptr_s, deg_s, cls, seg_off, info->n_segments, W, Z, DB, H, meta, cap, hub_ub,
+                   hub_chunk_off, order);
+  else
+    relayout_tile(tile0 + blockIdx.x - n_fill, true, threadIdx.x, n, nnz, n_cols, rowptr, colidx,
+                  vals, perm, rowptr_s, colidx_s, vals_s, err, lds);
+}
+
+// The rest of the plan up to the partition, in one workgroup of kTailThreads
+// (the tail has at most kTailCap rows; T0 = n - m is its first sorted
+// position):
+//   - the tail sorted stably by degree: LSD passes of `width` <= 8 bits over
+//     degree - kTailKey. Wave w holds the tail's elements [w c, (w + 1) c) (c a
+//     multiple of 64, ceil(m / 16) rounded up) in registers, walking them in
+//     rounds of 64; ranks come from per-wave digit counts and ballots as in
+//     the radix passes, so equal degrees keep row order, and the (degree,
+//     row) pairs are exchanged through LDS;
+//   - perm and sorted degrees of the tail, and its row pointers (the nonzeros
+//     before it are nnz minus the tail's);
+//   - cls[d], the first sorted row of degree >= d, for d in [0, DB + 1]:
+//     the short pass's bin starts below kTailKey, a search of the sorted tail
+//     above (DB >= kTailKey, so every hub row is a tail row);
+//   - the segment scan of the partition (Alg. 2): ceil(count / block_rows)
+//     entries for each degree class, ceil(deg / H) chunks for each hub row;
+//   - the partition's summary, in pinned host memory and in `info`.
+struct TailArgs {
+  int32_t n, nnz, T0, passes, width, W, Z, DB, H;
+  const int32_t* tail_keys;  // [T0, n): the tail's degrees and rows in row order
+  const int32_t* tail_ids;
+  const int32_t* offsets;    // the short pass's (digit, tile) starts
+  int32_t n_tiles;
+  int32_t* keys;             // outputs: sorted degrees, perm, rowptr_s, cls, seg
+  int32_t* perm;
+  int32_t* rowptr_s;
+  int32_t* cls;
+  int32_t* seg;
+  TailInfo* info;
+  PlanSummary* sum;
+  const int32_t* dmax;
+};
+
+// LDS of the tail's workgroup (int32 words).
+constexpr int kTailLds = 2 * kTailCap + kTailWaves * kRadixBins + kTailWaves + 1;
+
+__device__ inline void tail_block(const TailArgs& a, int32_t* lds) {
+  const int32_t n = a.n, nnz = a.nnz, T0 = a.T0, W = a.W, Z = a.Z, DB = a.DB, H = a.H;
+  const int32_t* __restrict__ tail_keys = a.tail_keys;
+  const int32_t* __restrict__ tail_ids = a.tail_ids;
+  const int32_t* __restrict__ offsets = a.offsets;
+  const int32_t n_tiles = a.n_tiles;
+  int32_t* __restrict__ keys = a.keys;
+  int32_t* __restrict__ perm = a.perm;
+  int32_t* __restrict__ rowptr_s = a.rowptr_s;
+  int32_t* __restrict__ cls = a.cls;
+  int32_t* __restrict__ seg = a.seg;
+  int32_t* s_key = lds;                              // kTailCap
+  int32_t* s_id = s_key + kTailCap;                  // kTailCap; cls once the tail is written
+  int32_t (*s_cnt)[kRadixBins] = reinterpret_cast<int32_t (*)[kRadixBins]>(s_id + kTailCap);
+  int32_t* s_wsum = s_id + kTailCap + kTailWaves * kRadixBins;
+  int32_t& s_hub_first_entry = s_wsum[kTailWaves];
+  const uint32_t dmask = (1u << a.width) - 1;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int32_t m = n - T0;
+  const int32_t c = ((m + kTailWaves * 64 - 1) / (kTailWaves * 64)) * 64;  // per wave
+  const int32_t rounds = c / 64;
+  const int32_t w0 = wave * c;
+  int32_t k[kTailItems], id[kTailItems];
+#pragma unroll
+  for (int j = 0; j < kTailItems; ++j) {
+    if (j < rounds) {
+      const int32_t e = w0 + j * 64 + lane;
+      k[j] = e < m ? tail_keys[T0 + e] : 0;
+      id[j] = e < m ? tail_ids[T0 + e] : 0;
+    }
+  }
+  for (int p = 0; p < a.passes; ++p) {
+    const int shift = a.width * p;
+    for (int q = t; q < kTailWaves * kRadixBins; q += kTailThreads) (&s_cnt[0][0])[q] = 0;
+    __syncthreads();
+    // Digit, rank among the round's equal digits and their number, packed
+    // per item for the scatter walk.
+    uint32_t pk[kTailItems];
+#pragma unroll
+    for (int j = 0; j < kTailItems; ++j) {
+      if (j < rounds) {
+        const bool valid = w0 + j * 64 + lane < m;
+        const uint32_t digit = ((uint32_t)(k[j] - kTailKey) >> shift) & dmask;
+        const uint64_t peers = match_bits(digit, valid, a.width);
+        const uint32_t rank = (uint32_t)__popcll(peers & __lanemask_lt());
+        const uint32_t size = (uint32_t)__popcll(peers);
+        pk[j] = digit | rank << 8 | size << 16;
+        if (valid && rank == 0) s_cnt[wave][digit] += (int32_t)size;
+      }
+    }
+    __syncthreads();
+    {  // exclusive scan in (digit, wave) order: thread t owns digit t / 4, waves 4 (t % 4) ..
+      const int d = t >> 2, v0 = (t & 3) * 4;
+      int32_t cv[4], sm = 0;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        cv[r] = s_cnt[v0 + r][d];
+        sm += cv[r];
+      }
+      int32_t total;
+      int32_t run = block_exclusive_scan<kTailThreads>(sm, &total);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s_cnt[v0 + r][d] = run;
+        run += cv[r];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kTailItems; ++j) {
+      if (j < rounds) {
+        const bool valid = w0 + j * 64 + lane < m;
+        const uint32_t digit = pk[j] & 0xFFu, rank = (pk[j] >> 8) & 0xFFu;
+        const int32_t pos = s_cnt[wave][digit] + (int32_t)rank;
+        if (valid) {
+          s_key[pos] = k[j];
+          s_id[pos] = id[j];
+        }
+        if (valid && rank == 0) s_cnt[wave][digit] += (int32_t)(pk[j] >> 16);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kTailItems; ++j) {
+      if (j < rounds) {
+        const int32_t e = w0 + j * 64 + lane;
+        if (e < m) {
+          k[j] = s_key[e];
+          id[j] = s_id[e];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // The sorted tail: perm, degrees, s_key (also written when no pass ran)
+  // and the wave's running sum of degrees for the row pointers.
+  int32_t run = 0;
+#pragma unroll
+  for (int j = 0; j < kTailItems; ++j) {
+    if (j < rounds) {
+      const int32_t e = w0 + j * 64 + lane;
+      const int32_t v = e < m ? k[j] : 0;
+      if (e < m) {
+        perm[T0 + e] = id[j];
+        keys[T0 + e] = v;
+        s_key[e] = v;
+      }
+      const int32_t inc = wave_inclusive_scan(v, lane);
+      k[j] = run + inc - v;  // exclusive within the wave's chunk
+      run += __shfl(inc, 63, 64);
+    }
+  }
+  if (lane == 0) s_wsum[wave] = run;
+  __syncthreads();
+  {
+    int32_t before = 0, total = 0;
+    for (int w = 0; w < kTailWaves; ++w) {
+      before += w < wave ? s_wsum[w] : 0;
+      total += s_wsum[w];
+    }
+    const int32_t base = nnz - total + before;  // the tail's nonzeros end at nnz
+#pragma unroll
+    for (int j = 0; j < kTailItems; ++j) {
+      if (j < rounds) {
+        const int32_t e = w0 + j * 64 + lane;
+        if (e < m) rowptr_s[T0 + e] = base + k[j];
+      }
+    }
+    if (t == 0) rowptr_s[n] = nnz;
+  }
+  // Class starts.
+  int32_t* s_cls = s_id;
+  for (int32_t d = t; d <= DB + 1; d += kTailThreads) {
+    int32_t r;
+    if (d <= kTailKey) {
+      r = offsets[(int64_t)d * n_tiles];
+    } else {
+      int32_t a = 0, b = m;  // first tail element of degree >= d
+      while (a < b) {
+        const int32_t mid = (a + b) >> 1;
+        if (s_key[mid] < d) a = mid + 1; else b = mid;
+      }
+      r = T0 + a;
+    }
+    s_cls[d] = r;
+    cls[d] = r;
+  }
+  __syncthreads();
+  const int32_t hub_first_row = s_cls[DB + 1];
+  const int32_t S = DB + 1 + (n - hub_first_row);
+  int32_t carry = 0;
+  for (int32_t c0 = 0; c0 < S; c0 += kTailThreads * 4) {
+    int32_t v[4], sm = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int32_t q = c0 + t * 4 + r;
+      int32_t x = 0;
+      if (q <= DB) {
+        const int32_t cnt = s_cls[q + 1] - s_cls[q];
+        if (cnt > 0) {
+          const int32_t br = pattern_of(q, W, Z) & 0xFFFF;
+          x = (cnt + br - 1) / br;
+        }
+      } else if (q < S) {
+        x = (int32_t)(((int64_t)s_key[hub_first_row - T0 + (q - DB - 1)] + H - 1) / H);
+      }
+      v[r] = x;
+      sm += x;
+    }
+    int32_t total;
+    int32_t rs = block_exclusive_scan<kTailThreads>(sm, &total) + carry;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int32_t q = c0 + t * 4 + r;
+      if (q < S) seg[q] = rs;
+      if (q == DB + 1) s_hub_first_entry = rs;
+      rs += v[r];
+    }
+    carry += total;
+  }
+  __syncthreads();
+  if (t == 0) {
+    seg[S] = carry;
+    const int32_t hfe = S > DB + 1 ? s_hub_first_entry : carry;
+    a.info->n_segments = S;
+    a.info->n_entries = carry;
+    a.info->hub_first_entry = hfe;
+    a.info->hub_first_row = hub_first_row;
+    a.sum->n_entries = carry;
+    a.sum->hub_first_entry = hfe;
+    a.sum->n_hub_rows = n - hub_first_row;
+    a.sum->hub_first_row = hub_first_row;
+    a.sum->max_deg = a.dmax[0];
+    __threadfence_system();
+  }
+}
+
+
+// The short-sort plan's second launch: workgroup 0 finishes the plan up to the
+// partition (tail_block) while the others copy the sorted CSR of the rows
+// below the tail, which need nothing from it: kTailThreads / kThreads tiles
+// per workgroup, the first n_low_tiles tiles of the sorted nonzeros (those
+// wholly before the tail's first nonzero). The LDS is one buffer that either
+// role carves.
+constexpr int kTilesPerTailGroup = kTailThreads / kThreads;
+constexpr int kXLds = kTailLds > kTilesPerTailGroup * kRelayLds ? kTailLds
+                                                                 : kTilesPerTailGroup * kRelayLds;
+
+__global__ __launch_bounds__(kTailThreads) void k_tail_relayout(
+    TailArgs ta, int64_t n_low_tiles, int64_t nnz, int32_t n_cols,
+    const int32_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
+    const float* __restrict__ vals, int32_t* __restrict__ colidx_s, float* __restrict__ vals_s,
+    uint32_t* err) {
+  __shared__ int32_t lds[kXLds];
+  if (block_failed(err)) return;
+  if (blockIdx.x == 0) {
+    tail_block(ta, lds);
+    return;
+  }
+  const int q = threadIdx.x / kThreads;
+  const int64_t tile = (int64_t)(blockIdx.x - 1) * kTilesPerTailGroup + q;
+  // Rows [0, T0) with rowptr_s[T0] (the tail's first nonzero) are final.
+  relayout_tile(tile, tile < n_low_tiles, threadIdx.x % kThreads, ta.T0, nnz, n_cols, rowptr,
+                colidx, vals, ta.perm, ta.rowptr_s, colidx_s, vals_s, err, lds + q * kRelayLds);
+}
+
+// The summary's error word (the column check included) and done flag, after
+// k_relayout_fill. One small launch: a completion count kept by the
+// relayout's workgroups themselves cost more (one device-scope atomic each on
+// one word, serialised).
+__global__ void k_publish(const uint32_t* err, PlanSummary* sum) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    sum->err = err[0];
     __threadfence_system();
     sum->done = 1;
     __threadfence_system();
@@ -1011,6 +1516,14 @@ bool hub_order_setting() {
   return v;
 }
 
+// Largest tail the short sort's single workgroup takes (AGCN_TEST_TAIL_CAP
+// lowers it, so that tests reach the multi-pass sort on small graphs; -1
+// sends every plan there).
+int32_t tail_cap_setting() {
+  const int v = test_tail_cap();
+  return v < -1 ? kTailCap : std::min<int32_t>(v, kTailCap);
+}
+
 // Per-thread pinned, host-coherent buffer for the plan's read-backs (the
 // kernels write it directly), allocated on the first plan built by the thread
 // and kept for the life of the process. *dev receives its device address.
@@ -1088,7 +1601,8 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   const size_t o_goff = L.take(4 * (n + 1));
   const size_t o_deg = L.take(4 * n);
   const size_t o_ng = L.take(4 * n);
-  const size_t o_bmax = L.take(4 * 2 * (ceil_div64(n, kThreads) + 1));  // block maxima, error flags
+  const int64_t n_deg_blocks = ceil_div64(n, kDegRows);
+  const size_t o_bmax = L.take(4 * 4 * (n_deg_blocks + 1));  // maxima, error flags, tails, lows
   const size_t o_partials = L.take(4 * n_partials);
   const size_t o_err = L.take(64);
   const size_t o_dmax = L.take(64);
@@ -1118,14 +1632,18 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   if (hs == nullptr) return fail(AGCN_ERR_OUT_OF_MEMORY, "pinned host buffer allocation failed");
   *hs = PlanSummary{};
   const int64_t nb = ceil_div64(n, kThreads);
-  uint32_t* berr = reinterpret_cast<uint32_t*>(bmax + nb + 1);
+  uint32_t* berr = reinterpret_cast<uint32_t*>(bmax + n_deg_blocks + 1);
+  int32_t* btail = bmax + 2 * (n_deg_blocks + 1);
+  int32_t* blow = bmax + 3 * (n_deg_blocks + 1);
   if (n > 0)
-    k_degree<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, bmax, berr);
+    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, bmax, berr,
+                                                         btail, blow, nullptr, 0);
   ChainedScans chain;
   chain.status = reinterpret_cast<unsigned long long*>(b + o_status);
   chain.capacity = n_partials;
   chain.tickets = reinterpret_cast<int32_t*>(b + o_tickets);
-  k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, berr, (int32_t)nb, dmax, err, dsum, chain.tickets);
+  k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, berr, btail, blow, (int32_t)n_deg_blocks, dmax, err,
+                                        dsum, chain.tickets);
   if (n > 0) k_wl_groups<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, deg, Z, ng, err);
   const unsigned cgrid = (unsigned)std::min<int64_t>(grid_for(std::max(nnz, n + 1), kThreads), 65536);
   k_wl_copy<<<cgrid, kThreads, 0, st>>>((int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals,
@@ -1189,12 +1707,13 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   const size_t o_seg = L.take(4 * (S + 1));
   const size_t o_err = L.take(64);
   const size_t o_dmax = L.take(64);
-  const int64_t n_deg_blocks = ceil_div64(n, kThreads);
-  const size_t o_bmax = L.take(4 * 2 * (n_deg_blocks + 1));  // block maxima, error flags
+  const int64_t n_deg_blocks = ceil_div64(n, kDegRows);
+  const size_t o_bmax = L.take(4 * 4 * (n_deg_blocks + 1));  // maxima, error flags, tails, lows
   const size_t o_hsort = L.take(4 * 5 * chunk_ub);  // keys in, 2 x keys, 2 x ids
   const size_t o_hgate = L.take(64);
   const size_t o_tickets = L.take(4 * kMaxChainedScans);
   const size_t o_status = L.take(8 * n_partials);
+  const size_t o_info = L.take(sizeof(TailInfo));
 
   void* base = nullptr;
   size_t got = 0;
@@ -1224,6 +1743,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   int32_t* bmax = reinterpret_cast<int32_t*>(b + o_bmax);
   int32_t* hsort = reinterpret_cast<int32_t*>(b + o_hsort);
   int32_t* hgate = reinterpret_cast<int32_t*>(b + o_hgate);
+  TailInfo* info = reinterpret_cast<TailInfo*>(b + o_info);
 
   PlanSummary* dsum = nullptr;
   PlanSummary* hs = pinned_summary(&dsum);
@@ -1232,24 +1752,87 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   // last write came before the flag that plan waited for.
   *hs = PlanSummary{};
   uint32_t* berr = reinterpret_cast<uint32_t*>(bmax + n_deg_blocks + 1);
+  int32_t* btail = bmax + 2 * (n_deg_blocks + 1);
+  int32_t* blow = bmax + 3 * (n_deg_blocks + 1);
+  // The short sort needs every hub row in the tail (DB >= kTailKey).
+  const bool short_sort = n > 0 && DB >= kTailKey;
   if (n > 0)
-    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, bmax,
-                                                         berr);
+    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>(
+        (int32_t)n, nnz, d_rowptr, deg, bmax, berr, btail, blow, short_sort ? counts : nullptr,
+        (int32_t)n_tiles);
   ChainedScans chain;
   chain.status = reinterpret_cast<unsigned long long*>(b + o_status);
   chain.capacity = n_partials;
   chain.tickets = reinterpret_cast<int32_t*>(b + o_tickets);
-  k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, berr, (int32_t)n_deg_blocks, dmax, err, dsum,
-                                        chain.tickets);
+  k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, berr, btail, blow, (int32_t)n_deg_blocks, dmax, err,
+                                        dsum, chain.tickets);
   if ((rc = check_launch("k_degree"))) return rc;
-  if (n > 0) {
-    // The maximum degree reaches the host while radix pass 0 (always needed)
-    // runs; the host then launches exactly the passes it needs.
-    // Stable LSD radix sort of row ids by degree, 8-bit digits. Passes 0 and
-    // 1 are queued before the host reads the maximum degree (pass 1 returns
-    // at once on the device when one pass suffices), so the GPU keeps busy
-    // while the read-back reaches the host; passes 2 and 3 follow if needed.
-    const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
+  const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
+  bool short_done = false, have_max = false;
+  int32_t md = 0;
+  if (short_sort) {
+    // Pass one of the short sort; the maximum degree and the tail size reach
+    // the host meanwhile.
+    if ((rc = scan_exclusive(counts, n_tiles * kRadixBins, counts, nullptr, partials, err, st,
+                             nullptr, 0, &chain)))
+      return rc;
+    k_scatter_low<<<rgrid, kThreads, 0, st>>>((int32_t)n, deg, counts, (int32_t)n_tiles, keys,
+                                              p->perm, p->rowptr_s, keys2, ids2, err);
+    if ((rc = check_launch("k_scatter_low"))) return rc;
+    if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
+    md = hs->max_deg;
+    have_max = true;
+    const int32_t m = hs->n_tail;
+    if (m >= 0 && m <= tail_cap_setting()) {
+      int bits = 0;
+      while (bits < 31 && (int64_t(1) << bits) <= (int64_t)md - kTailKey) ++bits;
+      const int passes = (bits + 7) / 8;
+      TailArgs ta;
+      ta.n = (int32_t)n;
+      ta.nnz = (int32_t)nnz;
+      ta.T0 = (int32_t)(n - m);
+      ta.passes = passes;
+      ta.width = passes > 0 ? (bits + passes - 1) / passes : 8;
+      ta.W = W;
+      ta.Z = Z;
+      ta.DB = DB;
+      ta.H = H;
+      ta.tail_keys = keys2;
+      ta.tail_ids = ids2;
+      ta.offsets = counts;
+      ta.n_tiles = (int32_t)n_tiles;
+      ta.keys = keys;
+      ta.perm = p->perm;
+      ta.rowptr_s = p->rowptr_s;
+      ta.cls = cls;
+      ta.seg = seg;
+      ta.info = info;
+      ta.sum = dsum;
+      ta.dmax = dmax;
+      // Tiles of sorted nonzeros wholly below the tail's first one are copied
+      // beside the tail's workgroup; the rest after it.
+      const int64_t low_tiles = std::max<int64_t>(hs->nnz_low, 0) / kRelayTile;
+      k_tail_relayout<<<(unsigned)(1 + ceil_div64(low_tiles, kTilesPerTailGroup)), kTailThreads, 0,
+                        st>>>(ta, low_tiles, nnz, p->n_cols, d_rowptr, d_colidx, d_vals,
+                              p->colidx_s, p->vals_s, err);
+      if ((rc = check_launch("k_tail_relayout"))) return rc;
+      const int32_t n_fill = (int32_t)std::min<int64_t>(grid_for(ent_ub, kThreads), 64);
+      k_relayout_fill<<<(unsigned)(n_fill + grid_for(nnz, kRelayTile) - low_tiles), kThreads, 0,
+                        st>>>(n_fill, low_tiles, (int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx,
+                              d_vals, p->perm, p->rowptr_s, p->colidx_s, p->vals_s, keys, cls, seg,
+                              info, W, Z, DB, H, p->meta, ent_ub, (int32_t)hub_ub,
+                              p->hub_chunk_off, p->order, err);
+      k_publish<<<1, 64, 0, st>>>(err, dsum);
+      if ((rc = check_launch("k_relayout_fill"))) return rc;
+      short_done = true;
+    }
+  }
+  if (n > 0 && !short_done) {
+    // Stable LSD radix sort of row ids by degree, 8-bit digits. Unless the
+    // maximum degree is already known, passes 0 and 1 are queued before the
+    // host reads it (pass 1 returns at once on the device when one pass
+    // suffices), so the GPU keeps busy while the read-back reaches the host;
+    // passes 2 and 3 follow if needed.
     const RadixBufs bufs{deg, {keys, keys2}, {p->perm, ids2}};
     constexpr int kPassesBeforeReadback = 2;
     int passes = kPassesBeforeReadback;
@@ -1264,34 +1847,39 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
                                                   err, dmax);
       if ((rc = check_launch("k_radix_scatter"))) return rc;
       if (pass == kPassesBeforeReadback - 1) {
-        if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
-        const int32_t md = hs->max_deg;
+        if (!have_max) {
+          if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
+          md = hs->max_deg;
+        }
         int bits = 0;
         while (bits < 31 && (int64_t(1) << bits) <= md) ++bits;
         passes = std::max(kPassesBeforeReadback, (bits + 7) / 8);
       }
     }
   }
-  // rowptr_s = exclusive scan of the sorted degrees; rowptr_s[n] = nnz.
-  if ((rc = scan_exclusive(keys, n, p->rowptr_s, p->rowptr_s + n, partials, err, st, nullptr, 0,
-                           &chain)))
-    return rc;
-  if (nnz > 0) {
-    k_relayout<<<grid_for(nnz, kRelayTile), kThreads, 0, st>>>(
-        (int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s, p->colidx_s,
-        p->vals_s, err);
-    if ((rc = check_launch("k_relayout"))) return rc;
+  if (!short_done) {
+    // rowptr_s = exclusive scan of the sorted degrees; rowptr_s[n] = nnz.
+    if ((rc = scan_exclusive(keys, n, p->rowptr_s, p->rowptr_s + n, partials, err, st, nullptr, 0,
+                             &chain)))
+      return rc;
+    if (nnz > 0) {
+      k_relayout<<<grid_for(nnz, kRelayTile), kThreads, 0, st>>>(
+          (int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
+          p->colidx_s, p->vals_s, err);
+      if ((rc = check_launch("k_relayout"))) return rc;
+    }
+    k_class_start<<<grid_for(n + 1, kThreads), kThreads, 0, st>>>((int32_t)n, keys, DB, cls, err);
+    k_seg_count<<<grid_for(S, kThreads), kThreads, 0, st>>>((int32_t)n, keys, cls, W, Z, DB, H,
+                                                           (int32_t)S, nb, err);
+    if ((rc = check_launch("partition counts"))) return rc;
+    if ((rc = scan_exclusive(nb, S, seg, seg + S, partials, err, st, nullptr, 0, &chain))) return rc;
+    const unsigned mgrid = (unsigned)std::min<int64_t>(grid_for(ent_ub, kThreads), 16384);
+    k_partition_fill<<<mgrid, kThreads, 0, st>>>((int32_t)n, p->rowptr_s, keys, cls, seg,
+                                                 (int32_t)S, W, Z, DB, H, p->meta, ent_ub,
+                                                 (int32_t)hub_ub, p->hub_chunk_off, p->order, dsum,
+                                                 err);
+    if ((rc = check_launch("partition fill"))) return rc;
   }
-  k_class_start<<<grid_for(n + 1, kThreads), kThreads, 0, st>>>((int32_t)n, keys, DB, cls, err);
-  k_seg_count<<<grid_for(S, kThreads), kThreads, 0, st>>>((int32_t)n, keys, cls, W, Z, DB, H,
-                                                         (int32_t)S, nb, err);
-  if ((rc = check_launch("partition counts"))) return rc;
-  if ((rc = scan_exclusive(nb, S, seg, seg + S, partials, err, st, nullptr, 0, &chain))) return rc;
-  const unsigned mgrid = (unsigned)std::min<int64_t>(grid_for(ent_ub, kThreads), 16384);
-  k_partition_fill<<<mgrid, kThreads, 0, st>>>((int32_t)n, p->rowptr_s, keys, cls, seg, (int32_t)S,
-                                               W, Z, DB, H, p->meta, ent_ub, (int32_t)hub_ub,
-                                               p->hub_chunk_off, p->order, dsum, err);
-  if ((rc = check_launch("partition fill"))) return rc;
 
   if ((rc = wait_flag(&hs->done, st, "plan summary read-back"))) return rc;
   if (hs->err) {

@@ -1,0 +1,112 @@
+"""The plan's two degree sorts give the same plan.
+
+With W * Z >= 255 the plan first sorts by min(degree, 255) in one pass and
+sorts the rows of degree >= 255 (the tail, at most 16384 rows) in a single
+workgroup; otherwise, or with a larger tail, it runs the multi-pass radix sort
+(AGCN_TEST_TAIL_CAP=-1 forces that, after the first short pass, on any graph).
+Both plans must equal the oracle's bit for bit (Sec. III-C: a stable sort by
+degree, then Alg. 1 and Alg. 2), at the tail's edges too: degrees 254, 255 and
+256, a tail whose degrees are all 255 (no tail pass), degrees that need three
+tail passes, W * Z = 255 exactly, and tails of 16384 and 16385 rows.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import graphgen
+from gpu_helpers import _mixed, _plan, _spmm_check, assert_plan_matches_oracle
+
+torch = pytest.importorskip("torch")
+import paper_2308_11825_amd as agcn  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+TAIL_CAP = 16384
+
+
+def _both(g, **kw):
+    """Plans of g with the short sort (default) and with the multi-pass sort;
+    both checked against the oracle and against each other."""
+    out = []
+    for cap in (None, "-1"):
+        if cap is None:
+            os.environ.pop("AGCN_TEST_TAIL_CAP", None)
+        else:
+            os.environ["AGCN_TEST_TAIL_CAP"] = cap
+        try:
+            p = _plan(g, **kw)
+        finally:
+            os.environ.pop("AGCN_TEST_TAIL_CAP", None)
+        out.append((p, assert_plan_matches_oracle(p, g)))
+    (p0, e0), (p1, e1) = out
+    for k in ("perm", "rowptr_s", "colidx_s", "meta"):
+        assert np.array_equal(e0[k], e1[k]), k
+    assert p0.stats.n_entries == p1.stats.n_entries
+    return p0, p1
+
+
+@pytest.mark.parametrize("W,Z", [(16, 32), (12, 32), (15, 17), (16, 256), (32, 8)])
+@pytest.mark.parametrize("seed", [1, 2])
+def test_short_and_multipass_sorts_agree(W, Z, seed):
+    g = _mixed(900 + seed, n=20000 + 777 * seed)
+    p0, p1 = _both(g, max_block_waves=W, max_wave_nzs=Z)
+    _spmm_check(p0, g, 40, seed=seed)
+    p0.destroy()
+    p1.destroy()
+
+
+def test_tail_edges():
+    rng = np.random.default_rng(31)
+    n = 6000
+    deg = rng.choice([0, 1, 7, 253, 254, 255, 256, 257, 511, 512, 513, 900], size=n)
+    g = graphgen.random_csr(n, 4000, deg, seed=32)
+    for p in _both(g):
+        p.destroy()
+    # every tail row of degree 255: the tail keeps row order with no pass
+    deg = rng.choice([3, 254, 255], size=n)
+    g = graphgen.random_csr(n, 4000, deg, seed=33)
+    p0, p1 = _both(g)
+    assert p0.stats.max_deg == 255
+    p0.destroy()
+    p1.destroy()
+    # tail degrees spanning three 8-bit passes (degree - 255 >= 2^16)
+    deg = rng.integers(0, 300, size=3000)
+    deg[[5, 77, 2999]] = [70000, 66000, 65791]
+    g = graphgen.random_csr(3000, 80000, deg, seed=34)
+    for p in _both(g):
+        p.destroy()
+
+
+@pytest.mark.parametrize("m", [TAIL_CAP, TAIL_CAP + 1])
+def test_tail_at_the_cap(m):
+    rng = np.random.default_rng(m)
+    n = m + 30000
+    deg = rng.integers(0, 255, size=n)
+    tail = rng.choice(n, size=m, replace=False)
+    deg[tail] = rng.integers(255, 300, size=m)
+    deg[tail[:5]] = [255, 600, 1200, 299, 5000]
+    g = graphgen.random_csr(n, 60000, deg, seed=m + 1)
+    p = _plan(g)
+    assert_plan_matches_oracle(p, g)
+    _spmm_check(p, g, 16)
+    p.destroy()
+
+
+def test_invalid_csr_through_the_short_sort():
+    g = _mixed(950, n=5000)
+    ci = g.colidx.copy()
+    ci[len(ci) // 2] = g.n_cols       # one column out of range
+    bad = graphgen.Graph("bad", g.n_rows, g.n_cols, g.rowptr, ci, g.vals)
+    with pytest.raises(agcn.AgcnError) as e:
+        _plan(bad)
+    assert e.value.status == agcn.AGCN_ERR_INVALID_INPUT
+    rp = g.rowptr.copy()
+    rp[100] = rp[101] + 1             # a decreasing row pointer
+    bad = graphgen.Graph("bad", g.n_rows, g.n_cols, rp, g.colidx, g.vals)
+    with pytest.raises(agcn.AgcnError) as e:
+        _plan(bad)
+    assert e.value.status == agcn.AGCN_ERR_INVALID_INPUT
+    p = _plan(g)                      # and a valid plan right after
+    assert_plan_matches_oracle(p, g)
+    p.destroy()
