@@ -139,14 +139,36 @@ __device__ inline uint32_t wave_or(uint32_t v) {
   return v;
 }
 
+// Inclusive scan over the 64 lanes of a wave with DPP row operations (no LDS
+// round trip per step): prefixes of 4 lanes from three row shifts of the
+// input, then of 8 and 16 lanes (row shifts by 4 and 8 on the upper banks of
+// each 16-lane row), then across rows by broadcasting lane 15 into rows 1 and
+// 3 and lane 31 into rows 2 and 3. Disabled or out-of-row lanes contribute 0,
+// the identity of op (sums, and maxima of non-negative values).
+template <typename Op>
+__device__ inline int32_t wave_scan_dpp(int32_t v, Op op) {
+  int32_t x = v;
+  x = op(x, __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, true));   // row_shr:1
+  x = op(x, __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, true));   // row_shr:2
+  x = op(x, __builtin_amdgcn_update_dpp(0, v, 0x113, 0xf, 0xf, true));   // row_shr:3
+  x = op(x, __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xe, false));  // row_shr:4, banks 1-3
+  x = op(x, __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xc, false));  // row_shr:8, banks 2-3
+  x = op(x, __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false));  // row_bcast:15, rows 1, 3
+  x = op(x, __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false));  // row_bcast:31, rows 2, 3
+  return x;
+}
+
+struct OpAdd {
+  __device__ int32_t operator()(int32_t a, int32_t b) const { return a + b; }
+};
+struct OpMax {
+  __device__ int32_t operator()(int32_t a, int32_t b) const { return max(a, b); }
+};
+
 // Inclusive scan over the 64 lanes of a wave.
 __device__ inline int32_t wave_inclusive_scan(int32_t v, int lane) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int32_t y = __shfl_up(v, o, 64);
-    if (lane >= o) v += y;
-  }
-  return v;
+  (void)lane;
+  return wave_scan_dpp(v, OpAdd());
 }
 
 // Exclusive scan across a workgroup of T threads; *total receives the sum.
@@ -849,12 +871,7 @@ __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t
     v[k] = m;
   }
   const int lane = tid & 63, wv = tid >> 6;
-  int32_t inc = m;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int32_t y = __shfl_up(inc, o, 64);
-    if (lane >= o) inc = max(inc, y);
-  }
+  const int32_t inc = wave_scan_dpp(m, OpMax());  // marks are >= 0
   if (lane == 63) s_wmax[wv] = inc;
   int32_t before = __shfl_up(inc, 1, 64);
   if (lane == 0) before = 0;
