@@ -556,16 +556,18 @@ struct Marks {
 };
 
 // Launch positions [e_begin, e_end) of the plan's launch order, every column
-// slice of one width.
+// slice of one width; no entry of the range holds more than max_nnz nonzeros
+// (the LDS staged per workgroup is sized for it).
 struct EntryRange {
   int32_t begin, end;
+  int32_t max_nnz;
 };
 
 template <int VW, int LT>
 void launch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols,
                  Marks& mk, bool last_part, EntryRange er) {
   const agcn_plan* p = a.p;
-  const int cap_pad = stage_words(std::max(p->deg_bound, p->H));
+  const int cap_pad = stage_words(er.max_nnz);
   const int want = p->W * L;
   const int T = std::min(1024, round_up(want, 64));
   const int rounds = (want + T - 1) / T;
@@ -703,11 +705,14 @@ int run_aggregation(const SpmmArgs& a, Marks& mk) {
   const int32_t n_chunks = p->n_hub_rows > 0 ? p->n_entries - p->hub_first_entry : 0;
   const int wide = VW == 4 ? kHubSliceCols : std::min(64, kHubSliceCols);
   if (p->hub_wide && n_chunks > 0 && std::min(a.F, wide) > std::min(a.F, sc)) {
-    int rc = run_phase<VW>(a, false, mk, wide, EntryRange{0, n_chunks}, n_chunks == p->n_entries);
+    // Hub chunks hold at most H nonzeros, the other entries at most W * Z.
+    int rc = run_phase<VW>(a, false, mk, wide, EntryRange{0, n_chunks, p->H},
+                           n_chunks == p->n_entries);
     if (rc || n_chunks == p->n_entries) return rc;
-    return run_phase<VW>(a, false, mk, sc, EntryRange{n_chunks, p->n_entries}, true);
+    return run_phase<VW>(a, false, mk, sc, EntryRange{n_chunks, p->n_entries, p->deg_bound}, true);
   }
-  return run_phase<VW>(a, false, mk, sc, EntryRange{0, p->n_entries}, true);
+  return run_phase<VW>(a, false, mk, sc,
+                       EntryRange{0, p->n_entries, std::max(p->deg_bound, p->H)}, true);
 }
 
 
@@ -870,7 +875,7 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
   int rc = vec ? run_aggregation<4>(a, mk) : run_aggregation<1>(a, mk);
   if (rc) return rc;
   Marks none{};
-  const EntryRange all{0, p->n_entries};
+  const EntryRange all{0, p->n_entries, std::max(p->deg_bound, p->H)};
   if (p->n_hub_rows > 0)
     rc = vec ? run_phase<4>(a, true, none, default_slice_cols<4>(), all, true)
              : run_phase<1>(a, true, none, default_slice_cols<1>(), all, true);
