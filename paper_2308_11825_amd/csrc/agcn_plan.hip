@@ -252,8 +252,15 @@ __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
                                                      uint32_t* __restrict__ block_err,
                                                      int32_t* __restrict__ block_tail,
                                                      int32_t* __restrict__ block_low,
-                                                     int32_t* __restrict__ counts, int32_t n_tiles) {
+                                                     int32_t* __restrict__ counts, int32_t n_tiles,
+                                                     uint32_t* err_init, int32_t* tickets_init) {
   __shared__ int32_t s_max[kRadixWaves], s_tail[kRadixWaves], s_low[kRadixWaves];
+  // The error word and the scans' ticket counters start at zero for the
+  // kernels after this one (when no k_dmax follows to do it).
+  if (blockIdx.x == 0 && err_init != nullptr) {
+    if (threadIdx.x == 0) err_init[0] = 0;
+    if (threadIdx.x < kMaxChainedScans) tickets_init[threadIdx.x] = 0;
+  }
   __shared__ uint32_t s_err[kRadixWaves];
   __shared__ int32_t cnt[kRadixWaves][kRadixBins];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -317,28 +324,34 @@ __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
   }
 }
 
+// Per-workgroup results of k_degree and where their reduction goes.
+struct DegreeBlocks {
+  const int32_t* block_max;
+  const uint32_t* block_err;
+  const int32_t* block_tail;
+  const int32_t* block_low;
+  int32_t nb;
+  int32_t* dmax;
+  uint32_t* err;
+  PlanSummary* host_sum;
+};
+
 // Maximum of the per-workgroup maxima, sums of their tail-row counts and
-// lower nonzeros, and OR of their error flags (one workgroup of
-// kScanTopThreads). It is the first writer of the plan's error
-// word and maximum degree (nb = 0: both become 0), so no clearing kernel runs
-// before it; every later kernel reads or ORs into them.
-__global__ __launch_bounds__(kScanTopThreads) void k_dmax(const int32_t* __restrict__ block_max,
-                                                          const uint32_t* __restrict__ block_err,
-                                                          const int32_t* __restrict__ block_tail,
-                                                          const int32_t* __restrict__ block_low,
-                                                          int32_t nb, int32_t* dmax, uint32_t* err,
-                                                          PlanSummary* host_sum, int32_t* tickets) {
-  if (threadIdx.x < kMaxChainedScans) tickets[threadIdx.x] = 0;  // the plan's scans start here
-  __shared__ int32_t s_max[kScanTopThreads / 64], s_tail[kScanTopThreads / 64],
-      s_low[kScanTopThreads / 64];
-  __shared__ uint32_t s_err[kScanTopThreads / 64];
+// lower nonzeros, and OR of their error flags, by a workgroup of T threads;
+// written to the plan (the error word by OR, as other workgroups of the
+// calling kernel may raise flags meanwhile) and to pinned host memory,
+// followed by the host's ready flag.
+template <int T>
+__device__ inline void reduce_degree_blocks(const DegreeBlocks& a) {
+  __shared__ int32_t s_max[T / 64], s_tail[T / 64], s_low[T / 64];
+  __shared__ uint32_t s_err[T / 64];
   int32_t m = 0, c = 0, l = 0;
   uint32_t e = 0;
-  for (int32_t i = threadIdx.x; i < nb; i += kScanTopThreads) {
-    m = max(m, block_max[i]);
-    c += block_tail[i];
-    l += block_low[i];
-    e |= block_err[i];
+  for (int32_t i = threadIdx.x; i < a.nb; i += T) {
+    m = max(m, a.block_max[i]);
+    c += a.block_tail[i];
+    l += a.block_low[i];
+    e |= a.block_err[i];
   }
   m = wave_max(m);
   c = wave_sum(c);
@@ -354,21 +367,32 @@ __global__ __launch_bounds__(kScanTopThreads) void k_dmax(const int32_t* __restr
   if (threadIdx.x == 0) {
     int32_t t = 0, tc = 0, tl = 0;
     uint32_t f = 0;
-    for (int w = 0; w < kScanTopThreads / 64; ++w) {
+    for (int w = 0; w < T / 64; ++w) {
       t = max(t, s_max[w]);
       tc += s_tail[w];
       tl += s_low[w];
       f |= s_err[w];
     }
-    dmax[0] = t;
-    err[0] = f;
-    host_sum->max_deg = t;
-    host_sum->n_tail = tc;
-    host_sum->nnz_low = tl;
+    a.dmax[0] = t;
+    if (f) atomicOr(a.err, f);
+    a.host_sum->max_deg = t;
+    a.host_sum->n_tail = tc;
+    a.host_sum->nnz_low = tl;
     __threadfence_system();
-    host_sum->dmax_ready = 1;
+    a.host_sum->dmax_ready = 1;
     __threadfence_system();
   }
+}
+
+// The reduction in a kernel of its own (one workgroup of kScanTopThreads). It
+// is the first writer of the plan's error word and maximum degree (nb = 0:
+// both become 0) when k_degree did not clear them, and clears the scans'
+// ticket counters.
+__global__ __launch_bounds__(kScanTopThreads) void k_dmax(DegreeBlocks a, int32_t* tickets) {
+  if (tickets && threadIdx.x < kMaxChainedScans) tickets[threadIdx.x] = 0;  // the plan's scans
+  if (threadIdx.x == 0) a.err[0] = 0;
+  __syncthreads();
+  reduce_degree_blocks<kScanTopThreads>(a);
 }
 
 // Buffers of the radix passes: pass p (if it runs) writes slot (need - 1 - p) % 2
@@ -655,7 +679,7 @@ __device__ inline void publish(unsigned long long* w, uint32_t state, uint32_t e
 __global__ __launch_bounds__(kThreads) void k_scan_chained(
     const int32_t* __restrict__ in, int64_t n, int32_t* __restrict__ out, int32_t* total_out,
     unsigned long long* status, int32_t* ticket, uint32_t epoch, uint32_t* err,
-    const int32_t* gate, int gate_pass) {
+    const int32_t* gate, int gate_pass, DegreeBlocks db) {
   if (failed(err) || gate_closed(gate, gate_pass)) return;
   __shared__ int32_t tile[kScanBlock + kScanBlock / 32];
   __shared__ int32_t s_t, s_base;
@@ -724,6 +748,9 @@ __global__ __launch_bounds__(kThreads) void k_scan_chained(
     if (lane == 0) s_base = prefix;
   }
   __syncthreads();
+  // With db given, the first tile (no look-back to wait for) also reduces
+  // k_degree's per-workgroup results, in place of a k_dmax launch.
+  if (t == 0 && db.dmax != nullptr) reduce_degree_blocks<kThreads>(db);
   run += s_base;
 #pragma unroll
   for (int k = 0; k < kScanItems; ++k) {
@@ -1489,10 +1516,22 @@ uint32_t next_scan_epoch() {
   return e;
 }
 
+// With db (dmax non-null), the scan also performs k_degree's reduction: in
+// its first tile when the scan runs in one pass, else by a k_dmax launch
+// before it.
 int scan_exclusive(const int32_t* in, int64_t n, int32_t* out, int32_t* total, int32_t* partials,
                    const uint32_t* err, hipStream_t st, const int32_t* gate = nullptr,
-                   int gate_pass = 0, ChainedScans* chain = nullptr) {
+                   int gate_pass = 0, ChainedScans* chain = nullptr, DegreeBlocks db = {}) {
   if (n > kScanMaxN) return fail(AGCN_ERR_UNSUPPORTED, "scan longer than the supported maximum");
+  const unsigned nb_tiles = n > 0 ? grid_for(n, kScanBlock) : 0;
+  const bool fused = db.dmax != nullptr && chain && chain->next < kMaxChainedScans &&
+                     n > kScanSingleMax && (int64_t)nb_tiles <= chain->capacity &&
+                     nb_tiles <= kChainedMaxTiles;
+  if (db.dmax != nullptr && !fused) {
+    k_dmax<<<1, kScanTopThreads, 0, st>>>(db, chain ? chain->tickets : nullptr);
+    if (int rc = check_launch("k_dmax")) return rc;
+    db = DegreeBlocks{};
+  }
   if (n == 0) {
     if (total) k_set<<<1, 64, 0, st>>>(total, 0);
     return check_launch("k_set");
@@ -1509,7 +1548,7 @@ int scan_exclusive(const int32_t* in, int64_t n, int32_t* out, int32_t* total, i
       nb <= kChainedMaxTiles) {
     k_scan_chained<<<nb, kThreads, 0, st>>>(in, n, out, total, chain->status,
                                             chain->tickets + chain->next, next_scan_epoch(),
-                                            const_cast<uint32_t*>(err), gate, gate_pass);
+                                            const_cast<uint32_t*>(err), gate, gate_pass, db);
     ++chain->next;
     return check_launch("k_scan_chained");
   }
@@ -1654,13 +1693,13 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   int32_t* blow = bmax + 3 * (n_deg_blocks + 1);
   if (n > 0)
     k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, bmax, berr,
-                                                         btail, blow, nullptr, 0);
+                                                         btail, blow, nullptr, 0, nullptr, nullptr);
   ChainedScans chain;
   chain.status = reinterpret_cast<unsigned long long*>(b + o_status);
   chain.capacity = n_partials;
   chain.tickets = reinterpret_cast<int32_t*>(b + o_tickets);
-  k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, berr, btail, blow, (int32_t)n_deg_blocks, dmax, err,
-                                        dsum, chain.tickets);
+  k_dmax<<<1, kScanTopThreads, 0, st>>>(
+      DegreeBlocks{bmax, berr, btail, blow, (int32_t)n_deg_blocks, dmax, err, dsum}, chain.tickets);
   if (n > 0) k_wl_groups<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, deg, Z, ng, err);
   const unsigned cgrid = (unsigned)std::min<int64_t>(grid_for(std::max(nnz, n + 1), kThreads), 65536);
   k_wl_copy<<<cgrid, kThreads, 0, st>>>((int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals,
@@ -1773,16 +1812,18 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   int32_t* blow = bmax + 3 * (n_deg_blocks + 1);
   // The short sort needs every hub row in the tail (DB >= kTailKey).
   const bool short_sort = n > 0 && DB >= kTailKey;
-  if (n > 0)
-    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>(
-        (int32_t)n, nnz, d_rowptr, deg, bmax, berr, btail, blow, short_sort ? counts : nullptr,
-        (int32_t)n_tiles);
   ChainedScans chain;
   chain.status = reinterpret_cast<unsigned long long*>(b + o_status);
   chain.capacity = n_partials;
   chain.tickets = reinterpret_cast<int32_t*>(b + o_tickets);
-  k_dmax<<<1, kScanTopThreads, 0, st>>>(bmax, berr, btail, blow, (int32_t)n_deg_blocks, dmax, err,
-                                        dsum, chain.tickets);
+  const DegreeBlocks dblocks{bmax, berr, btail, blow, (int32_t)n_deg_blocks, dmax, err, dsum};
+  // With the short sort, k_degree clears the error word and the tickets and
+  // the scan of its counts does the reduction (or launches k_dmax).
+  if (n > 0)
+    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>(
+        (int32_t)n, nnz, d_rowptr, deg, bmax, berr, btail, blow, short_sort ? counts : nullptr,
+        (int32_t)n_tiles, short_sort ? err : nullptr, short_sort ? chain.tickets : nullptr);
+  if (!short_sort) k_dmax<<<1, kScanTopThreads, 0, st>>>(dblocks, chain.tickets);
   if ((rc = check_launch("k_degree"))) return rc;
   const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
   bool short_done = false, have_max = false;
@@ -1791,7 +1832,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     // Pass one of the short sort; the maximum degree and the tail size reach
     // the host meanwhile.
     if ((rc = scan_exclusive(counts, n_tiles * kRadixBins, counts, nullptr, partials, err, st,
-                             nullptr, 0, &chain)))
+                             nullptr, 0, &chain, dblocks)))
       return rc;
     k_scatter_low<<<rgrid, kThreads, 0, st>>>((int32_t)n, deg, counts, (int32_t)n_tiles, keys,
                                               p->perm, p->rowptr_s, keys2, ids2, err);
