@@ -289,11 +289,7 @@ __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
     m = max(m, d);
     tail += d >= kTailKey;
     low += d < kTailKey ? d : 0;
-    if (counts) {
-      const uint32_t key = (uint32_t)min(d, kTailKey);
-      const uint64_t peers = match_digit(key, valid);
-      if (valid && __popcll(peers & __lanemask_lt()) == 0) cnt[wave][key] += __popcll(peers);
-    }
+    if (counts && valid) atomicAdd(&cnt[wave][min(d, kTailKey)], 1);  // counts only: any order
   }
   if (counts && tile < n_tiles)
     for (int d = lane; d < kRadixBins; d += 64) counts[(int64_t)d * n_tiles + tile] = cnt[wave][d];
@@ -431,9 +427,7 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(int32_t n, RadixBufs bu
   for (int j = 0; j < kRadixItems; ++j) {
     const bool valid = base + (int64_t)j * 64 + lane < n;
     const uint32_t digit = (((uint32_t)k[j]) >> shift) & 0xFFu;
-    const uint64_t peers = match_digit(digit, valid);
-    // The lowest lane of each digit group adds the group's size (one writer per digit).
-    if (valid && __popcll(peers & __lanemask_lt()) == 0) cnt[wave][digit] += __popcll(peers);
+    if (valid) atomicAdd(&cnt[wave][digit], 1);  // counts only: any order
   }
   for (int d = lane; d < kRadixBins; d += 64) counts[(int64_t)d * n_tiles + tile] = cnt[wave][d];
 }
