@@ -1822,18 +1822,35 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
   bool short_done = false, have_max = false;
   int32_t md = 0;
-  if (short_sort) {
-    // Pass one of the short sort; the maximum degree and the tail size reach
-    // the host meanwhile.
+  // When the counts scan takes several launches (graphs of over 512 K rows),
+  // the reduction runs first and the host reads the tail size before
+  // queueing the short sort's first pass, which a tail over the cap would
+  // waste; otherwise the first tile of the scan does the reduction and the
+  // read-back arrives while the pass runs.
+  const bool reduce_first =
+      short_sort && n_tiles * kRadixBins > (int64_t)kChainedMaxTiles * kScanBlock;
+  bool take_short = short_sort;
+  if (reduce_first) {
+    k_dmax<<<1, kScanTopThreads, 0, st>>>(dblocks, chain.tickets);
+    if ((rc = check_launch("k_dmax"))) return rc;
+    if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
+    md = hs->max_deg;
+    have_max = true;
+    take_short = hs->n_tail >= 0 && hs->n_tail <= tail_cap_setting();
+  }
+  if (take_short) {
+    // Pass one of the short sort.
     if ((rc = scan_exclusive(counts, n_tiles * kRadixBins, counts, nullptr, partials, err, st,
-                             nullptr, 0, &chain, dblocks)))
+                             nullptr, 0, &chain, reduce_first ? DegreeBlocks{} : dblocks)))
       return rc;
     k_scatter_low<<<rgrid, kThreads, 0, st>>>((int32_t)n, deg, counts, (int32_t)n_tiles, keys,
                                               p->perm, p->rowptr_s, keys2, ids2, err);
     if ((rc = check_launch("k_scatter_low"))) return rc;
-    if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
-    md = hs->max_deg;
-    have_max = true;
+    if (!have_max) {
+      if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
+      md = hs->max_deg;
+      have_max = true;
+    }
     const int32_t m = hs->n_tail;
     if (m >= 0 && m <= tail_cap_setting()) {
       int bits = 0;

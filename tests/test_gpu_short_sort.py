@@ -110,3 +110,17 @@ def test_invalid_csr_through_the_short_sort():
     p = _plan(g)                      # and a valid plan right after
     assert_plan_matches_oracle(p, g)
     p.destroy()
+
+
+def test_short_sort_on_a_graph_whose_counts_scan_is_multi_launch():
+    # Over 512 K rows: the reduction runs before the short sort's first pass,
+    # whose tail (here 700 rows) is read back first.
+    rng = np.random.default_rng(41)
+    n = 600_000
+    deg = rng.integers(0, 20, size=n)
+    deg[rng.choice(n, 700, replace=False)] = rng.integers(255, 2000, size=700)
+    g = graphgen.random_csr(n, 200_000, deg, seed=42)
+    p0, p1 = _both(g)
+    _spmm_check(p0, g, 16)
+    p0.destroy()
+    p1.destroy()
