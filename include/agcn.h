@@ -119,8 +119,9 @@ void agcn_default_params(agcn_plan_params* p);
  * permutation, sorted CSR copy, metadata); the inputs may be freed once the
  * call returns (every kernel that reads them has finished by then). Work is
  * ordered on `stream`. The call waits on the host, by polling pinned memory,
- * for two results the device writes there: the maximum degree and the number
- * of metadata entries. The plan's last kernels may still run on `stream` when
+ * for two results the device writes there: the maximum degree (with the
+ * number of rows of degree >= 255, which chooses between the plan's two
+ * degree sorts) and the number of metadata entries. The plan's last kernels may still run on `stream` when
  * it returns; later work on that stream comes after them, and agcn_spmm* on
  * another stream waits for them. The warp-level plan (AGCN_PLAN_WARP_LEVEL)
  * synchronises `stream` instead. `stream` must remain valid until the plan is
@@ -143,7 +144,10 @@ void agcn_default_params(agcn_plan_params* p);
  * memory allocation attempt of each agcn_plan_create call on the calling
  * thread fail with OUT_OF_MEMORY; AGCN_TEST_FAIL_ORDER_SORT=1 raises the
  * internal-error flag before the hub-chunk launch-order sort, which then
- * keeps the plain heaviest-first order (the plan stays valid). */
+ * keeps the plain heaviest-first order (the plan stays valid);
+ * AGCN_TEST_TAIL_CAP=c lowers to c the number of rows of degree >= 255 that
+ * the short degree sort takes (-1: none, so every plan takes the multi-pass
+ * sort; the result is the same stable sort either way). */
 int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t nnz,
                      const int32_t* d_rowptr, const int32_t* d_colidx, const float* d_vals,
                      const agcn_plan_params* params, void* stream);
