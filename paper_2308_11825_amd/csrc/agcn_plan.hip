@@ -5,22 +5,26 @@
 // and the tail size, and for the partition's summary). With W * Z >= 255 and a
 // tail of at most kTailCap rows (the short sort):
 //   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
-//                   per-workgroup maximum degree, tail size and error flags;
-//                   per-tile histograms of min(deg, 255)
-//   k_dmax          maximum degree and tail size (one workgroup), written to
-//                   pinned host memory
-//   scan            bin starts of every (digit, tile)
+//                   per-workgroup maximum degree, tail size, lower nonzeros and
+//                   error flags; per-tile histograms of min(deg, 255); clears
+//                   the error word and the scans' tickets
+//   scan            bin starts of every (digit, tile); its first tile also
+//                   reduces k_degree's per-workgroup results and writes the
+//                   maximum degree and the tail size to pinned host memory
+//                   (graphs whose scan takes several launches run k_dmax for
+//                   that first, and the host reads the tail size before the
+//                   scan)
 //   k_scatter_low   stable scatter by min(deg, 255): rows of degree < 255 reach
 //                   their final sorted place, with their sorted row pointer in
 //                   closed form; the tail (degree >= 255) follows in row order
-//   k_tail          one workgroup: the tail sorted by degree in LDS, its row
+//   k_tail_relayout workgroup 0: the tail sorted by degree in LDS, its row
 //                   pointers, the class starts, the segment scan of Alg. 2 and
-//                   the summary
+//                   the summary; the others: the sorted CSR of the rows below
+//                   the tail (column indices checked against n_cols)
 //   k_relayout_fill the partition's int4 entries {deg, loc, row, info} in
 //                   Alg. 2's order, the first chunk of each hub row and the
 //                   launch order (hub chunks, then the other entries heaviest
-//                   first), side by side with the sorted CSR copy (column
-//                   indices checked against n_cols)
+//                   first), side by side with the sorted CSR of the tail's rows
 //   k_publish       the summary's error word and done flag
 // Otherwise (the multi-pass sort):
 //   radix passes    stable LSD radix sort of row ids by degree, 8-bit digits:
@@ -536,12 +540,10 @@ __global__ __launch_bounds__(kThreads) void k_scatter_low(
   }
 }
 
-// Information the short sort's tail kernel leaves for k_relayout_fill.
+// What the tail's workgroup leaves for k_relayout_fill: the number of
+// partition segments (degree classes 0..DB and one per hub row).
 struct TailInfo {
-  int32_t n_segments;  // degree classes 0..DB and one segment per hub row
-  int32_t n_entries;
-  int32_t hub_first_entry;
-  int32_t hub_first_row;
+  int32_t n_segments;
 };
 
 // --- exclusive scan of int32 -------------------------------------------------
@@ -1107,7 +1109,8 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
 //     above (DB >= kTailKey, so every hub row is a tail row);
 //   - the segment scan of the partition (Alg. 2): ceil(count / block_rows)
 //     entries for each degree class, ceil(deg / H) chunks for each hub row;
-//   - the partition's summary, in pinned host memory and in `info`.
+//   - the partition's summary, in pinned host memory (the segment count in
+//     `info`).
 struct TailArgs {
   int32_t n, nnz, T0, passes, width, W, Z, DB, H;
   const int32_t* tail_keys;  // [T0, n): the tail's degrees and rows in row order
@@ -1312,9 +1315,6 @@ __device__ inline void tail_block(const TailArgs& a, int32_t* lds) {
     seg[S] = carry;
     const int32_t hfe = S > DB + 1 ? s_hub_first_entry : carry;
     a.info->n_segments = S;
-    a.info->n_entries = carry;
-    a.info->hub_first_entry = hfe;
-    a.info->hub_first_row = hub_first_row;
     a.sum->n_entries = carry;
     a.sum->hub_first_entry = hfe;
     a.sum->n_hub_rows = n - hub_first_row;
