@@ -124,3 +124,20 @@ def test_short_sort_on_a_graph_whose_counts_scan_is_multi_launch():
     _spmm_check(p0, g, 16)
     p0.destroy()
     p1.destroy()
+
+
+def test_every_row_in_the_tail_and_none():
+    rng = np.random.default_rng(51)
+    # every row of degree >= 255: no rows below the tail, no lower nonzeros
+    deg = rng.integers(255, 700, size=2000)
+    g = graphgen.random_csr(2000, 3000, deg, seed=52)
+    p0, p1 = _both(g)
+    assert p0.stats.n_hub_rows == int((deg > 512).sum())
+    _spmm_check(p0, g, 32)
+    p0.destroy()
+    p1.destroy()
+    # no row of degree >= 255, W * Z = 4096 (class starts up to 4097)
+    deg = rng.integers(0, 255, size=5000)
+    g = graphgen.random_csr(5000, 3000, deg, seed=53)
+    for p in _both(g, max_block_waves=16, max_wave_nzs=256):
+        p.destroy()
