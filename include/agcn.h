@@ -116,8 +116,10 @@ void agcn_default_params(agcn_plan_params* p);
  *
  * Inputs: d_rowptr[n_rows + 1], d_colidx[nnz], d_vals[nnz] on the current
  * device; params NULL = defaults. The plan copies what it needs (sorted
- * permutation, sorted CSR copy, metadata); the inputs may be freed once the
- * call returns (every kernel that reads them has finished by then). Work is
+ * permutation, sorted CSR copy, metadata). The call's last kernel may still
+ * read the inputs when it returns: keep them unchanged until the work it
+ * queued on `stream` has run (free or overwrite them in `stream`'s order, or
+ * after synchronising it). Work is
  * ordered on `stream`. The call waits on the host, by polling pinned memory,
  * for two results the device writes there: the maximum degree (with the
  * number of rows of degree >= 255, which chooses between the plan's two
@@ -270,7 +272,10 @@ int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* out);
  * in the sorted CSR; first sorted row; for deg <= deg_bound
  * warp_nzs << 16 | rows, else the chunk's nnz). AGCN_PLAN_WARP_LEVEL plans:
  * perm is the identity, the CSR is the input's, and h_meta holds one
- * {row, first nnz, nnz count, 0} per group. */
+ * {row, first nnz, nnz count, 0} per group. Errors: INVALID_ARGUMENT (NULL
+ * plan, another current device), HIP (including an internal consistency
+ * check of the plan's last relayout, which runs after agcn_plan_create
+ * returns: a row order that is not sorted). */
 int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s,
                      int32_t* h_colidx_s, float* h_vals_s, int32_t* h_meta);
 

@@ -299,6 +299,11 @@ class Plan:
             self._handle = agcn_plan_create(self.n_rows, self.n_cols, self.nnz, rowptr.data_ptr(),
                                             colidx.data_ptr() if self.nnz else None,
                                             vals.data_ptr() if self.nnz else None, prm, st)
+            # The plan's last kernel may still read the inputs: on another
+            # stream, torch's allocator must not reuse their memory before it.
+            if stream is not None:
+                for t in (rowptr, colidx, vals):
+                    t.record_stream(stream)
         self.stats = agcn_plan_info(self._handle)
         self._ws = {}
 

@@ -77,11 +77,19 @@ int hip_fail(hipError_t e, const char* what) {
 // which synchronises the device -- each time. A destroyed plan's block stays
 // cached, one block per device, and the next plan on that device reuses it
 // when it fits without wasting more than half of it. The block travels with
-// events marking its previous owner's last work on every stream; the reusing
-// plan's stream waits on those of the other streams (on its own stream, stream
-// order already does it, and a wait would add a barrier packet, around which
-// the GPU idles for microseconds), so nothing blocks on the host.
+// events marking its previous owner's last work on the streams its executes
+// ran on; the reusing plan's stream waits on those of the other streams (on
+// its own stream, stream order already does it, and a wait would add a
+// barrier packet, around which the GPU idles for microseconds), so nothing
+// blocks on the host. The previous owner's own stream has no event (the same
+// marker cost at every release): a plan on another stream synchronises the
+// device before reusing the block.
 namespace {
+// Events that only order device work (another stream's wait) or precede a
+// hipFree: a device-scope release, without the system-scope cache writeback
+// that makes the GPU idle for microseconds around the marker.
+constexpr unsigned kOrderEventFlags = hipEventDisableTiming | hipEventReleaseToDevice;
+
 struct CachedBlock {
   void* ptr = nullptr;
   size_t bytes = 0;
@@ -92,10 +100,16 @@ std::map<int, CachedBlock> g_cache;
 
 // Frees a block no plan will reuse (the caller has made its device current).
 void free_block(CachedBlock& b) {
+  bool sync = false;
   for (const StreamEvent& se : b.pending) {
+    if (se.ev == nullptr) {
+      sync = true;
+      continue;
+    }
     (void)hipEventSynchronize(se.ev);
     (void)hipEventDestroy(se.ev);
   }
+  if (sync) (void)hipDeviceSynchronize();
   b.pending.clear();
   if (b.ptr) (void)hipFree(b.ptr);
   b.ptr = nullptr;
@@ -122,13 +136,19 @@ int device_alloc(int device, size_t bytes, hipStream_t stream, void** out, size_
     }
   }
   if (reuse.ptr != nullptr) {
+    bool sync = false;
     for (const StreamEvent& se : reuse.pending) {
+      if (se.ev == nullptr) {  // no event: stream order, or the whole device
+        sync = sync || se.stream != stream;
+        continue;
+      }
       if (se.stream != stream && hipStreamWaitEvent(stream, se.ev, 0) != hipSuccess) {
         (void)hipGetLastError();
         (void)hipEventSynchronize(se.ev);
       }
       (void)hipEventDestroy(se.ev);
     }
+    if (sync) (void)hipDeviceSynchronize();
     *out = reuse.ptr;
     *got = reuse.bytes;
     return AGCN_OK;
@@ -221,7 +241,7 @@ void note_use(agcn_plan* p, hipStream_t stream) {
     }
   }
   hipEvent_t ev = nullptr;
-  if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess ||
+  if (hipEventCreateWithFlags(&ev, kOrderEventFlags) != hipSuccess ||
       hipEventRecord(ev, stream) != hipSuccess) {
     (void)hipGetLastError();
     if (ev) (void)hipEventDestroy(ev);
@@ -267,25 +287,11 @@ static void plan_free(agcn_plan* p) {
     else (void)hipEventDestroy(p->ready);
   }
   for (auto& u : p->uses) pending.push_back({u.second, u.first});
-  // Calls on the plan's own stream record no event of their own: one event
-  // recorded now on that stream follows all of them (and the plan's kernels).
-  if (p->base != nullptr) {
-    int prev = 0;
-    hipEvent_t ev = nullptr;
-    if (agcn::with_device(p->device, &prev) == AGCN_OK) {
-      if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess &&
-          hipEventRecord(ev, p->stream) == hipSuccess) {
-        pending.push_back({ev, p->stream});
-      } else {
-        (void)hipGetLastError();
-        if (ev) (void)hipEventDestroy(ev);
-        p->sync_on_release = true;
-      }
-      if (prev != p->device) (void)hipSetDevice(prev);
-    } else {
-      p->sync_on_release = true;
-    }
-  }
+  // The plan's own stream gets no event: recording one queues a marker
+  // packet, around which the GPU idles for microseconds between this plan's
+  // work and the next call's. A later plan on that stream follows in stream
+  // order; one on another stream, or a hipFree, synchronises the device.
+  if (p->base != nullptr) pending.push_back({nullptr, p->stream});
   if (p->sync_on_release) {
     int prev = 0;
     if (agcn::with_device(p->device, &prev) == AGCN_OK) {
@@ -625,6 +631,14 @@ int agcn_plan_export(agcn_plan_t plan, int32_t* h_perm, int32_t* h_rowptr_s, int
   if (int rc = agcn::plan_ready_event(plan, &ready)) return rc;
   if ((he = hipEventSynchronize(ready)) != hipSuccess)
     return agcn::hip_fail(he, "hipEventSynchronize(plan ready)");
+  // The short sort's last relayout runs after agcn_plan_create returned; its
+  // window check (never raised for a sorted row order) is reported here.
+  if (plan->err_word != nullptr) {
+    uint32_t e = 0;
+    if ((he = hipMemcpy(&e, plan->err_word, sizeof(e), hipMemcpyDeviceToHost)) != hipSuccess)
+      return agcn::hip_fail(he, "hipMemcpy(export error word)");
+    if (e & agcn::kErrRelayout) return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
+  }
   for (const Item& it : items) {
     if (it.dst == nullptr || it.bytes == 0) continue;
     he = hipMemcpy(it.dst, it.src, it.bytes, hipMemcpyDeviceToHost);

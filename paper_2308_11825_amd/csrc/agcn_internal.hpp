@@ -20,6 +20,9 @@ enum : uint32_t {
   kErrRowptrOrder = 1u << 1,   // rowptr decreases
   kErrRowptrEnd = 1u << 2,     // rowptr[n_rows] != nnz
   kErrColumn = 1u << 3,        // a column index outside [0, n_cols)
+  kErrInternal = 1u << 8,      // a consistency check of the plan's own kernels
+  kErrRelayout = 1u << 9,      // the relayout's window check (a row order that is not
+                               // sorted); may be raised after the summary was read
 };
 
 // Facts the device computes while partitioning, written into pinned host
@@ -64,6 +67,7 @@ struct agcn_plan {
   int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
   bool hub_wide = false;            // hub chunks of long rows launched in column order
   int32_t* group_off = nullptr;     // warp-level plans: [n_rows + 1] first group of each row
+  uint32_t* err_word = nullptr;     // the plan kernels' error flags (device)
   hipEvent_t ready = nullptr;       // the plan's kernels done (created with the plan,
                                     // recorded on first need: plan_ready_event; use_mu)
   bool ready_recorded = false;
@@ -126,7 +130,8 @@ int noalloc_scratch(int device, float** out);
 // Dynamic LDS bytes the SpMM kernel needs for a plan (worst case over F).
 size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz);
 
-// An event and the stream it was recorded on.
+// An event and the stream it was recorded on. ev == nullptr stands for the
+// work a released plan queued on its own stream, marked by no event.
 struct StreamEvent {
   hipEvent_t ev;
   hipStream_t stream;
@@ -136,8 +141,9 @@ struct StreamEvent {
 // the per-device cache (*got receives its size, >= bytes); `stream` then
 // waits (device-side) on the events that mark the previous owner's last work
 // on other streams; on `stream` itself its own order already puts that work
-// first. device_release keeps the block cached (one per device) with those
-// events and takes ownership of them; it does not block.
+// first. Work marked by no event on another stream makes it synchronise the
+// device instead. device_release keeps the block cached (one per device) with
+// those entries and takes ownership of the events; it does not block.
 int device_alloc(int device, size_t bytes, hipStream_t stream, void** out, size_t* got);
 void device_release(int device, void* ptr, size_t bytes, std::vector<StreamEvent> pending);
 

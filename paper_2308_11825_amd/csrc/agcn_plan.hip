@@ -1,31 +1,36 @@
 // Device-side preprocessing: degree sort and block-level partition
 // (Sec. III-C "Degree Sorting" and "Block-level Partition", Alg. 1 and Alg. 2).
 //
-// Pipeline (all on one stream; the host waits twice: for the maximum degree
-// and the tail size, and for the partition's summary). With W * Z >= 255 and a
-// tail of at most kTailCap rows (the short sort):
+// Pipeline (all on one stream; the host reads back the maximum degree and the
+// tail size, which decide between the two sorts, and the partition's summary,
+// while the GPU keeps running). With W * Z >= 255 and a tail of at most
+// kTailCap rows (the short sort):
 //   k_degree        deg[i] = rowptr[i+1] - rowptr[i]; validates the row pointer;
 //                   per-workgroup maximum degree, tail size, lower nonzeros and
 //                   error flags; per-tile histograms of min(deg, 255); clears
-//                   the error word and the scans' tickets
+//                   the error word and the scans' tickets; further workgroups
+//                   check the column indices against n_cols
 //   scan            bin starts of every (digit, tile); its first tile also
-//                   reduces k_degree's per-workgroup results and writes the
-//                   maximum degree and the tail size to pinned host memory
-//                   (graphs whose scan takes several launches run k_dmax for
-//                   that first, and the host reads the tail size before the
-//                   scan)
+//                   reduces k_degree's per-workgroup results (every input error
+//                   is then known) and writes the maximum degree, the tail size
+//                   and the lower nonzeros to the device and to pinned host
+//                   memory (graphs whose scan takes several launches run k_dmax
+//                   for that first, and the host reads the tail size before
+//                   the scan)
 //   k_scatter_low   stable scatter by min(deg, 255): rows of degree < 255 reach
 //                   their final sorted place, with their sorted row pointer in
 //                   closed form; the tail (degree >= 255) follows in row order
 //   k_tail_relayout workgroup 0: the tail sorted by degree in LDS, its row
 //                   pointers, the class starts, the segment scan of Alg. 2 and
-//                   the summary; the others: the sorted CSR of the rows below
-//                   the tail (column indices checked against n_cols)
+//                   the summary with the host's done flag; the others: the
+//                   sorted CSR of the rows below the tail
 //   k_relayout_fill the partition's int4 entries {deg, loc, row, info} in
 //                   Alg. 2's order, the first chunk of each hub row and the
 //                   launch order (hub chunks, then the other entries heaviest
-//                   first), side by side with the sorted CSR of the tail's rows
-//   k_publish       the summary's error word and done flag
+//                   first), side by side with the sorted CSR of the tail's rows;
+//                   it may still run when agcn_plan_create returns
+// The last two are queued without waiting for the read-back: they read the
+// tail size from the device and return at once if it is over the cap.
 // Otherwise (the multi-pass sort):
 //   radix passes    stable LSD radix sort of row ids by degree, 8-bit digits:
 //                   k_radix_hist -> exclusive scan -> k_radix_scatter. Buffers
@@ -59,6 +64,7 @@
 // of the group counts, k_wl_fill (one {row, first nnz, count, 0} per group)
 // and k_wl_summary.
 #include <algorithm>
+#include <chrono>
 #include <climits>
 #include <cstdlib>
 #include <atomic>
@@ -105,8 +111,6 @@ constexpr int32_t kTailCap = kTailThreads * kTailItems;  // 16384 rows
 // Relayout tile (sorted nnz positions per workgroup).
 constexpr int kRelayItems = 8;
 constexpr int kRelayTile = kThreads * kRelayItems;  // 2048
-
-constexpr uint32_t kErrInternal = 1u << 8;
 
 // Launch-order sort of hub chunks: minimum mean chunks per hub row.
 constexpr int kOrderMinChunks = 8;
@@ -243,12 +247,56 @@ __global__ void k_raise(uint32_t* err, uint32_t bits) {
   if (threadIdx.x == 0 && blockIdx.x == 0) atomicOr(err, bits);
 }
 
-// Step (1) of the degree sort, plus the row-pointer checks. One workgroup
-// covers kDegRows rows, each wave the kRadixTile consecutive rows of one radix
-// tile, and writes: the degrees; the workgroup's maximum degree, error flags
-// and number of rows of degree >= kTailKey; and, when `counts` is given, each
-// tile's histogram of min(degree, kTailKey) in the digit-major layout of
-// k_radix_hist (the counts of the first pass of the short sort).
+// The column indices are checked against n_cols by workgroups that k_degree
+// carries past its own: chunk c of the input's colidx per workgroup, chunks a
+// multiple of this many entries. (Split between k_degree and k_scatter_low,
+// the check cost more in all.)
+constexpr int kColCheckItems = 8;
+constexpr int64_t kColCheckChunk = (int64_t)kThreads * kColCheckItems * 8;  // 16384
+constexpr int32_t kColCheckMaxBlocks = 2048;
+
+struct ColumnCheck {
+  const int32_t* colidx;
+  int64_t nnz, chunk;
+  int32_t n_cols;
+  int32_t c0;  // first chunk
+};
+
+// Error flag (kErrColumn or 0) of chunk c0 + c, by one workgroup of kThreads
+// (the result in thread 0).
+__device__ inline uint32_t check_chunk(const ColumnCheck& cc, int32_t c) {
+  __shared__ uint32_t s_bad[kThreads / 64];
+  const int64_t lo = (int64_t)(cc.c0 + c) * cc.chunk;
+  const int64_t hi = lo + cc.chunk < cc.nnz ? lo + cc.chunk : cc.nnz;
+  uint32_t bad = 0;
+  for (int64_t i = lo + threadIdx.x; i < hi; i += (int64_t)kThreads * kColCheckItems) {
+    int32_t col[kColCheckItems];
+#pragma unroll
+    for (int u = 0; u < kColCheckItems; ++u) {
+      const int64_t k = i + (int64_t)u * kThreads;
+      col[u] = k < hi ? cc.colidx[k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kColCheckItems; ++u)
+      bad |= (uint32_t)col[u] >= (uint32_t)cc.n_cols ? kErrColumn : 0u;
+  }
+  bad = wave_or(bad);
+  if ((threadIdx.x & 63) == 0) s_bad[threadIdx.x >> 6] = bad;
+  __syncthreads();
+  uint32_t f = 0;
+  if (threadIdx.x == 0)
+    for (int w = 0; w < kThreads / 64; ++w) f |= s_bad[w];
+  return f;
+}
+
+// Step (1) of the degree sort, plus the input checks. Workgroups [0, nb)
+// cover kDegRows rows each, each wave the kRadixTile consecutive rows of one
+// radix tile, and write: the degrees; the workgroup's maximum degree, error
+// flags and number of rows of degree >= kTailKey; and, when `counts` is given,
+// each tile's histogram of min(degree, kTailKey) in the digit-major layout of
+// k_radix_hist (the counts of the first pass of the short sort). Workgroup
+// nb + c checks the column indices of chunk c and writes its flag to
+// block_err[nb + c], which the reduction of the per-workgroup results reads.
 __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
                                                      const int32_t* __restrict__ rowptr,
                                                      int32_t* __restrict__ deg,
@@ -257,7 +305,13 @@ __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
                                                      int32_t* __restrict__ block_tail,
                                                      int32_t* __restrict__ block_low,
                                                      int32_t* __restrict__ counts, int32_t n_tiles,
-                                                     uint32_t* err_init, int32_t* tickets_init) {
+                                                     uint32_t* err_init, int32_t* tickets_init,
+                                                     int32_t nb, ColumnCheck cc) {
+  if ((int32_t)blockIdx.x >= nb) {  // uniform per workgroup
+    const uint32_t f = check_chunk(cc, blockIdx.x - nb);
+    if (threadIdx.x == 0) block_err[blockIdx.x] = f;
+    return;
+  }
   __shared__ int32_t s_max[kRadixWaves], s_tail[kRadixWaves], s_low[kRadixWaves];
   // The error word and the scans' ticket counters start at zero for the
   // kernels after this one (when no k_dmax follows to do it).
@@ -324,13 +378,16 @@ __global__ __launch_bounds__(kThreads) void k_degree(int32_t n, int64_t nnz,
   }
 }
 
-// Per-workgroup results of k_degree and where their reduction goes.
+// Per-workgroup results of k_degree and where their reduction goes: the
+// maximum degree, tail size and lower nonzeros to dmax[0], dmax[1], dmax[2]
+// and to pinned host memory.
 struct DegreeBlocks {
   const int32_t* block_max;
   const uint32_t* block_err;
   const int32_t* block_tail;
   const int32_t* block_low;
-  int32_t nb;
+  int32_t nb;      // degree workgroups
+  int32_t nb_err;  // error flags: nb, then one per column-check workgroup
   int32_t* dmax;
   uint32_t* err;
   PlanSummary* host_sum;
@@ -351,8 +408,8 @@ __device__ inline void reduce_degree_blocks(const DegreeBlocks& a) {
     m = max(m, a.block_max[i]);
     c += a.block_tail[i];
     l += a.block_low[i];
-    e |= a.block_err[i];
   }
+  for (int32_t i = threadIdx.x; i < a.nb_err; i += T) e |= a.block_err[i];
   m = wave_max(m);
   c = wave_sum(c);
   l = wave_sum(l);
@@ -374,6 +431,8 @@ __device__ inline void reduce_degree_blocks(const DegreeBlocks& a) {
       f |= s_err[w];
     }
     a.dmax[0] = t;
+    a.dmax[1] = tc;
+    a.dmax[2] = tl;
     if (f) atomicOr(a.err, f);
     a.host_sum->max_deg = t;
     a.host_sum->n_tail = tc;
@@ -545,6 +604,28 @@ __global__ __launch_bounds__(kThreads) void k_scatter_low(
 struct TailInfo {
   int32_t n_segments;
 };
+
+// The short sort's second half as the reduction of k_degree's results
+// decides it, read on the device, so that its launches need no read-back.
+struct TailShape {
+  bool take;         // the tail fits: these launches sort it (else they return at once)
+  int32_t m, T0;     // tail rows; its first sorted position
+  int32_t passes, width;  // LSD passes over degree - kTailKey
+  int64_t nnz_low;   // nonzeros of the rows below the tail
+};
+
+__device__ inline TailShape tail_shape(const int32_t* dmax, int32_t n, int32_t cap) {
+  TailShape s;
+  s.m = dmax[1];
+  s.nnz_low = dmax[2];
+  s.take = s.m >= 0 && s.m <= cap && s.m <= kTailCap;
+  s.T0 = n - s.m;
+  int bits = 0;
+  while (bits < 31 && (int64_t(1) << bits) <= (int64_t)dmax[0] - kTailKey) ++bits;
+  s.passes = (bits + 7) / 8;
+  s.width = s.passes > 0 ? (bits + s.passes - 1) / s.passes : 8;
+  return s;
+}
 
 // --- exclusive scan of int32 -------------------------------------------------
 
@@ -842,7 +923,7 @@ constexpr int kRelayLds = (kRelayTile + 1) + kRelayTile + (kRelayTile + kRelayTi
                           kThreads / 64 + 2;
 
 __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t n, int64_t nnz,
-                                     int32_t n_cols, const int32_t* __restrict__ rowptr,
+                                     const int32_t* __restrict__ rowptr,
                                      const int32_t* __restrict__ colidx,
                                      const float* __restrict__ vals,
                                      const int32_t* __restrict__ perm,
@@ -874,7 +955,7 @@ __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t
   const int32_t lo = active ? s_lo : 0;
   const int32_t nw = active ? s_hi - lo + 1 : 0;
   if (active && (nw > kRelayTile || nw < 1)) {  // cannot happen for a sorted row order
-    if (tid == 0) atomicOr(err, kErrInternal);
+    if (tid == 0) atomicOr(err, kErrRelayout);
     active = false;
   }
   if (active) {
@@ -905,7 +986,6 @@ __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t
     s_row[rpad(tid * kRelayItems + k)] = max(before, v[k]);
   __syncthreads();
   if (!active) return;  // no barrier below
-  uint32_t bad = 0;
 #pragma unroll
   for (int k = 0; k < kRelayItems; ++k) {
     const int j = k * kThreads + tid;
@@ -913,14 +993,10 @@ __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t
     if (e < e1) {
       const int32_t w = s_row[rpad(j)];
       const int64_t src = (int64_t)s_src[w] + (e - s_ptr[w]);
-      const int32_t c = colidx[src];
-      const float val = vals[src];
-      if ((uint32_t)c >= (uint32_t)n_cols) bad = kErrColumn;
-      colidx_s[e] = c;
-      vals_s[e] = val;
+      colidx_s[e] = colidx[src];
+      vals_s[e] = vals[src];
     }
   }
-  if (bad) atomicOr(err, bad);
 }
 
 // The error word as one workgroup sees it, read once (other workgroups may
@@ -935,13 +1011,13 @@ __device__ inline bool block_failed(const uint32_t* err) {
 }
 
 __global__ __launch_bounds__(kThreads) void k_relayout(
-    int32_t n, int64_t nnz, int32_t n_cols, const int32_t* __restrict__ rowptr,
+    int32_t n, int64_t nnz, const int32_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, const float* __restrict__ vals,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ rowptr_s,
     int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, uint32_t* err) {
   __shared__ int32_t lds[kRelayLds];
   if (block_failed(err)) return;
-  relayout_tile(blockIdx.x, true, threadIdx.x, n, nnz, n_cols, rowptr, colidx, vals, perm, rowptr_s,
+  relayout_tile(blockIdx.x, true, threadIdx.x, n, nnz, rowptr, colidx, vals, perm, rowptr_s,
                 colidx_s, vals_s, err, lds);
 }
 
@@ -1070,27 +1146,34 @@ __global__ __launch_bounds__(kThreads) void k_partition_fill(
 }
 
 // The last partition launch of the short-sort plan: workgroups [0, n_fill)
-// fill the partition from the tail workgroup's segment scan while the others
-// build the sorted CSR from tile `tile0` on (the tiles before it went with
-// the tail).
+// fill the partition from the tail workgroup's segment scan while the other
+// n_copy build the sorted CSR from the tile holding the tail's first nonzero
+// on (the tiles before it went with the tail), tile after tile. Returns at
+// once when the tail is over the cap (the multi-pass sort follows).
 __global__ __launch_bounds__(kThreads) void k_relayout_fill(
-    int32_t n_fill, int64_t tile0, int32_t n, int64_t nnz, int32_t n_cols,
-    const int32_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
-    const float* __restrict__ vals, const int32_t* __restrict__ perm,
-    const int32_t* __restrict__ rowptr_s, int32_t* __restrict__ colidx_s,
-    float* __restrict__ vals_s, const int32_t* __restrict__ deg_s, const int32_t* __restrict__ cls,
-    const int32_t* __restrict__ seg_off, const TailInfo* __restrict__ info, int32_t W, int32_t Z,
-    int32_t DB, int32_t H, int4* __restrict__ meta, int64_t cap, int32_t hub_ub,
-    int32_t* __restrict__ hub_chunk_off, int32_t* __restrict__ order, uint32_t* err) {
+    int32_t n_fill, int32_t n_copy, int32_t n, int64_t nnz, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ colidx, const float* __restrict__ vals,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ rowptr_s,
+    int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, const int32_t* __restrict__ deg_s,
+    const int32_t* __restrict__ cls, const int32_t* __restrict__ seg_off,
+    const TailInfo* __restrict__ info, int32_t W, int32_t Z, int32_t DB, int32_t H,
+    int4* __restrict__ meta, int64_t cap, int32_t hub_ub, int32_t* __restrict__ hub_chunk_off,
+    int32_t* __restrict__ order, const int32_t* __restrict__ dmax, int32_t tail_cap,
+    uint32_t* err) {
   __shared__ int32_t lds[kRelayLds];
-  if (block_failed(err)) return;
-  if ((int32_t)blockIdx.x < n_fill)
+  const TailShape ts = tail_shape(dmax, n, tail_cap);
+  if (!ts.take || block_failed(err)) return;
+  if ((int32_t)blockIdx.x < n_fill) {
     fill_partition((int64_t)blockIdx.x * kThreads + threadIdx.x, (int64_t)n_fill * kThreads, n,
                    rowptr_s, deg_s, cls, seg_off, info->n_segments, W, Z, DB, H, meta, cap, hub_ub,
                    hub_chunk_off, order);
-  else
-    relayout_tile(tile0 + blockIdx.x - n_fill, true, threadIdx.x, n, nnz, n_cols, rowptr, colidx,
-                  vals, perm, rowptr_s, colidx_s, vals_s, err, lds);
+    return;
+  }
+  const int64_t tiles = (nnz + kRelayTile - 1) / kRelayTile;
+  for (int64_t tile = ts.nnz_low / kRelayTile + (blockIdx.x - n_fill); tile < tiles;
+       tile += n_copy)
+    relayout_tile(tile, true, threadIdx.x, n, nnz, rowptr, colidx, vals, perm, rowptr_s, colidx_s,
+                  vals_s, err, lds);
 }
 
 // The rest of the plan up to the partition, in one workgroup of kTailThreads
@@ -1112,7 +1195,8 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
 //   - the partition's summary, in pinned host memory (the segment count in
 //     `info`).
 struct TailArgs {
-  int32_t n, nnz, T0, passes, width, W, Z, DB, H;
+  int32_t n, nnz, W, Z, DB, H;
+  int32_t cap;               // the short sort's largest tail
   const int32_t* tail_keys;  // [T0, n): the tail's degrees and rows in row order
   const int32_t* tail_ids;
   const int32_t* offsets;    // the short pass's (digit, tile) starts
@@ -1124,14 +1208,16 @@ struct TailArgs {
   int32_t* seg;
   TailInfo* info;
   PlanSummary* sum;
-  const int32_t* dmax;
+  const int32_t* dmax;       // maximum degree, tail size, lower nonzeros
+  const uint32_t* err;
 };
+
 
 // LDS of the tail's workgroup (int32 words).
 constexpr int kTailLds = 2 * kTailCap + kTailWaves * kRadixBins + kTailWaves + 1;
 
-__device__ inline void tail_block(const TailArgs& a, int32_t* lds) {
-  const int32_t n = a.n, nnz = a.nnz, T0 = a.T0, W = a.W, Z = a.Z, DB = a.DB, H = a.H;
+__device__ inline void tail_block(const TailArgs& a, const TailShape& ts, int32_t* lds) {
+  const int32_t n = a.n, nnz = a.nnz, T0 = ts.T0, W = a.W, Z = a.Z, DB = a.DB, H = a.H;
   const int32_t* __restrict__ tail_keys = a.tail_keys;
   const int32_t* __restrict__ tail_ids = a.tail_ids;
   const int32_t* __restrict__ offsets = a.offsets;
@@ -1146,7 +1232,7 @@ __device__ inline void tail_block(const TailArgs& a, int32_t* lds) {
   int32_t (*s_cnt)[kRadixBins] = reinterpret_cast<int32_t (*)[kRadixBins]>(s_id + kTailCap);
   int32_t* s_wsum = s_id + kTailCap + kTailWaves * kRadixBins;
   int32_t& s_hub_first_entry = s_wsum[kTailWaves];
-  const uint32_t dmask = (1u << a.width) - 1;
+  const uint32_t dmask = (1u << ts.width) - 1;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int32_t m = n - T0;
   const int32_t c = ((m + kTailWaves * 64 - 1) / (kTailWaves * 64)) * 64;  // per wave
@@ -1161,8 +1247,8 @@ __device__ inline void tail_block(const TailArgs& a, int32_t* lds) {
       id[j] = e < m ? tail_ids[T0 + e] : 0;
     }
   }
-  for (int p = 0; p < a.passes; ++p) {
-    const int shift = a.width * p;
+  for (int p = 0; p < ts.passes; ++p) {
+    const int shift = ts.width * p;
     for (int q = t; q < kTailWaves * kRadixBins; q += kTailThreads) (&s_cnt[0][0])[q] = 0;
     __syncthreads();
     // Digit, rank among the round's equal digits and their number, packed
@@ -1173,7 +1259,7 @@ __device__ inline void tail_block(const TailArgs& a, int32_t* lds) {
       if (j < rounds) {
         const bool valid = w0 + j * 64 + lane < m;
         const uint32_t digit = ((uint32_t)(k[j] - kTailKey) >> shift) & dmask;
-        const uint64_t peers = match_bits(digit, valid, a.width);
+        const uint64_t peers = match_bits(digit, valid, ts.width);
         const uint32_t rank = (uint32_t)__popcll(peers & __lanemask_lt());
         const uint32_t size = (uint32_t)__popcll(peers);
         pk[j] = digit | rank << 8 | size << 16;
@@ -1320,49 +1406,55 @@ __device__ inline void tail_block(const TailArgs& a, int32_t* lds) {
     a.sum->n_hub_rows = n - hub_first_row;
     a.sum->hub_first_row = hub_first_row;
     a.sum->max_deg = a.dmax[0];
+    a.sum->err = a.err[0];  // final but for kErrRelayout, which k_relayout_fill may raise
+    __threadfence_system();
+    a.sum->done = 1;
     __threadfence_system();
   }
 }
 
 
 // The short-sort plan's second launch: workgroup 0 finishes the plan up to the
-// partition (tail_block) while the others copy the sorted CSR of the rows
-// below the tail, which need nothing from it: kTailThreads / kThreads tiles
-// per workgroup, the first n_low_tiles tiles of the sorted nonzeros (those
-// wholly before the tail's first nonzero). The LDS is one buffer that either
-// role carves.
+// partition (tail_block) and publishes the summary, while the other n_groups
+// copy the sorted CSR of the rows below the tail, which need nothing from it:
+// kTailThreads / kThreads tiles per workgroup and round, the tiles of sorted
+// nonzeros wholly before the tail's first nonzero. The LDS is one buffer that
+// either role carves. Returns at once when the tail is over the cap (the
+// multi-pass sort follows); on an input error workgroup 0 publishes it.
 constexpr int kTilesPerTailGroup = kTailThreads / kThreads;
+// Relayout workgroups of k_relayout_fill per CU (its LDS allows six).
+constexpr int kRelayGroupsPerCu = 6;
 constexpr int kXLds = kTailLds > kTilesPerTailGroup * kRelayLds ? kTailLds
                                                                  : kTilesPerTailGroup * kRelayLds;
 
 __global__ __launch_bounds__(kTailThreads) void k_tail_relayout(
-    TailArgs ta, int64_t n_low_tiles, int64_t nnz, int32_t n_cols,
-    const int32_t* __restrict__ rowptr, const int32_t* __restrict__ colidx,
-    const float* __restrict__ vals, int32_t* __restrict__ colidx_s, float* __restrict__ vals_s,
-    uint32_t* err) {
+    TailArgs ta, int32_t n_groups, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ colidx, const float* __restrict__ vals,
+    int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, uint32_t* err) {
   __shared__ int32_t lds[kXLds];
-  if (block_failed(err)) return;
+  const TailShape ts = tail_shape(ta.dmax, ta.n, ta.cap);
+  if (!ts.take) return;
+  if (block_failed(err)) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      ta.sum->err = err[0];
+      __threadfence_system();
+      ta.sum->done = 1;
+      __threadfence_system();
+    }
+    return;
+  }
   if (blockIdx.x == 0) {
-    tail_block(ta, lds);
+    tail_block(ta, ts, lds);
     return;
   }
   const int q = threadIdx.x / kThreads;
-  const int64_t tile = (int64_t)(blockIdx.x - 1) * kTilesPerTailGroup + q;
   // Rows [0, T0) with rowptr_s[T0] (the tail's first nonzero) are final.
-  relayout_tile(tile, tile < n_low_tiles, threadIdx.x % kThreads, ta.T0, nnz, n_cols, rowptr,
-                colidx, vals, ta.perm, ta.rowptr_s, colidx_s, vals_s, err, lds + q * kRelayLds);
-}
-
-// The summary's error word (the column check included) and done flag, after
-// k_relayout_fill. One small launch: a completion count kept by the
-// relayout's workgroups themselves cost more (one device-scope atomic each on
-// one word, serialised).
-__global__ void k_publish(const uint32_t* err, PlanSummary* sum) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) {
-    sum->err = err[0];
-    __threadfence_system();
-    sum->done = 1;
-    __threadfence_system();
+  const int64_t low_tiles = ts.nnz_low / kRelayTile;
+  for (int64_t t0 = (int64_t)(blockIdx.x - 1) * kTilesPerTailGroup; t0 < low_tiles;
+       t0 += (int64_t)n_groups * kTilesPerTailGroup) {
+    const int64_t tile = t0 + q;
+    relayout_tile(tile, tile < low_tiles, threadIdx.x % kThreads, ts.T0, ta.nnz, rowptr, colidx,
+                  vals, ta.perm, ta.rowptr_s, colidx_s, vals_s, err, lds + q * kRelayLds);
   }
 }
 
@@ -1574,6 +1666,22 @@ int32_t tail_cap_setting() {
   return v < -1 ? kTailCap : std::min<int32_t>(v, kTailCap);
 }
 
+// Compute units of a device, queried once per device.
+int32_t device_cus(int dev) {
+  static std::atomic<int32_t> cached[64];
+  if (dev < 0 || dev >= 64) return 256;
+  const int32_t v = cached[dev].load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0) {
+    (void)hipGetLastError();
+    cus = 256;
+  }
+  cached[dev].store(cus, std::memory_order_relaxed);
+  return cus;
+}
+
 // Per-thread pinned, host-coherent buffer for the plan's read-backs (the
 // kernels write it directly), allocated on the first plan built by the thread
 // and kept for the life of the process. *dev receives its device address.
@@ -1604,12 +1712,21 @@ PlanSummary* pinned_summary(PlanSummary** dev) {
 }
 
 // Waits until the device sets *flag, a word of the pinned summary, polling
-// it; every 64 polls the stream is queried, so a failed launch or a stream
-// that finished without setting the flag ends the wait with an error.
+// it. Once the wait has taken kQueryAfterUs, the stream is queried every 64
+// polls, so a failed launch or a stream that finished without setting the
+// flag ends the wait with an error. (A query of a busy stream queues a
+// marker behind its work, around which the GPU idles several microseconds;
+// a plan queued behind a whole step of other work waits milliseconds.)
+constexpr int kQueryAfterUs = 2000000;
+
 int wait_flag(const uint32_t* flag, hipStream_t st, const char* what) {
+  const auto t0 = std::chrono::steady_clock::now();
+  bool query = false;
   for (uint32_t it = 1;; ++it) {
     if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) != 0) return AGCN_OK;
-    if ((it & 63) == 0) {
+    if (!query && (it & 63) == 0)
+      query = std::chrono::steady_clock::now() - t0 > std::chrono::microseconds(kQueryAfterUs);
+    if (query && (it & 63) == 0) {
       const hipError_t q = hipStreamQuery(st);
       if (q == hipSuccess) {
         if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) != 0) return AGCN_OK;
@@ -1686,14 +1803,17 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   int32_t* btail = bmax + 2 * (n_deg_blocks + 1);
   int32_t* blow = bmax + 3 * (n_deg_blocks + 1);
   if (n > 0)
-    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>((int32_t)n, nnz, d_rowptr, deg, bmax, berr,
-                                                         btail, blow, nullptr, 0, nullptr, nullptr);
+    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>(
+        (int32_t)n, nnz, d_rowptr, deg, bmax, berr, btail, blow, nullptr, 0, nullptr, nullptr,
+        (int32_t)n_deg_blocks, ColumnCheck{});  // k_wl_copy checks the columns
   ChainedScans chain;
   chain.status = reinterpret_cast<unsigned long long*>(b + o_status);
   chain.capacity = n_partials;
   chain.tickets = reinterpret_cast<int32_t*>(b + o_tickets);
   k_dmax<<<1, kScanTopThreads, 0, st>>>(
-      DegreeBlocks{bmax, berr, btail, blow, (int32_t)n_deg_blocks, dmax, err, dsum}, chain.tickets);
+      DegreeBlocks{bmax, berr, btail, blow, (int32_t)n_deg_blocks, (int32_t)n_deg_blocks, dmax, err,
+                   dsum},
+      chain.tickets);
   if (n > 0) k_wl_groups<<<(unsigned)nb, kThreads, 0, st>>>((int32_t)n, deg, Z, ng, err);
   const unsigned cgrid = (unsigned)std::min<int64_t>(grid_for(std::max(nnz, n + 1), kThreads), 65536);
   k_wl_copy<<<cgrid, kThreads, 0, st>>>((int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals,
@@ -1711,7 +1831,8 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   hipError_t he = hipStreamSynchronize(st);
   if (he != hipSuccess) return hip_fail(he, "hipStreamSynchronize(plan)");
   if (hs->err) {
-    if (hs->err & kErrInternal) return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
+    if (hs->err & (kErrInternal | kErrRelayout))
+      return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
     return fail(AGCN_ERR_INVALID_INPUT, "invalid CSR (row pointer or column index)");
   }
   p->n_entries = hs->n_entries;
@@ -1758,7 +1879,14 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   const size_t o_err = L.take(64);
   const size_t o_dmax = L.take(64);
   const int64_t n_deg_blocks = ceil_div64(n, kDegRows);
-  const size_t o_bmax = L.take(4 * 4 * (n_deg_blocks + 1));  // maxima, error flags, tails, lows
+  // Column-check chunks: at least kColCheckChunk entries, at most
+  // kColCheckMaxBlocks of them.
+  int64_t col_chunk = kColCheckChunk;
+  if (nnz > col_chunk * kColCheckMaxBlocks)
+    col_chunk = ceil_div64(ceil_div64(nnz, kColCheckMaxBlocks), kColCheckChunk) * kColCheckChunk;
+  const int64_t n_col_chunks = ceil_div64(nnz, col_chunk);
+  const size_t o_bmax = L.take(4 * 4 * (n_deg_blocks + 1));  // maxima, (unused), tails, lows
+  const size_t o_berr = L.take(4 * (n_deg_blocks + n_col_chunks + 1));  // error flags
   const size_t o_hsort = L.take(4 * 5 * chunk_ub);  // keys in, 2 x keys, 2 x ids
   const size_t o_hgate = L.take(64);
   const size_t o_tickets = L.take(4 * kMaxChainedScans);
@@ -1789,6 +1917,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   int32_t* nb = reinterpret_cast<int32_t*>(b + o_nb);
   int32_t* seg = reinterpret_cast<int32_t*>(b + o_seg);
   uint32_t* err = reinterpret_cast<uint32_t*>(b + o_err);
+  p->err_word = err;
   int32_t* dmax = reinterpret_cast<int32_t*>(b + o_dmax);
   int32_t* bmax = reinterpret_cast<int32_t*>(b + o_bmax);
   int32_t* hsort = reinterpret_cast<int32_t*>(b + o_hsort);
@@ -1801,7 +1930,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   // No kernel of this thread's previous plan writes the summary any more: its
   // last write came before the flag that plan waited for.
   *hs = PlanSummary{};
-  uint32_t* berr = reinterpret_cast<uint32_t*>(bmax + n_deg_blocks + 1);
+  uint32_t* berr = reinterpret_cast<uint32_t*>(b + o_berr);
   int32_t* btail = bmax + 2 * (n_deg_blocks + 1);
   int32_t* blow = bmax + 3 * (n_deg_blocks + 1);
   // The short sort needs every hub row in the tail (DB >= kTailKey).
@@ -1810,13 +1939,17 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   chain.status = reinterpret_cast<unsigned long long*>(b + o_status);
   chain.capacity = n_partials;
   chain.tickets = reinterpret_cast<int32_t*>(b + o_tickets);
-  const DegreeBlocks dblocks{bmax, berr, btail, blow, (int32_t)n_deg_blocks, dmax, err, dsum};
+  const DegreeBlocks dblocks{bmax,  berr, btail, blow, (int32_t)n_deg_blocks,
+                            (int32_t)(n_deg_blocks + n_col_chunks), dmax, err, dsum};
   // With the short sort, k_degree clears the error word and the tickets and
-  // the scan of its counts does the reduction (or launches k_dmax).
+  // the scan of its counts does the reduction (or launches k_dmax). Its
+  // column checks make every input error known at the reduction, before the
+  // short sort's second half (n > 0 whenever nnz > 0).
   if (n > 0)
-    k_degree<<<(unsigned)n_deg_blocks, kThreads, 0, st>>>(
+    k_degree<<<(unsigned)(n_deg_blocks + n_col_chunks), kThreads, 0, st>>>(
         (int32_t)n, nnz, d_rowptr, deg, bmax, berr, btail, blow, short_sort ? counts : nullptr,
-        (int32_t)n_tiles, short_sort ? err : nullptr, short_sort ? chain.tickets : nullptr);
+        (int32_t)n_tiles, short_sort ? err : nullptr, short_sort ? chain.tickets : nullptr,
+        (int32_t)n_deg_blocks, ColumnCheck{d_colidx, nnz, col_chunk, p->n_cols, 0});
   if (!short_sort) k_dmax<<<1, kScanTopThreads, 0, st>>>(dblocks, chain.tickets);
   if ((rc = check_launch("k_degree"))) return rc;
   const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
@@ -1830,13 +1963,14 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   const bool reduce_first =
       short_sort && n_tiles * kRadixBins > (int64_t)kChainedMaxTiles * kScanBlock;
   bool take_short = short_sort;
+  const int32_t cap = tail_cap_setting();
   if (reduce_first) {
     k_dmax<<<1, kScanTopThreads, 0, st>>>(dblocks, chain.tickets);
     if ((rc = check_launch("k_dmax"))) return rc;
     if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
     md = hs->max_deg;
     have_max = true;
-    take_short = hs->n_tail >= 0 && hs->n_tail <= tail_cap_setting();
+    take_short = hs->n_tail >= 0 && hs->n_tail <= cap;
   }
   if (take_short) {
     // Pass one of the short sort.
@@ -1846,55 +1980,55 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     k_scatter_low<<<rgrid, kThreads, 0, st>>>((int32_t)n, deg, counts, (int32_t)n_tiles, keys,
                                               p->perm, p->rowptr_s, keys2, ids2, err);
     if ((rc = check_launch("k_scatter_low"))) return rc;
+    // The second half is queued at once: its kernels read the tail's size,
+    // the maximum degree and the lower nonzeros on the device and return at
+    // once when the tail is over the cap, so the GPU need not wait for the
+    // host's read-back. Their copies loop over tiles on grids of a size that
+    // needs none of it.
+    TailArgs ta;
+    ta.n = (int32_t)n;
+    ta.nnz = (int32_t)nnz;
+    ta.W = W;
+    ta.Z = Z;
+    ta.DB = DB;
+    ta.H = H;
+    ta.cap = cap;
+    ta.tail_keys = keys2;
+    ta.tail_ids = ids2;
+    ta.offsets = counts;
+    ta.n_tiles = (int32_t)n_tiles;
+    ta.keys = keys;
+    ta.perm = p->perm;
+    ta.rowptr_s = p->rowptr_s;
+    ta.cls = cls;
+    ta.seg = seg;
+    ta.info = info;
+    ta.sum = dsum;
+    ta.dmax = dmax;
+    ta.err = err;
+    const int32_t cus = device_cus(p->device);
+    const int64_t max_tiles = ceil_div64(nnz, kRelayTile);
+    // One 1024-thread workgroup per CU (the tail's LDS), the tail's on one.
+    const int32_t n_groups = (int32_t)std::max<int64_t>(
+        1, std::min<int64_t>(ceil_div64(max_tiles, kTilesPerTailGroup), cus - 1));
+    k_tail_relayout<<<(unsigned)(1 + n_groups), kTailThreads, 0, st>>>(
+        ta, n_groups, d_rowptr, d_colidx, d_vals, p->colidx_s, p->vals_s, err);
+    if ((rc = check_launch("k_tail_relayout"))) return rc;
+    const int32_t n_fill = (int32_t)std::min<int64_t>(grid_for(ent_ub, kThreads), 64);
+    const int32_t n_copy = (int32_t)std::max<int64_t>(
+        1, std::min<int64_t>(max_tiles, (int64_t)kRelayGroupsPerCu * cus));
+    k_relayout_fill<<<(unsigned)(n_fill + n_copy), kThreads, 0, st>>>(
+        n_fill, n_copy, (int32_t)n, nnz, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
+        p->colidx_s, p->vals_s, keys, cls, seg, info, W, Z, DB, H, p->meta, ent_ub,
+        (int32_t)hub_ub, p->hub_chunk_off, p->order, dmax, cap, err);
+    if ((rc = check_launch("k_relayout_fill"))) return rc;
     if (!have_max) {
       if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
       md = hs->max_deg;
       have_max = true;
     }
-    const int32_t m = hs->n_tail;
-    if (m >= 0 && m <= tail_cap_setting()) {
-      int bits = 0;
-      while (bits < 31 && (int64_t(1) << bits) <= (int64_t)md - kTailKey) ++bits;
-      const int passes = (bits + 7) / 8;
-      TailArgs ta;
-      ta.n = (int32_t)n;
-      ta.nnz = (int32_t)nnz;
-      ta.T0 = (int32_t)(n - m);
-      ta.passes = passes;
-      ta.width = passes > 0 ? (bits + passes - 1) / passes : 8;
-      ta.W = W;
-      ta.Z = Z;
-      ta.DB = DB;
-      ta.H = H;
-      ta.tail_keys = keys2;
-      ta.tail_ids = ids2;
-      ta.offsets = counts;
-      ta.n_tiles = (int32_t)n_tiles;
-      ta.keys = keys;
-      ta.perm = p->perm;
-      ta.rowptr_s = p->rowptr_s;
-      ta.cls = cls;
-      ta.seg = seg;
-      ta.info = info;
-      ta.sum = dsum;
-      ta.dmax = dmax;
-      // Tiles of sorted nonzeros wholly below the tail's first one are copied
-      // beside the tail's workgroup; the rest after it.
-      const int64_t low_tiles = std::max<int64_t>(hs->nnz_low, 0) / kRelayTile;
-      k_tail_relayout<<<(unsigned)(1 + ceil_div64(low_tiles, kTilesPerTailGroup)), kTailThreads, 0,
-                        st>>>(ta, low_tiles, nnz, p->n_cols, d_rowptr, d_colidx, d_vals,
-                              p->colidx_s, p->vals_s, err);
-      if ((rc = check_launch("k_tail_relayout"))) return rc;
-      const int32_t n_fill = (int32_t)std::min<int64_t>(grid_for(ent_ub, kThreads), 64);
-      k_relayout_fill<<<(unsigned)(n_fill + grid_for(nnz, kRelayTile) - low_tiles), kThreads, 0,
-                        st>>>(n_fill, low_tiles, (int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx,
-                              d_vals, p->perm, p->rowptr_s, p->colidx_s, p->vals_s, keys, cls, seg,
-                              info, W, Z, DB, H, p->meta, ent_ub, (int32_t)hub_ub,
-                              p->hub_chunk_off, p->order, err);
-      k_publish<<<1, 64, 0, st>>>(err, dsum);
-      if ((rc = check_launch("k_relayout_fill"))) return rc;
-      short_done = true;
-    }
+    // The same test the two kernels made; otherwise they returned at once.
+    short_done = hs->n_tail >= 0 && hs->n_tail <= cap;
   }
   if (n > 0 && !short_done) {
     // Stable LSD radix sort of row ids by degree, 8-bit digits. Unless the
@@ -1933,7 +2067,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
       return rc;
     if (nnz > 0) {
       k_relayout<<<grid_for(nnz, kRelayTile), kThreads, 0, st>>>(
-          (int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
+          (int32_t)n, nnz, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
           p->colidx_s, p->vals_s, err);
       if ((rc = check_launch("k_relayout"))) return rc;
     }
@@ -1957,7 +2091,8 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     if (hs->err & kErrRowptrOrder) why += " rowptr decreases or leaves [0, nnz];";
     if (hs->err & kErrRowptrEnd) why += " rowptr[n_rows] != nnz;";
     if (hs->err & kErrColumn) why += " column index outside [0, n_cols);";
-    if (hs->err & kErrInternal) return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
+    if (hs->err & (kErrInternal | kErrRelayout))
+      return fail(AGCN_ERR_HIP, "internal plan consistency check failed");
     return fail(AGCN_ERR_INVALID_INPUT, "invalid CSR:" + why);
   }
   p->n_entries = hs->n_entries;
