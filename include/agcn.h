@@ -149,7 +149,11 @@ void agcn_default_params(agcn_plan_params* p);
  * keeps the plain heaviest-first order (the plan stays valid);
  * AGCN_TEST_TAIL_CAP=c lowers to c the number of rows of degree >= 255 that
  * the short degree sort takes (-1: none, so every plan takes the multi-pass
- * sort; the result is the same stable sort either way). */
+ * sort; the result is the same stable sort either way);
+ * AGCN_TEST_EARLY_CHECK_NNZ=k sets to k the largest graph whose column
+ * indices the short sort checks before its last relayout, returning while
+ * that relayout runs (larger graphs: checked by the relayout, and the call
+ * returns after it; the plan is the same either way). */
 int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t nnz,
                      const int32_t* d_rowptr, const int32_t* d_colidx, const float* d_vals,
                      const agcn_plan_params* params, void* stream);

@@ -58,6 +58,11 @@ int test_tail_cap() {
   return v ? std::atoi(v) : -2;
 }
 
+long long test_early_check_nnz() {
+  const char* v = std::getenv("AGCN_TEST_EARLY_CHECK_NNZ");
+  return v ? std::atoll(v) : -1;
+}
+
 void set_error(const std::string& msg) { g_last_error = msg; }
 
 int fail(int status, const std::string& msg) {

@@ -91,11 +91,17 @@ namespace agcn {
 //                                fails as if the memory were exhausted;
 //   AGCN_TEST_FAIL_ORDER_SORT=1  the launch-order sort of hub chunks starts
 //                                with the internal-error flag raised, as when
-//                                one of its scans gives up its bounded wait.
+//                                one of its scans gives up its bounded wait;
+//   AGCN_TEST_TAIL_CAP=c         the short sort takes tails of at most c rows;
+//   AGCN_TEST_EARLY_CHECK_NNZ=k  the short sort checks the column indices in
+//                                k_degree (and publishes its summary before
+//                                the last relayout) for graphs of at most k
+//                                nonzeros.
 void test_alloc_reset();    // start of agcn_plan_create
 bool test_alloc_fails();    // counts one allocation attempt; true: fail it
 bool test_order_sort_fails();
 int test_tail_cap();         // AGCN_TEST_TAIL_CAP, or -2 when unset
+long long test_early_check_nnz();  // AGCN_TEST_EARLY_CHECK_NNZ, or -1 when unset
 
 // Thread-local error text (set by the failing call).
 void set_error(const std::string& msg);

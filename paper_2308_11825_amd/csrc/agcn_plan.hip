@@ -247,13 +247,20 @@ __global__ void k_raise(uint32_t* err, uint32_t bits) {
   if (threadIdx.x == 0 && blockIdx.x == 0) atomicOr(err, bits);
 }
 
-// The column indices are checked against n_cols by workgroups that k_degree
-// carries past its own: chunk c of the input's colidx per workgroup, chunks a
-// multiple of this many entries. (Split between k_degree and k_scatter_low,
-// the check cost more in all.)
+// For the short sort of a graph of at most kEarlyCheckMaxNnz nonzeros, the
+// column indices are checked against n_cols by workgroups that k_degree
+// carries past its own, so that every input error is known when the tail's
+// workgroup publishes the summary, before the last relayout: chunk c of the
+// input's colidx per workgroup, chunks a multiple of this many entries.
+// (Split between k_degree and k_scatter_low, the check cost more in all.)
+// Otherwise the relayout copies check them.
 constexpr int kColCheckItems = 8;
 constexpr int64_t kColCheckChunk = (int64_t)kThreads * kColCheckItems * 8;  // 16384
 constexpr int32_t kColCheckMaxBlocks = 2048;
+// Largest graph whose columns k_degree checks (about 4 us of the plan at
+// 11.4 M nonzeros, and growing with them, against the host latency that the
+// early summary hides).
+constexpr int64_t kEarlyCheckMaxNnz = int64_t(1) << 24;
 
 struct ColumnCheck {
   const int32_t* colidx;
@@ -918,12 +925,14 @@ __device__ inline int rpad(int i) { return i + (i >> 5); }
 // non-empty and at most kRelayTile rows (the "window") are involved. Each
 // window row marks its first position; an inclusive max-scan of the marks
 // then gives every position its row in O(1). Called by whole workgroups.
+// Column indices are checked against check_cols (INT32_MAX when k_degree has
+// checked them already).
 // LDS of one relayout tile (int32 words), also lent to the tail's workgroup.
 constexpr int kRelayLds = (kRelayTile + 1) + kRelayTile + (kRelayTile + kRelayTile / 32) +
                           kThreads / 64 + 2;
 
 __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t n, int64_t nnz,
-                                     const int32_t* __restrict__ rowptr,
+                                     int32_t check_cols, const int32_t* __restrict__ rowptr,
                                      const int32_t* __restrict__ colidx,
                                      const float* __restrict__ vals,
                                      const int32_t* __restrict__ perm,
@@ -986,6 +995,7 @@ __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t
     s_row[rpad(tid * kRelayItems + k)] = max(before, v[k]);
   __syncthreads();
   if (!active) return;  // no barrier below
+  uint32_t bad = 0;
 #pragma unroll
   for (int k = 0; k < kRelayItems; ++k) {
     const int j = k * kThreads + tid;
@@ -993,10 +1003,13 @@ __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t
     if (e < e1) {
       const int32_t w = s_row[rpad(j)];
       const int64_t src = (int64_t)s_src[w] + (e - s_ptr[w]);
-      colidx_s[e] = colidx[src];
+      const int32_t c = colidx[src];
+      if ((uint32_t)c >= (uint32_t)check_cols) bad = kErrColumn;
+      colidx_s[e] = c;
       vals_s[e] = vals[src];
     }
   }
+  if (bad) atomicOr(err, bad);
 }
 
 // The error word as one workgroup sees it, read once (other workgroups may
@@ -1011,13 +1024,13 @@ __device__ inline bool block_failed(const uint32_t* err) {
 }
 
 __global__ __launch_bounds__(kThreads) void k_relayout(
-    int32_t n, int64_t nnz, const int32_t* __restrict__ rowptr,
+    int32_t n, int64_t nnz, int32_t n_cols, const int32_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, const float* __restrict__ vals,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ rowptr_s,
     int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, uint32_t* err) {
   __shared__ int32_t lds[kRelayLds];
   if (block_failed(err)) return;
-  relayout_tile(blockIdx.x, true, threadIdx.x, n, nnz, rowptr, colidx, vals, perm, rowptr_s,
+  relayout_tile(blockIdx.x, true, threadIdx.x, n, nnz, n_cols, rowptr, colidx, vals, perm, rowptr_s,
                 colidx_s, vals_s, err, lds);
 }
 
@@ -1159,7 +1172,7 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
     const TailInfo* __restrict__ info, int32_t W, int32_t Z, int32_t DB, int32_t H,
     int4* __restrict__ meta, int64_t cap, int32_t hub_ub, int32_t* __restrict__ hub_chunk_off,
     int32_t* __restrict__ order, const int32_t* __restrict__ dmax, int32_t tail_cap,
-    uint32_t* err) {
+    int32_t check_cols, uint32_t* err) {
   __shared__ int32_t lds[kRelayLds];
   const TailShape ts = tail_shape(dmax, n, tail_cap);
   if (!ts.take || block_failed(err)) return;
@@ -1172,7 +1185,7 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
   const int64_t tiles = (nnz + kRelayTile - 1) / kRelayTile;
   for (int64_t tile = ts.nnz_low / kRelayTile + (blockIdx.x - n_fill); tile < tiles;
        tile += n_copy)
-    relayout_tile(tile, true, threadIdx.x, n, nnz, rowptr, colidx, vals, perm, rowptr_s, colidx_s,
+    relayout_tile(tile, true, threadIdx.x, n, nnz, check_cols, rowptr, colidx, vals, perm, rowptr_s, colidx_s,
                   vals_s, err, lds);
 }
 
@@ -1197,6 +1210,8 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
 struct TailArgs {
   int32_t n, nnz, W, Z, DB, H;
   int32_t cap;               // the short sort's largest tail
+  int32_t check_cols;        // the relayout's column bound (INT32_MAX: checked before)
+  int32_t publish;           // the tail's workgroup sets the host's done flag
   const int32_t* tail_keys;  // [T0, n): the tail's degrees and rows in row order
   const int32_t* tail_ids;
   const int32_t* offsets;    // the short pass's (digit, tile) starts
@@ -1406,9 +1421,11 @@ __device__ inline void tail_block(const TailArgs& a, const TailShape& ts, int32_
     a.sum->n_hub_rows = n - hub_first_row;
     a.sum->hub_first_row = hub_first_row;
     a.sum->max_deg = a.dmax[0];
-    a.sum->err = a.err[0];  // final but for kErrRelayout, which k_relayout_fill may raise
-    __threadfence_system();
-    a.sum->done = 1;
+    if (a.publish) {  // every input error is known: k_degree checked the columns
+      a.sum->err = a.err[0];  // final but for kErrRelayout, which k_relayout_fill may raise
+      __threadfence_system();
+      a.sum->done = 1;
+    }
     __threadfence_system();
   }
 }
@@ -1435,7 +1452,7 @@ __global__ __launch_bounds__(kTailThreads) void k_tail_relayout(
   const TailShape ts = tail_shape(ta.dmax, ta.n, ta.cap);
   if (!ts.take) return;
   if (block_failed(err)) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (ta.publish && blockIdx.x == 0 && threadIdx.x == 0) {
       ta.sum->err = err[0];
       __threadfence_system();
       ta.sum->done = 1;
@@ -1453,8 +1470,25 @@ __global__ __launch_bounds__(kTailThreads) void k_tail_relayout(
   for (int64_t t0 = (int64_t)(blockIdx.x - 1) * kTilesPerTailGroup; t0 < low_tiles;
        t0 += (int64_t)n_groups * kTilesPerTailGroup) {
     const int64_t tile = t0 + q;
-    relayout_tile(tile, tile < low_tiles, threadIdx.x % kThreads, ts.T0, ta.nnz, rowptr, colidx,
+    relayout_tile(tile, tile < low_tiles, threadIdx.x % kThreads, ts.T0, ta.nnz, ta.check_cols, rowptr, colidx,
                   vals, ta.perm, ta.rowptr_s, colidx_s, vals_s, err, lds + q * kRelayLds);
+  }
+}
+
+// The summary's error word (the relayout's column check included) and done
+// flag, after k_relayout_fill, when the tail's workgroup could not publish
+// them. One small launch: a completion count kept by the relayout's
+// workgroups themselves cost more (one device-scope atomic each on one word,
+// serialised). Like the launches before it, it returns at once when the tail
+// is over the cap (the multi-pass sort publishes instead).
+__global__ void k_publish(const uint32_t* err, PlanSummary* sum, const int32_t* dmax, int32_t n,
+                          int32_t tail_cap) {
+  if (!tail_shape(dmax, n, tail_cap).take) return;
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    sum->err = err[0];
+    __threadfence_system();
+    sum->done = 1;
+    __threadfence_system();
   }
 }
 
@@ -1884,7 +1918,13 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   int64_t col_chunk = kColCheckChunk;
   if (nnz > col_chunk * kColCheckMaxBlocks)
     col_chunk = ceil_div64(ceil_div64(nnz, kColCheckMaxBlocks), kColCheckChunk) * kColCheckChunk;
-  const int64_t n_col_chunks = ceil_div64(nnz, col_chunk);
+  // k_degree checks the columns when the short sort's summary is to be read
+  // before its last relayout (graphs of at most kEarlyCheckMaxNnz nonzeros);
+  // otherwise the relayout copies check them for free.
+  const long long early_max = test_early_check_nnz();
+  const bool early_check =
+      n > 0 && DB >= kTailKey && nnz <= (early_max >= 0 ? early_max : kEarlyCheckMaxNnz);
+  const int64_t n_col_chunks = early_check ? ceil_div64(nnz, col_chunk) : 0;
   const size_t o_bmax = L.take(4 * 4 * (n_deg_blocks + 1));  // maxima, (unused), tails, lows
   const size_t o_berr = L.take(4 * (n_deg_blocks + n_col_chunks + 1));  // error flags
   const size_t o_hsort = L.take(4 * 5 * chunk_ub);  // keys in, 2 x keys, 2 x ids
@@ -1993,6 +2033,8 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     ta.DB = DB;
     ta.H = H;
     ta.cap = cap;
+    ta.check_cols = early_check ? INT32_MAX : p->n_cols;
+    ta.publish = early_check;
     ta.tail_keys = keys2;
     ta.tail_ids = ids2;
     ta.offsets = counts;
@@ -2020,8 +2062,12 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     k_relayout_fill<<<(unsigned)(n_fill + n_copy), kThreads, 0, st>>>(
         n_fill, n_copy, (int32_t)n, nnz, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
         p->colidx_s, p->vals_s, keys, cls, seg, info, W, Z, DB, H, p->meta, ent_ub,
-        (int32_t)hub_ub, p->hub_chunk_off, p->order, dmax, cap, err);
+        (int32_t)hub_ub, p->hub_chunk_off, p->order, dmax, cap, ta.check_cols, err);
     if ((rc = check_launch("k_relayout_fill"))) return rc;
+    if (!early_check) {
+      k_publish<<<1, 64, 0, st>>>(err, dsum, dmax, (int32_t)n, cap);
+      if ((rc = check_launch("k_publish"))) return rc;
+    }
     if (!have_max) {
       if ((rc = wait_flag(&hs->dmax_ready, st, "maximum degree read-back"))) return rc;
       md = hs->max_deg;
@@ -2067,7 +2113,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
       return rc;
     if (nnz > 0) {
       k_relayout<<<grid_for(nnz, kRelayTile), kThreads, 0, st>>>(
-          (int32_t)n, nnz, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
+          (int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
           p->colidx_s, p->vals_s, err);
       if ((rc = check_launch("k_relayout"))) return rc;
     }

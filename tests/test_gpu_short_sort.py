@@ -3,12 +3,17 @@
 With W * Z >= 255 the plan first sorts by min(degree, 255) in one pass and
 sorts the rows of degree >= 255 (the tail, at most 16384 rows) in a single
 workgroup; otherwise, or with a larger tail, it runs the multi-pass radix sort
-(AGCN_TEST_TAIL_CAP=-1 forces that, after the first short pass, on any graph).
-Both plans must equal the oracle's bit for bit (Sec. III-C: a stable sort by
-degree, then Alg. 1 and Alg. 2), at the tail's edges too: degrees 254, 255 and
-256, a tail whose degrees are all 255 (no tail pass), degrees that need three
-tail passes, W * Z = 255 exactly, and tails of 16384 and 16385 rows.
+(AGCN_TEST_TAIL_CAP=-1 forces that, after the first short pass, on any graph;
+the short sort's second half is then queued all the same and must leave the
+plan alone). Graphs of at most 2^24 nonzeros have their column indices checked
+before the short sort's last relayout, which then runs after the call returns;
+larger ones in the relayout (AGCN_TEST_EARLY_CHECK_NNZ=0 forces that). Every
+combination must equal the oracle's plan bit for bit (Sec. III-C: a stable
+sort by degree, then Alg. 1 and Alg. 2), at the tail's edges too: degrees 254,
+255 and 256, a tail whose degrees are all 255 (no tail pass), degrees that
+need three tail passes, W * Z = 255 exactly, and tails of 16384 and 16385 rows.
 """
+import contextlib
 import os
 
 import numpy as np
@@ -25,25 +30,49 @@ pytestmark = pytest.mark.gpu
 TAIL_CAP = 16384
 
 
+@contextlib.contextmanager
+def _env(**kv):
+    """Sets (value str) or clears (None) the given variables for the block."""
+    old = {k: os.environ.get(k) for k in kv}
+    try:
+        for k, v in kv.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+        yield
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+# (tail cap, early-check limit): the short sort with the early column check
+# (the default on these graphs) and with the relayout's, the multi-pass sort
+# after a short attempt under either.
+PATHS = [(None, None), (None, "0"), ("-1", None), ("-1", "0")]
+
+
 def _both(g, **kw):
-    """Plans of g with the short sort (default) and with the multi-pass sort;
-    both checked against the oracle and against each other."""
+    """Plans of g along every path of PATHS, each checked against the oracle
+    and against the others; returns the short-sort (default) and the
+    multi-pass plans."""
     out = []
-    for cap in (None, "-1"):
-        if cap is None:
-            os.environ.pop("AGCN_TEST_TAIL_CAP", None)
-        else:
-            os.environ["AGCN_TEST_TAIL_CAP"] = cap
-        try:
+    for cap, early in PATHS:
+        with _env(AGCN_TEST_TAIL_CAP=cap, AGCN_TEST_EARLY_CHECK_NNZ=early):
             p = _plan(g, **kw)
-        finally:
-            os.environ.pop("AGCN_TEST_TAIL_CAP", None)
         out.append((p, assert_plan_matches_oracle(p, g)))
-    (p0, e0), (p1, e1) = out
-    for k in ("perm", "rowptr_s", "colidx_s", "meta"):
-        assert np.array_equal(e0[k], e1[k]), k
-    assert p0.stats.n_entries == p1.stats.n_entries
-    return p0, p1
+    p0, e0 = out[0]
+    for p, e in out[1:]:
+        for k in ("perm", "rowptr_s", "colidx_s", "meta"):
+            assert np.array_equal(e0[k], e[k]), k
+        assert p0.stats.n_entries == p.stats.n_entries
+    for p, _ in out[1:]:
+        if p is not out[2][0]:
+            p.destroy()
+    return p0, out[2][0]
 
 
 @pytest.mark.parametrize("W,Z", [(16, 32), (12, 32), (15, 17), (16, 256), (32, 8)])
@@ -93,23 +122,48 @@ def test_tail_at_the_cap(m):
     p.destroy()
 
 
-def test_invalid_csr_through_the_short_sort():
+@pytest.mark.parametrize("cap,early", PATHS)
+def test_invalid_csr_through_the_short_sort(cap, early):
     g = _mixed(950, n=5000)
-    ci = g.colidx.copy()
-    ci[len(ci) // 2] = g.n_cols       # one column out of range
-    bad = graphgen.Graph("bad", g.n_rows, g.n_cols, g.rowptr, ci, g.vals)
-    with pytest.raises(agcn.AgcnError) as e:
-        _plan(bad)
-    assert e.value.status == agcn.AGCN_ERR_INVALID_INPUT
-    rp = g.rowptr.copy()
-    rp[100] = rp[101] + 1             # a decreasing row pointer
-    bad = graphgen.Graph("bad", g.n_rows, g.n_cols, rp, g.colidx, g.vals)
-    with pytest.raises(agcn.AgcnError) as e:
-        _plan(bad)
-    assert e.value.status == agcn.AGCN_ERR_INVALID_INPUT
-    p = _plan(g)                      # and a valid plan right after
-    assert_plan_matches_oracle(p, g)
-    p.destroy()
+    with _env(AGCN_TEST_TAIL_CAP=cap, AGCN_TEST_EARLY_CHECK_NNZ=early):
+        for where in (0, len(g.colidx) // 2, len(g.colidx) - 1):
+            ci = g.colidx.copy()
+            ci[where] = g.n_cols if where else -1   # one column out of range
+            bad = graphgen.Graph("bad", g.n_rows, g.n_cols, g.rowptr, ci, g.vals)
+            with pytest.raises(agcn.AgcnError) as e:
+                _plan(bad)
+            assert e.value.status == agcn.AGCN_ERR_INVALID_INPUT
+            assert "column index" in str(e.value)
+        rp = g.rowptr.copy()
+        rp[100] = rp[101] + 1             # a decreasing row pointer
+        bad = graphgen.Graph("bad", g.n_rows, g.n_cols, rp, g.colidx, g.vals)
+        with pytest.raises(agcn.AgcnError) as e:
+            _plan(bad)
+        assert e.value.status == agcn.AGCN_ERR_INVALID_INPUT
+        p = _plan(g)                      # and a valid plan right after
+        assert_plan_matches_oracle(p, g)
+        p.destroy()
+
+
+def test_inputs_overwritten_in_stream_order_after_create():
+    # The short sort's last relayout still reads the inputs when the call
+    # returns; work queued after it on the same stream may overwrite them.
+    g = _mixed(960, n=30000)
+    dev = torch.device("cuda:0")
+    rp = torch.from_numpy(g.rowptr.copy()).to(dev)
+    ci = torch.from_numpy(g.colidx.copy()).to(dev)
+    va = torch.from_numpy(g.vals.copy()).to(dev)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        p = agcn.Plan(rp, ci, va, n_cols=g.n_cols)
+        ci.fill_(-5)
+        va.fill_(float("nan"))
+        rp.fill_(-3)
+        assert_plan_matches_oracle(p, g)
+        p.destroy()
+        rp.copy_(torch.from_numpy(g.rowptr))
+        ci.copy_(torch.from_numpy(g.colidx))
+        va.copy_(torch.from_numpy(g.vals))
 
 
 def test_short_sort_on_a_graph_whose_counts_scan_is_multi_launch():
