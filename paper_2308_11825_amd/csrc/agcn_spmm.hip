@@ -280,11 +280,15 @@ __global__ __launch_bounds__(1024) void k_hub_reduce(const int32_t* __restrict__
 // bounds, loads all of its (column, value) pairs at once, issues every gather
 // before the first FMA, and adds in nnz order. With every degree <= Z each
 // row is one vwarp of the block-level partition, so Y equals k_spmm's bit for
-// bit.
+// bit. The kernel is unrolled for MD pairs, the plan's maximum degree rounded
+// up to a multiple of kSmallDegStep: a shorter kernel (fewer registers, less
+// code) launches and runs measurably faster (4096-row graph of maximum degree
+// 21: 4.8 us for 32-deep loops, 4.3 us for 24-deep ones).
 constexpr int kSmallMaxDeg = 32;
+constexpr int kSmallDegStep = 8;
 constexpr int kSmallThreads = 256;  // measured: 64-thread workgroups (every CU busy) were slower
 
-template <int VW, int LT>
+template <int VW, int LT, int MD>
 __global__ __launch_bounds__(kSmallThreads) void k_spmm_rows(
     int32_t n_rows, const int32_t* __restrict__ rowptr_s, const int32_t* __restrict__ colidx_s,
     const float* __restrict__ vals_s, const int32_t* __restrict__ perm, const float* __restrict__ X,
@@ -302,22 +306,22 @@ __global__ __launch_bounds__(kSmallThreads) void k_spmm_rows(
   const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
   const V* __restrict__ Xv = reinterpret_cast<const V*>(X + col0);
   const int64_t ldxv = ldx / VW;
-  int32_t c[kSmallMaxDeg];
-  float w[kSmallMaxDeg];
+  int32_t c[MD];
+  float w[MD];
 #pragma unroll
-  for (int k = 0; k < kSmallMaxDeg; ++k) {
+  for (int k = 0; k < MD; ++k) {
     if (k < d) {
       c[k] = colidx_s[a + k];
       w[k] = vals_s[a + k];
     }
   }
-  V x[kSmallMaxDeg];
+  V x[MD];
 #pragma unroll
-  for (int k = 0; k < kSmallMaxDeg; ++k)
+  for (int k = 0; k < MD; ++k)
     if (k < d) x[k] = Xv[(int64_t)c[k] * ldxv + lane];
   V acc = V(0.0f);
 #pragma unroll
-  for (int k = 0; k < kSmallMaxDeg; ++k)
+  for (int k = 0; k < MD; ++k)
     if (k < d) acc = fma_v(w[k], x[k], acc);
   V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[r] * ldy + col0);
   __builtin_nontemporal_store(act_v(acc, act), yr + lane);
@@ -652,17 +656,29 @@ bool small_path(const agcn_plan* p) {
          p->nnz <= kSmallMaxNnz && p->n_rows <= kSmallMaxRows;
 }
 
-template <int VW, int LT>
-void launch_rows(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols, Marks& mk,
-                 bool last_part) {
+template <int VW, int LT, int MD>
+void launch_rows_md(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols,
+                    Marks& mk, bool last_part) {
   const agcn_plan* p = a.p;
   const int64_t threads = (int64_t)p->n_rows * L;
   dim3 grid((unsigned)ceil_div64(threads, kSmallThreads), (unsigned)n_slices);
   const hipEvent_t stop = last_part ? mk.stop : nullptr;
-  hipExtLaunchKernelGGL(k_spmm_rows<VW, LT>, grid, dim3(kSmallThreads), 0, a.st, mk.start, stop, 0,
-                        p->n_rows, p->rowptr_s, p->colidx_s, p->vals_s, p->perm, a.X, a.ldx, a.Y,
-                        a.ldy, col_base, slice_cols, L, a.act);
+  hipExtLaunchKernelGGL(k_spmm_rows<VW, LT, MD>, grid, dim3(kSmallThreads), 0, a.st, mk.start,
+                        stop, 0, p->n_rows, p->rowptr_s, p->colidx_s, p->vals_s, p->perm, a.X,
+                        a.ldx, a.Y, a.ldy, col_base, slice_cols, L, a.act);
   mk.start = nullptr;
+}
+
+template <int VW, int LT>
+void launch_rows(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols, Marks& mk,
+                 bool last_part) {
+  // The loops' depth: the maximum degree rounded up to a multiple of kSmallDegStep.
+  switch ((std::max(a.p->max_deg, 1) + kSmallDegStep - 1) / kSmallDegStep) {
+    case 1: launch_rows_md<VW, LT, 8>(a, L, n_slices, col_base, slice_cols, mk, last_part); break;
+    case 2: launch_rows_md<VW, LT, 16>(a, L, n_slices, col_base, slice_cols, mk, last_part); break;
+    case 3: launch_rows_md<VW, LT, 24>(a, L, n_slices, col_base, slice_cols, mk, last_part); break;
+    default: launch_rows_md<VW, LT, 32>(a, L, n_slices, col_base, slice_cols, mk, last_part); break;
+  }
 }
 
 template <int VW>
