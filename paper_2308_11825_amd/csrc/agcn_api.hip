@@ -58,6 +58,11 @@ int test_tail_cap() {
   return v ? std::atoi(v) : -2;
 }
 
+int test_tiny_plan() {
+  const char* v = std::getenv("AGCN_TEST_TINY");
+  return v ? std::atoi(v) : 1;
+}
+
 long long test_early_check_nnz() {
   const char* v = std::getenv("AGCN_TEST_EARLY_CHECK_NNZ");
   return v ? std::atoll(v) : -1;

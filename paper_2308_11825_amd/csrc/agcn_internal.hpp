@@ -96,12 +96,15 @@ namespace agcn {
 //   AGCN_TEST_EARLY_CHECK_NNZ=k  the short sort checks the column indices in
 //                                k_degree (and publishes its summary before
 //                                the last relayout) for graphs of at most k
-//                                nonzeros.
+//                                nonzeros;
+//   AGCN_TEST_TINY=0             no small graph takes the single-workgroup
+//                                plan (k_plan_tiny).
 void test_alloc_reset();    // start of agcn_plan_create
 bool test_alloc_fails();    // counts one allocation attempt; true: fail it
 bool test_order_sort_fails();
 int test_tail_cap();         // AGCN_TEST_TAIL_CAP, or -2 when unset
 long long test_early_check_nnz();  // AGCN_TEST_EARLY_CHECK_NNZ, or -1 when unset
+int test_tiny_plan();        // AGCN_TEST_TINY (0: no single-workgroup plan), or 1 when unset
 
 // Thread-local error text (set by the failing call).
 void set_error(const std::string& msg);

@@ -1193,7 +1193,7 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
 // (the tail has at most kTailCap rows; T0 = n - m is its first sorted
 // position):
 //   - the tail sorted stably by degree: LSD passes of `width` <= 8 bits over
-//     degree - kTailKey. Wave w holds the tail's elements [w c, (w + 1) c) (c a
+//     degree - key_base. Wave w holds the tail's elements [w c, (w + 1) c) (c a
 //     multiple of 64, ceil(m / 16) rounded up) in registers, walking them in
 //     rounds of 64; ranks come from per-wave digit counts and ballots as in
 //     the radix passes, so equal degrees keep row order, and the (degree,
@@ -1201,8 +1201,9 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
 //   - perm and sorted degrees of the tail, and its row pointers (the nonzeros
 //     before it are nnz minus the tail's);
 //   - cls[d], the first sorted row of degree >= d, for d in [0, DB + 1]:
-//     the short pass's bin starts below kTailKey, a search of the sorted tail
-//     above (DB >= kTailKey, so every hub row is a tail row);
+//     the short pass's bin starts up to key_base when `offsets` is given, a
+//     search of the sorted tail above (DB >= kTailKey, so every hub row is a
+//     tail row) or, without `offsets`, for every d;
 //   - the segment scan of the partition (Alg. 2): ceil(count / block_rows)
 //     entries for each degree class, ceil(deg / H) chunks for each hub row;
 //   - the partition's summary, in pinned host memory (the segment count in
@@ -1212,9 +1213,12 @@ struct TailArgs {
   int32_t cap;               // the short sort's largest tail
   int32_t check_cols;        // the relayout's column bound (INT32_MAX: checked before)
   int32_t publish;           // the tail's workgroup sets the host's done flag
+  int32_t key_base;          // the sort's keys are degree - key_base (>= 0)
   const int32_t* tail_keys;  // [T0, n): the tail's degrees and rows in row order
   const int32_t* tail_ids;
-  const int32_t* offsets;    // the short pass's (digit, tile) starts
+  const int32_t* rowptr_in;  // instead of tail_keys / tail_ids (the whole graph,
+                             // T0 = 0): degrees from the row pointer, rows in order
+  const int32_t* offsets;    // the short pass's (digit, tile) starts, or null
   int32_t n_tiles;
   int32_t* keys;             // outputs: sorted degrees, perm, rowptr_s, cls, seg
   int32_t* perm;
@@ -1258,8 +1262,13 @@ __device__ inline void tail_block(const TailArgs& a, const TailShape& ts, int32_
   for (int j = 0; j < kTailItems; ++j) {
     if (j < rounds) {
       const int32_t e = w0 + j * 64 + lane;
-      k[j] = e < m ? tail_keys[T0 + e] : 0;
-      id[j] = e < m ? tail_ids[T0 + e] : 0;
+      if (a.rowptr_in != nullptr) {
+        k[j] = e < m ? a.rowptr_in[e + 1] - a.rowptr_in[e] : 0;
+        id[j] = e;
+      } else {
+        k[j] = e < m ? tail_keys[T0 + e] : 0;
+        id[j] = e < m ? tail_ids[T0 + e] : 0;
+      }
     }
   }
   for (int p = 0; p < ts.passes; ++p) {
@@ -1273,7 +1282,7 @@ __device__ inline void tail_block(const TailArgs& a, const TailShape& ts, int32_
     for (int j = 0; j < kTailItems; ++j) {
       if (j < rounds) {
         const bool valid = w0 + j * 64 + lane < m;
-        const uint32_t digit = ((uint32_t)(k[j] - kTailKey) >> shift) & dmask;
+        const uint32_t digit = ((uint32_t)(k[j] - a.key_base) >> shift) & dmask;
         const uint64_t peers = match_bits(digit, valid, ts.width);
         const uint32_t rank = (uint32_t)__popcll(peers & __lanemask_lt());
         const uint32_t size = (uint32_t)__popcll(peers);
@@ -1365,7 +1374,7 @@ __device__ inline void tail_block(const TailArgs& a, const TailShape& ts, int32_
   int32_t* s_cls = s_id;
   for (int32_t d = t; d <= DB + 1; d += kTailThreads) {
     int32_t r;
-    if (d <= kTailKey) {
+    if (offsets != nullptr && d <= a.key_base) {
       r = offsets[(int64_t)d * n_tiles];
     } else {
       int32_t a = 0, b = m;  // first tail element of degree >= d
@@ -1473,6 +1482,93 @@ __global__ __launch_bounds__(kTailThreads) void k_tail_relayout(
     relayout_tile(tile, tile < low_tiles, threadIdx.x % kThreads, ts.T0, ta.nnz, ta.check_cols, rowptr, colidx,
                   vals, ta.perm, ta.rowptr_s, colidx_s, vals_s, err, lds + q * kRelayLds);
   }
+}
+
+// The plan of a small graph (at most kTinyMaxRows rows and kTinyMaxNnz
+// nonzeros) up to the partition, in one workgroup of kTailThreads, in place of
+// k_degree, the scans and k_scatter_low: the input checked (row pointer and
+// column indices), every row sorted by degree by the tail's code (key base 0,
+// any W and Z), the class starts, the segment scan and the summary with the
+// host's done flag. k_relayout_fill then copies the whole sorted CSR and fills
+// the partition, reading the tail size (all rows) and the lower nonzeros (none)
+// that this kernel leaves in dmax.
+constexpr int32_t kTinyMaxRows = kTailCap;
+constexpr int64_t kTinyMaxNnz = int64_t(1) << 17;
+constexpr int kTinyCheckItems = 16;
+
+__global__ __launch_bounds__(kTailThreads) void k_plan_tiny(TailArgs ta, int32_t n_cols,
+                                                            const int32_t* __restrict__ rowptr,
+                                                            const int32_t* __restrict__ colidx,
+                                                            uint32_t* err, int32_t* tickets,
+                                                            int32_t* dmax) {
+  __shared__ int32_t lds[kXLds];
+  __shared__ uint32_t s_err;
+  __shared__ int32_t s_max;
+  const int t = threadIdx.x;
+  const int32_t n = ta.n;
+  const int64_t nnz = ta.nnz;
+  if (t == 0) {
+    s_err = 0;
+    s_max = 0;
+  }
+  if (t < kMaxChainedScans) tickets[t] = 0;  // the scans of the hub-chunk order sort
+  __syncthreads();
+  uint32_t e = 0;
+  int32_t mx = 0;
+#pragma unroll
+  for (int j = 0; j < kTailItems; ++j) {  // n <= kTailThreads * kTailItems
+    const int32_t i = j * kTailThreads + t;
+    if (i < n) {
+      const int32_t a0 = rowptr[i], b0 = rowptr[i + 1];
+      if (a0 < 0 || b0 < a0 || (int64_t)b0 > nnz) e |= kErrRowptrOrder;
+      else mx = max(mx, b0 - a0);
+      if (i == 0 && a0 != 0) e |= kErrRowptrStart;
+      if (i == n - 1 && (int64_t)b0 != nnz) e |= kErrRowptrEnd;
+    }
+  }
+  for (int64_t k0 = t; k0 < nnz; k0 += (int64_t)kTailThreads * kTinyCheckItems) {
+    int32_t c[kTinyCheckItems];
+#pragma unroll
+    for (int u = 0; u < kTinyCheckItems; ++u) {
+      const int64_t k = k0 + (int64_t)u * kTailThreads;
+      c[u] = k < nnz ? colidx[k] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kTinyCheckItems; ++u)
+      e |= (uint32_t)c[u] >= (uint32_t)n_cols ? kErrColumn : 0u;
+  }
+  e = wave_or(e);
+  mx = wave_max(mx);
+  if ((t & 63) == 0) {
+    if (e) atomicOr(&s_err, e);
+    atomicMax(&s_max, mx);
+  }
+  __syncthreads();
+  if (t == 0) {
+    err[0] = s_err;
+    dmax[0] = s_max;
+    dmax[1] = n;  // for k_relayout_fill: every row sorted here, no lower nonzeros
+    dmax[2] = 0;
+  }
+  if (s_err != 0) {
+    if (t == 0) {
+      ta.sum->err = s_err;
+      __threadfence_system();
+      ta.sum->done = 1;
+      __threadfence_system();
+    }
+    return;
+  }
+  TailShape ts;
+  ts.take = true;
+  ts.m = n;
+  ts.T0 = 0;
+  ts.nnz_low = 0;
+  int bits = 0;
+  while (bits < 31 && (int64_t(1) << bits) <= (int64_t)s_max) ++bits;
+  ts.passes = (bits + 7) / 8;
+  ts.width = ts.passes > 0 ? (bits + ts.passes - 1) / ts.passes : 8;
+  tail_block(ta, ts, lds);
 }
 
 // The summary's error word (the relayout's column check included) and done
@@ -1973,8 +2069,10 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   uint32_t* berr = reinterpret_cast<uint32_t*>(b + o_berr);
   int32_t* btail = bmax + 2 * (n_deg_blocks + 1);
   int32_t* blow = bmax + 3 * (n_deg_blocks + 1);
+  // A small graph's plan: one workgroup up to the partition (k_plan_tiny).
+  const bool tiny = n > 0 && n <= kTinyMaxRows && nnz <= kTinyMaxNnz && test_tiny_plan() != 0;
   // The short sort needs every hub row in the tail (DB >= kTailKey).
-  const bool short_sort = n > 0 && DB >= kTailKey;
+  const bool short_sort = n > 0 && DB >= kTailKey && !tiny;
   ChainedScans chain;
   chain.status = reinterpret_cast<unsigned long long*>(b + o_status);
   chain.capacity = n_partials;
@@ -1985,12 +2083,12 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   // the scan of its counts does the reduction (or launches k_dmax). Its
   // column checks make every input error known at the reduction, before the
   // short sort's second half (n > 0 whenever nnz > 0).
-  if (n > 0)
+  if (n > 0 && !tiny)
     k_degree<<<(unsigned)(n_deg_blocks + n_col_chunks), kThreads, 0, st>>>(
         (int32_t)n, nnz, d_rowptr, deg, bmax, berr, btail, blow, short_sort ? counts : nullptr,
         (int32_t)n_tiles, short_sort ? err : nullptr, short_sort ? chain.tickets : nullptr,
         (int32_t)n_deg_blocks, ColumnCheck{d_colidx, nnz, col_chunk, p->n_cols, 0});
-  if (!short_sort) k_dmax<<<1, kScanTopThreads, 0, st>>>(dblocks, chain.tickets);
+  if (!short_sort && !tiny) k_dmax<<<1, kScanTopThreads, 0, st>>>(dblocks, chain.tickets);
   if ((rc = check_launch("k_degree"))) return rc;
   const unsigned rgrid = grid_for(n_tiles, kRadixWaves);
   bool short_done = false, have_max = false;
@@ -2035,8 +2133,10 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     ta.cap = cap;
     ta.check_cols = early_check ? INT32_MAX : p->n_cols;
     ta.publish = early_check;
+    ta.key_base = kTailKey;
     ta.tail_keys = keys2;
     ta.tail_ids = ids2;
+    ta.rowptr_in = nullptr;
     ta.offsets = counts;
     ta.n_tiles = (int32_t)n_tiles;
     ta.keys = keys;
@@ -2075,6 +2175,43 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     }
     // The same test the two kernels made; otherwise they returned at once.
     short_done = hs->n_tail >= 0 && hs->n_tail <= cap;
+  }
+  if (tiny) {
+    TailArgs ta{};
+    ta.n = (int32_t)n;
+    ta.nnz = (int32_t)nnz;
+    ta.W = W;
+    ta.Z = Z;
+    ta.DB = DB;
+    ta.H = H;
+    ta.cap = kTailCap;
+    ta.check_cols = INT32_MAX;  // checked by k_plan_tiny
+    ta.publish = 1;
+    ta.key_base = 0;
+    ta.rowptr_in = d_rowptr;
+    ta.offsets = nullptr;
+    ta.keys = keys;
+    ta.perm = p->perm;
+    ta.rowptr_s = p->rowptr_s;
+    ta.cls = cls;
+    ta.seg = seg;
+    ta.info = info;
+    ta.sum = dsum;
+    ta.dmax = dmax;
+    ta.err = err;
+    k_plan_tiny<<<1, kTailThreads, 0, st>>>(ta, p->n_cols, d_rowptr, d_colidx, err, chain.tickets,
+                                            dmax);
+    if ((rc = check_launch("k_plan_tiny"))) return rc;
+    const int32_t cus = device_cus(p->device);
+    const int32_t n_fill = (int32_t)std::min<int64_t>(grid_for(ent_ub, kThreads), 64);
+    const int32_t n_copy = (int32_t)std::max<int64_t>(
+        1, std::min<int64_t>(ceil_div64(nnz, kRelayTile), (int64_t)kRelayGroupsPerCu * cus));
+    k_relayout_fill<<<(unsigned)(n_fill + n_copy), kThreads, 0, st>>>(
+        n_fill, n_copy, (int32_t)n, nnz, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
+        p->colidx_s, p->vals_s, keys, cls, seg, info, W, Z, DB, H, p->meta, ent_ub,
+        (int32_t)hub_ub, p->hub_chunk_off, p->order, dmax, kTailCap, INT32_MAX, err);
+    if ((rc = check_launch("k_relayout_fill"))) return rc;
+    short_done = true;
   }
   if (n > 0 && !short_done) {
     // Stable LSD radix sort of row ids by degree, 8-bit digits. Unless the

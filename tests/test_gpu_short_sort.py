@@ -1,7 +1,9 @@
-"""The plan's two degree sorts give the same plan.
+"""The plan's degree sorts give the same plan.
 
-With W * Z >= 255 the plan first sorts by min(degree, 255) in one pass and
-sorts the rows of degree >= 255 (the tail, at most 16384 rows) in a single
+Graphs of at most 16384 rows and 2^17 nonzeros are planned by one workgroup up
+to the partition (AGCN_TEST_TINY=0 turns that off). Otherwise, with
+W * Z >= 255, the plan first sorts by min(degree, 255) in one pass and sorts
+the rows of degree >= 255 (the tail, at most 16384 rows) in a single
 workgroup; otherwise, or with a larger tail, it runs the multi-pass radix sort
 (AGCN_TEST_TAIL_CAP=-1 forces that, after the first short pass, on any graph;
 the short sort's second half is then queued all the same and must leave the
@@ -49,19 +51,21 @@ def _env(**kv):
                 os.environ[k] = v
 
 
-# (tail cap, early-check limit): the short sort with the early column check
-# (the default on these graphs) and with the relayout's, the multi-pass sort
-# after a short attempt under either.
-PATHS = [(None, None), (None, "0"), ("-1", None), ("-1", "0")]
+# (tail cap, early-check limit, tiny plan): the default (the single-workgroup
+# plan on a small graph, else the short sort with the early column check); the
+# short sort with the early column check and with the relayout's; the
+# multi-pass sort after a short attempt under either.
+PATHS = [(None, None, None), (None, None, "0"), (None, "0", "0"), ("-1", None, "0"),
+         ("-1", "0", "0")]
+MULTI = 3  # index of the first multi-pass path
 
 
 def _both(g, **kw):
     """Plans of g along every path of PATHS, each checked against the oracle
-    and against the others; returns the short-sort (default) and the
-    multi-pass plans."""
+    and against the others; returns the default and a multi-pass plan."""
     out = []
-    for cap, early in PATHS:
-        with _env(AGCN_TEST_TAIL_CAP=cap, AGCN_TEST_EARLY_CHECK_NNZ=early):
+    for cap, early, tiny in PATHS:
+        with _env(AGCN_TEST_TAIL_CAP=cap, AGCN_TEST_EARLY_CHECK_NNZ=early, AGCN_TEST_TINY=tiny):
             p = _plan(g, **kw)
         out.append((p, assert_plan_matches_oracle(p, g)))
     p0, e0 = out[0]
@@ -69,10 +73,10 @@ def _both(g, **kw):
         for k in ("perm", "rowptr_s", "colidx_s", "meta"):
             assert np.array_equal(e0[k], e[k]), k
         assert p0.stats.n_entries == p.stats.n_entries
-    for p, _ in out[1:]:
-        if p is not out[2][0]:
+    for i, (p, _) in enumerate(out):
+        if i not in (0, MULTI):
             p.destroy()
-    return p0, out[2][0]
+    return p0, out[MULTI][0]
 
 
 @pytest.mark.parametrize("W,Z", [(16, 32), (12, 32), (15, 17), (16, 256), (32, 8)])
@@ -122,10 +126,10 @@ def test_tail_at_the_cap(m):
     p.destroy()
 
 
-@pytest.mark.parametrize("cap,early", PATHS)
-def test_invalid_csr_through_the_short_sort(cap, early):
+@pytest.mark.parametrize("cap,early,tiny", PATHS)
+def test_invalid_csr_through_the_short_sort(cap, early, tiny):
     g = _mixed(950, n=5000)
-    with _env(AGCN_TEST_TAIL_CAP=cap, AGCN_TEST_EARLY_CHECK_NNZ=early):
+    with _env(AGCN_TEST_TAIL_CAP=cap, AGCN_TEST_EARLY_CHECK_NNZ=early, AGCN_TEST_TINY=tiny):
         for where in (0, len(g.colidx) // 2, len(g.colidx) - 1):
             ci = g.colidx.copy()
             ci[where] = g.n_cols if where else -1   # one column out of range
@@ -145,10 +149,12 @@ def test_invalid_csr_through_the_short_sort(cap, early):
         p.destroy()
 
 
-def test_inputs_overwritten_in_stream_order_after_create():
-    # The short sort's last relayout still reads the inputs when the call
-    # returns; work queued after it on the same stream may overwrite them.
-    g = _mixed(960, n=30000)
+@pytest.mark.parametrize("n", [30000, 3000])
+def test_inputs_overwritten_in_stream_order_after_create(n):
+    # The last relayout (of the short sort, or after the single-workgroup plan
+    # of a small graph) still reads the inputs when the call returns; work
+    # queued after it on the same stream may overwrite them.
+    g = _mixed(960, n=n)
     dev = torch.device("cuda:0")
     rp = torch.from_numpy(g.rowptr.copy()).to(dev)
     ci = torch.from_numpy(g.colidx.copy()).to(dev)
