@@ -153,7 +153,9 @@ void agcn_default_params(agcn_plan_params* p);
  * AGCN_TEST_EARLY_CHECK_NNZ=k sets to k the largest graph whose column
  * indices the short sort checks before its last relayout, returning while
  * that relayout runs (larger graphs: checked by the relayout, and the call
- * returns after it; the plan is the same either way). */
+ * returns after it; the plan is the same either way); AGCN_TEST_TINY=0 keeps
+ * graphs of at most 16384 rows and 2^17 nonzeros off the single-workgroup
+ * plan (the same plan again). */
 int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t nnz,
                      const int32_t* d_rowptr, const int32_t* d_colidx, const float* d_vals,
                      const agcn_plan_params* params, void* stream);

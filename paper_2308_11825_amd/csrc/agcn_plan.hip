@@ -31,6 +31,11 @@
 //                   it may still run when agcn_plan_create returns
 // The last two are queued without waiting for the read-back: they read the
 // tail size from the device and return at once if it is over the cap.
+// A graph of at most kTinyMaxRows rows and kTinyMaxNnz nonzeros instead runs
+//   k_plan_tiny     one workgroup: the input checks, every row sorted by degree
+//                   (the tail's code), row pointers, class starts, segment scan
+//                   and summary with the done flag
+//   k_relayout_fill as above, over the whole sorted CSR
 // Otherwise (the multi-pass sort):
 //   radix passes    stable LSD radix sort of row ids by degree, 8-bit digits:
 //                   k_radix_hist -> exclusive scan -> k_radix_scatter. Buffers
