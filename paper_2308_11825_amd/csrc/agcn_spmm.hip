@@ -271,6 +271,41 @@ __global__ __launch_bounds__(1024) void k_hub_reduce(const int32_t* __restrict__
   }
 }
 
+// Hub rows of at most MC chunks (every hub row of a plan whose maximum degree
+// is at most MC * H): one vwarp of L lanes per (hub row, slice), each lane
+// loading all of the row's chunk partials at once and adding them in chunk
+// order. The tree of k_hub_reduce leaves most of its 16 lane groups idle on
+// such rows and pays four barriers; the sum here is just as fixed (a
+// different order, so Y may differ from the tree's in the last bits).
+constexpr int kFlatThreads = 64;
+constexpr int kFlatMaxChunks = 32;
+
+template <int VW, int MC>
+__global__ __launch_bounds__(kFlatThreads) void k_hub_reduce_flat(
+    const int32_t* __restrict__ hub_chunk_off, int32_t hub_first_row,
+    const int32_t* __restrict__ perm, const float* __restrict__ ws, int32_t F,
+    float* __restrict__ Y, int64_t ldy, int32_t col_base, int32_t slice_cols, int32_t L,
+    int32_t n_hub, int32_t act) {
+  using V = typename VecOf<VW>::T;
+  const int64_t t = (int64_t)blockIdx.x * kFlatThreads + threadIdx.x;
+  const int32_t h = (int32_t)(t / L);
+  const int l = (int)(t - (int64_t)h * L);
+  if (h >= n_hub) return;
+  const int32_t col0 = col_base + (int32_t)blockIdx.y * slice_cols;
+  const int32_t c0 = hub_chunk_off[h];
+  const int32_t nc = hub_chunk_off[h + 1] - c0;
+  V part[MC];
+#pragma unroll
+  for (int k = 0; k < MC; ++k)
+    if (k < nc) part[k] = reinterpret_cast<const V*>(ws + (int64_t)(c0 + k) * F + col0)[l];
+  V acc = V(0.0f);
+#pragma unroll
+  for (int k = 0; k < MC; ++k)
+    if (k < nc) acc += part[k];
+  V* yr = reinterpret_cast<V*>(Y + (int64_t)perm[hub_first_row + h] * ldy + col0);
+  __builtin_nontemporal_store(act_v(acc, act), yr + l);
+}
+
 // Small plans (no hub rows, every degree <= min(Z, kSmallMaxDeg), few rows):
 // the whole launch is a chain of dependent memory round trips on a mostly idle
 // GPU, so this path drops the two that k_spmm adds before its gathers (the
@@ -611,9 +646,28 @@ void dispatch_spmm(const SpmmArgs& a, int L, int n_slices, int col_base, int sli
   }
 }
 
+template <int VW, int MC>
+void launch_hub_flat(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols) {
+  const agcn_plan* p = a.p;
+  dim3 grid((unsigned)ceil_div64((int64_t)p->n_hub_rows * L, kFlatThreads), (unsigned)n_slices);
+  k_hub_reduce_flat<VW, MC><<<grid, kFlatThreads, 0, a.st>>>(
+      p->hub_chunk_off, p->hub_first_row, p->perm, a.ws, a.F, a.Y, a.ldy, col_base, slice_cols, L,
+      p->n_hub_rows, a.act);
+}
+
 template <int VW>
 void launch_hub(const SpmmArgs& a, int L, int n_slices, int col_base, int slice_cols) {
   const agcn_plan* p = a.p;
+  // The flat kernel when every hub row has few chunks and the launch covers
+  // several slices (sweep_powerlaw, 7 chunks at most, per launch: 9.5 against
+  // 13.8 us at 8 slices, 6.3 against 7.8 at 4; at 1 and 2 slices the tree's
+  // one workgroup per row was faster, 4.6 against 5.1 and 5.2 against 5.4).
+  const int64_t max_chunks = ceil_div64(std::max(p->max_deg, 1), p->H);
+  if (max_chunks <= kFlatMaxChunks && n_slices > 2) {
+    if (max_chunks <= 8) return launch_hub_flat<VW, 8>(a, L, n_slices, col_base, slice_cols);
+    if (max_chunks <= 16) return launch_hub_flat<VW, 16>(a, L, n_slices, col_base, slice_cols);
+    return launch_hub_flat<VW, 32>(a, L, n_slices, col_base, slice_cols);
+  }
   int G = 1;
   while (G < 16 && 2 * G * L <= 1024) G *= 2;
   const int T = round_up(G * L, 64);
