@@ -9,7 +9,8 @@
 //                   per-workgroup maximum degree, tail size, lower nonzeros and
 //                   error flags; per-tile histograms of min(deg, 255); clears
 //                   the error word and the scans' tickets; further workgroups
-//                   check the column indices against n_cols
+//                   check the column indices against n_cols (graphs of at most
+//                   kEarlyCheckMaxNnz nonzeros)
 //   scan            bin starts of every (digit, tile); its first tile also
 //                   reduces k_degree's per-workgroup results (every input error
 //                   is then known) and writes the maximum degree, the tail size
@@ -30,7 +31,10 @@
 //                   first), side by side with the sorted CSR of the tail's rows;
 //                   it may still run when agcn_plan_create returns
 // The last two are queued without waiting for the read-back: they read the
-// tail size from the device and return at once if it is over the cap.
+// tail size from the device and return at once if it is over the cap. On a
+// graph of more than kEarlyCheckMaxNnz nonzeros the relayout copies check the
+// column indices instead of k_degree, and k_publish after k_relayout_fill sets
+// the done flag.
 // A graph of at most kTinyMaxRows rows and kTinyMaxNnz nonzeros instead runs
 //   k_plan_tiny     one workgroup: the input checks, every row sorted by degree
 //                   (the tail's code), row pointers, class starts, segment scan
