@@ -121,11 +121,12 @@ void agcn_default_params(agcn_plan_params* p);
  * queued on `stream` has run (free or overwrite them in `stream`'s order, or
  * after synchronising it). Work is
  * ordered on `stream`. The call waits on the host, by polling pinned memory,
- * for two results the device writes there: the maximum degree (with the
- * number of rows of degree >= 255, which chooses between the plan's two
- * degree sorts) and the number of metadata entries. The plan's last kernels may still run on `stream` when
- * it returns; later work on that stream comes after them, and agcn_spmm* on
- * another stream waits for them. The warp-level plan (AGCN_PLAN_WARP_LEVEL)
+ * for results the device writes there: the maximum degree with the number of
+ * rows of degree >= 255 (which chooses between the plan's degree sorts; the
+ * kernels that depend on it are queued before it arrives) and the summary
+ * with the number of metadata entries. The plan's last kernels may still run
+ * on `stream` when it returns; later work on that stream comes after them,
+ * and agcn_spmm* on another stream waits for them. The warp-level plan (AGCN_PLAN_WARP_LEVEL)
  * synchronises `stream` instead. `stream` must remain valid until the plan is
  * destroyed (agcn_plan_destroy marks the plan's last work on it).
  *
