@@ -80,6 +80,48 @@ def kernel_bytes(st, F, n_ref, variant="block"):
     return k7, k8
 
 
+# Hub-row windows (plans whose agcn_plan_stats.hub_windows > 0, at F >= 64 on
+# the float4 path): the library's launch shape, as agcn_spmm.hip computes it.
+WIN_COLS, WIN_ROWS, WIN_SLICE, WIN_TARGET_GROUPS = 512, 1024, 64, 512
+# LDS read bandwidth of the chip (the window kernel's gathers are LDS reads):
+# 256 bytes per clock per CU, 256 CUs, 2.4 GHz. A read-only probe of ds_read_b128
+# measured 135.7 TB/s (221 B/clk/CU) conflict-free and 111.5 TB/s with the
+# window kernel's pattern (16-lane groups reading random 256-byte rows).
+LDS_PEAK_GBPS = 256 * 256 * 2.4
+
+
+def windows_used(st, F, variant="block"):
+    return variant == "block" and st.hub_windows > 0 and F >= 64 and F % 4 == 0
+
+
+def win_shape(st, F):
+    n_slices = -(-F // WIN_SLICE)
+    n_b = -(-st.n_hub_rows // WIN_ROWS)
+    want = max(1, -(-WIN_TARGET_GROUPS // max(1, n_slices * n_b)))
+    G = max(1, -(-st.hub_windows // want))
+    return n_slices, n_b, G, -(-st.hub_windows // G)
+
+
+def window_bytes(st, F, hub):
+    """Algorithmic HBM bytes of the hub phase on windows (k_hub_win +
+    k_hub_win_reduce), and of the aggregation of the other rows (k_spmm).
+
+    k_hub_win + reduce: 8 per hub nonzero; X once per row batch (4 F per X
+                  row); 8 per (hub row, window, slice) of window ranges;
+                  (4 F + 4) per (hub row, window group) written and read
+                  back (partial row, stray flag); 4 F + 4 per hub row (Y, perm)
+    k_spmm:       as kernel_bytes, over the rows of degree <= deg_bound only
+    hub: dict(hub_nnz, n_cols, low_nnz, low_ref, low_entries)."""
+    n_slices, n_b, G, n_grp = win_shape(st, F)
+    nh = st.n_hub_rows
+    b_hub = (8 * hub["hub_nnz"] + 4 * F * hub["n_cols"] * n_b + 8 * nh * st.hub_windows * n_slices
+             + 2 * (4 * F + 4) * nh * n_grp + (4 * F + 4) * nh)
+    nonhub = st.n_rows - nh
+    b_low = (8 * hub["low_nnz"] + 16 * hub["low_entries"] + 4 * nonhub + 4 * F * hub["low_ref"]
+             + 4 * F * nonhub)
+    return b_low, b_hub
+
+
 def gather_requests(st, F):
     """Gather requests one aggregation launch issues for X: every nonzero
     loads its X row's piece of every column slice of 32 floats (one 128-byte
@@ -442,7 +484,7 @@ def main():
     probe = agcn.agcn_plan_create(g.n_rows, g.n_cols, g.nnz, d_rowptr.data_ptr(),
                                   d_colidx.data_ptr(), d_vals.data_ptr(), prm, sh)
     st = agcn.agcn_plan_info(probe)
-    ws_bytes = agcn.agcn_spmm_workspace_size(probe, max(Fs))
+    ws_bytes = max(agcn.agcn_spmm_workspace_size(probe, F) for F in Fs)
     agcn.agcn_plan_destroy(probe)
     ws = torch.empty(max(1, (ws_bytes + 3) // 4), dtype=torch.float32, device=dev)
     log(f"plan: entries={st.n_entries} hub_rows={st.n_hub_rows} hub_chunks={st.n_hub_chunks} "
@@ -525,15 +567,25 @@ def main():
     torch.cuda.synchronize()
     plan_alone_ms = pe0.elapsed_time(pe1) / 5
 
+    hub = None
+    if st.hub_windows > 0:
+        deg = np.diff(g.rowptr.astype(np.int64))
+        low_rows = deg <= st.deg_bound
+        low_cols = g.colidx[np.repeat(low_rows, deg)]
+        hub = {"hub_nnz": int(deg[~low_rows].sum()), "n_cols": g.n_cols,
+               "low_nnz": int(deg[low_rows].sum()), "low_entries": st.hub_first_entry,
+               "low_ref": int(np.count_nonzero(np.bincount(low_cols, minlength=g.n_cols)))}
     per_f = {}
     flops_step = 0.0
     exec_ms_sum = 0.0
     for F in Fs:
         marks = [ev[F] for ev in events if F in ev]
         k7 = np.array([b.elapsed_time(m) for b, m, _ in marks])
-        # hub-row reduction and the launch gap before it
+        # hub phase (hub-chunk reduction, or the windows and their reduction)
+        # and the launch gap before it
         k8 = np.array([m.elapsed_time(a) for _, m, a in marks])
-        b7, b8 = kernel_bytes(st, F, n_ref, args.variant)
+        win = windows_used(st, F, args.variant)
+        b7, b8 = window_bytes(st, F, hub) if win else kernel_bytes(st, F, n_ref, args.variant)
         ex_ms = float(np.mean(k7 + k8))
         exec_ms_sum += ex_ms
         fl = 2.0 * g.nnz * F
@@ -546,6 +598,15 @@ def main():
             "frac_hbm": round((b7 + b8) / (ex_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
             "spmm_bytes": int(b7), "spmm_GBps": round(b7 / (k7.mean() * 1e-3) / 1e9, 1),
         }
+        if win:
+            # k_spmm covers the rows of degree <= deg_bound; the hub phase is
+            # k_hub_win + k_hub_win_reduce, whose X reads are LDS reads (4 F
+            # bytes per hub nonzero)
+            lds = 4 * F * hub["hub_nnz"]
+            per_f[F].update({"hub_path": "windows", "hub_bytes": int(b8),
+                             "hub_GBps": round(b8 / (k8.mean() * 1e-3) / 1e9, 1),
+                             "hub_lds_bytes": int(lds),
+                             "hub_lds_GBps": round(lds / (k8.mean() * 1e-3) / 1e9, 1)})
     # serial steps: the plan plus the launch gaps between executes; overlapped
     # steps: whatever of the plan and the gaps the executes did not hide
     plan_ms = ms_step - exec_ms_sum
@@ -576,7 +637,9 @@ def main():
         pass
     # Model ceiling of any kernel that gathers X rows per nonzero: its gather
     # requests all served by L2 at the measured L2 gather rate.
-    req = float(np.mean([gather_requests(st, F) for F in dom_F]))
+    req = float(np.mean([gather_requests(st, F) * (hub["low_nnz"] / st.nnz
+                                                   if windows_used(st, F, args.variant) else 1.0)
+                         for F in dom_F]))
     cap_ms = req / L2_GATHER_REQ_PER_S * 1e3
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBPS, 4), "traffic": traffic,
@@ -586,12 +649,31 @@ def main():
                                   "frac_at_cap": round(mean_bytes / (cap_ms * 1e-3) / 1e9
                                                        / HBM_PEAK_GBPS, 4),
                                   "achieved_over_cap": round(cap_ms / mean_ms, 4)}}
-    if traffic is not None:
+    win_F = [F for F in Fs if windows_used(st, F, args.variant)]
+    win_roof = bool(win_F) and (sum(per_f[F]["hub_reduce_ms"] for F in win_F)
+                                > sum(per_f[F]["spmm_ms"] for F in dom_F))
+    if win_roof:
+        # The hub windows dominate: their bound is the LDS reads of the staged
+        # X windows. The marks frame the whole hub phase (k_hub_win,
+        # k_hub_win_reduce and the gap before them), so achieved is a lower
+        # bound for k_hub_win alone.
+        lds_b = float(np.mean([per_f[F]["hub_lds_bytes"] for F in win_F]))
+        hub_ms = float(np.mean([per_f[F]["hub_reduce_ms"] for F in win_F]))
+        lds_ach = lds_b / (hub_ms * 1e-3) / 1e9
+        hbm_b = float(np.mean([per_f[F]["hub_bytes"] for F in win_F]))
+        roofline = {"bound": "lds", "achieved": round(lds_ach, 1), "peak": LDS_PEAK_GBPS,
+                    "unit": "GB/s", "frac": round(lds_ach / LDS_PEAK_GBPS, 4), "traffic": None,
+                    "kernel": "k_hub_win", "launches_per_step": len(win_F), "F": win_F,
+                    "alg_bytes_per_launch": int(lds_b), "avg_launch_ms": round(hub_ms, 5),
+                    "timed": "k_hub_win + k_hub_win_reduce",
+                    "hbm_bytes_per_launch": int(hbm_b),
+                    "hbm_GBps": round(hbm_b / (hub_ms * 1e-3) / 1e9, 1)}
+    if traffic is not None and not win_roof:
         # counter-measured bytes past L2 (Infinity Cache hits included) over the same time
         tg = traffic / (mean_ms * 1e-3) / 1e9
         roofline["past_l2_GBps"] = round(tg, 1)
         roofline["past_l2_frac_of_hbm_peak"] = round(tg / HBM_PEAK_GBPS, 4)
-    if past_l2_req:
+    if past_l2_req and not win_roof:
         # the binding ceiling: random line requests past L2 (the L2 misses)
         rate = past_l2_req / (mean_ms * 1e-3)
         roofline["past_l2_request_cap"] = {
@@ -615,7 +697,8 @@ def main():
     copy_GBps = 3 * 2 * src.numel() * 4 / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del src, dst
     roofline["copy_GBps"] = round(copy_GBps, 1)
-    roofline["frac_of_copy"] = round(ach / copy_GBps, 4)
+    if not win_roof:
+        roofline["frac_of_copy"] = round(ach / copy_GBps, 4)
     log(f"copy probe: 1 GiB device copy at {copy_GBps:.0f} GB/s (read + write)")
 
     out = {
@@ -645,8 +728,13 @@ def main():
         agcn.agcn_plan_destroy(plan)
         # the dominant kernel's roofline fraction from its cold launches (X, the
         # CSR and Y outside L2 and the Infinity Cache when each launch starts)
-        cold_ms = float(np.mean([cw[F]["cold"]["spmm"]["median_ms"] for F in dom_F]))
-        roofline["frac_cold"] = round(mean_bytes / (cold_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)
+        if win_roof:  # the hub phase of the cold executes: the execute minus k_spmm
+            cold_ms = float(np.mean([cw[F]["cold"]["median_ms"] - cw[F]["cold"]["spmm"]["median_ms"]
+                                     for F in win_F]))
+            roofline["frac_cold"] = round(lds_b / (cold_ms * 1e-3) / 1e9 / LDS_PEAK_GBPS, 4)
+        else:
+            cold_ms = float(np.mean([cw[F]["cold"]["spmm"]["median_ms"] for F in dom_F]))
+            roofline["frac_cold"] = round(mean_bytes / (cold_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)
         roofline["avg_launch_ms_cold"] = round(cold_ms, 5)
     if args.rocsparse:
         log("rocSPARSE comparison ...")

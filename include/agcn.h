@@ -104,6 +104,8 @@ typedef struct agcn_plan_stats {
   int32_t max_wave_nzs;
   uint32_t flags;          /* the plan's AGCN_PLAN_* flags */
   size_t device_bytes;     /* device memory the plan holds */
+  int32_t hub_windows;     /* column windows of 512 columns over which the hub rows are
+                              aggregated at F >= 64 (0: hub chunks at every F) */
 } agcn_plan_stats;
 
 typedef struct agcn_plan* agcn_plan_t;

@@ -62,7 +62,8 @@ class PlanStats(ctypes.Structure):
                 ("hub_first_row", ctypes.c_int32), ("deg_bound", ctypes.c_int32),
                 ("hub_chunk_nnz", ctypes.c_int32), ("max_deg", ctypes.c_int32),
                 ("max_block_waves", ctypes.c_int32), ("max_wave_nzs", ctypes.c_int32),
-                ("flags", ctypes.c_uint32), ("device_bytes", ctypes.c_size_t)]
+                ("flags", ctypes.c_uint32), ("device_bytes", ctypes.c_size_t),
+                ("hub_windows", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

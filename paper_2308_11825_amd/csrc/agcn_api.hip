@@ -407,11 +407,7 @@ int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t n
 int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes) {
   if (plan == nullptr || bytes == nullptr) return fail(AGCN_ERR_INVALID_ARGUMENT, "NULL argument");
   if (F < 1) return fail(AGCN_ERR_INVALID_ARGUMENT, "F must be >= 1");
-  const int64_t chunks =
-      plan->flags & AGCN_PLAN_WARP_LEVEL
-          ? 2 * agcn::warp_level_blocks(plan)
-          : (plan->n_hub_rows > 0 ? (int64_t)plan->n_entries - plan->hub_first_entry : 0);
-  *bytes = (size_t)chunks * (size_t)F * sizeof(float);
+  *bytes = std::max(agcn::chunk_workspace_bytes(plan, F), agcn::win_workspace_bytes(plan, F));
   return AGCN_OK;
 }
 
@@ -443,6 +439,9 @@ int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
   size_t ws_need = 0;
   agcn_spmm_workspace_size(plan, F, &ws_need);
   if (noalloc) {
+    // The hub windows only when their partials fit the fixed workspace; the
+    // hub chunks need less.
+    if (ws_need > agcn::kNoallocScratchBytes) ws_need = agcn::chunk_workspace_bytes(plan, F);
     if (ws_need > agcn::kNoallocScratchBytes)
       return fail(AGCN_ERR_UNSUPPORTED,
                   "agcn_spmm_noalloc: this plan needs " + std::to_string(ws_need) +
@@ -479,7 +478,7 @@ int spmm_checked(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
     const hipError_t e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), ready, 0);
     if (e != hipSuccess) return agcn::hip_fail(e, "hipStreamWaitEvent(plan ready)");
   }
-  const int rc = agcn::run_spmm(plan, F, d_X, ldx, d_Y, ldy, static_cast<float*>(d_ws),
+  const int rc = agcn::run_spmm(plan, F, d_X, ldx, d_Y, ldy, static_cast<float*>(d_ws), ws_need,
                                 static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(ev_begin),
                                 static_cast<hipEvent_t>(ev_mid), static_cast<hipEvent_t>(ev_end),
                                 epilogue);
@@ -613,6 +612,7 @@ int agcn_plan_info(agcn_plan_t plan, agcn_plan_stats* s) {
   s->max_wave_nzs = plan->Z;
   s->flags = plan->flags;
   s->device_bytes = plan->bytes;
+  s->hub_windows = plan->n_win;
   return AGCN_OK;
 }
 

@@ -47,6 +47,27 @@ constexpr int kMaxBlockWaves = 32;
 // Feature columns one workgroup covers: 64 lanes x (4 or 1) floats.
 constexpr int kSliceLanes = 64;
 
+// Column windows of the hub rows. A plan whose hub rows average at least
+// kWinMinPairs nonzeros per (hub row, window of kWinCols columns), over at
+// least kWinMinHubRows hub rows, gets a table of where each hub row's
+// nonzeros of each window start; executes at F >= kWinMinF then aggregate
+// the hub rows window by window from X staged in LDS (k_hub_win) instead of
+// by hub chunks. A workgroup holds kWinRows hub rows: 64 lane groups of 16
+// lanes, kWinRowsPerGroup rows each.
+constexpr int32_t kWinCols = 512;
+constexpr int32_t kWinMinPairs = 16;
+constexpr int32_t kWinMinHubRows = 64;
+constexpr int32_t kWinMinF = 64;
+constexpr int32_t kWinSliceCols = 64;
+constexpr int32_t kWinRowsPerGroup = 16;
+constexpr int32_t kWinRows = 64 * kWinRowsPerGroup;
+// Workgroups a launch aims for (one fits per CU: about two rounds on 256 CUs).
+constexpr int64_t kWinTargetGroups = 512;
+
+// AGCN_HUB_WINDOWS=0 builds no window table (plans then aggregate hub rows by
+// chunks at every F); read at each agcn_plan_create.
+bool hub_windows_setting();
+
 }  // namespace agcn
 
 struct agcn_plan {
@@ -67,6 +88,15 @@ struct agcn_plan {
   int32_t* order = nullptr;         // [entries] launch order of k_spmm (entry per workgroup)
   bool hub_wide = false;            // hub chunks of long rows launched in column order
   int32_t* group_off = nullptr;     // warp-level plans: [n_rows + 1] first group of each row
+  // Hub-row windows (n_win > 0 only when built): win_tab[k * n_hub_rows + h],
+  // k in [0, n_win], is the position in colidx_s of the first nonzero of
+  // sorted hub row hub_first_row + h whose column is >= k * kWinCols (a lower
+  // bound by search; [0] and [n_win] are the row's ends). Positions do not
+  // decrease in k even where a row's columns do not ascend, so the windows
+  // always partition each row. It lies in the block at `base`, over the
+  // working buffers of the plan's construction.
+  int32_t n_win = 0;
+  int32_t* win_tab = nullptr;
   uint32_t* err_word = nullptr;     // the plan kernels' error flags (device)
   hipEvent_t ready = nullptr;       // the plan's kernels done (created with the plan,
                                     // recorded on first need: plan_ready_event; use_mu)
@@ -121,9 +151,25 @@ inline int64_t warp_level_blocks(const agcn_plan* p) {
 }
 
 // Execute (agcn_spmm.hip). act: 0 = identity, 1 = ReLU on every Y write.
+// ws holds ws_bytes; the hub windows run when the plan has them, F >=
+// kWinMinF, the float4 path applies and ws_bytes >= win_workspace_bytes.
 int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,
-             float* ws, hipStream_t stream, hipEvent_t ev_begin, hipEvent_t ev_mid,
-             hipEvent_t ev_end, int32_t act);
+             float* ws, size_t ws_bytes, hipStream_t stream, hipEvent_t ev_begin,
+             hipEvent_t ev_mid, hipEvent_t ev_end, int32_t act);
+
+// Launch shape of the hub windows at F: n_slices slices of kWinSliceCols
+// columns, n_b batches of kWinRows hub rows, the plan's n_win windows taken G
+// at a time by n_grp window groups (G chosen so that n_b * n_slices * n_grp is
+// about kWinTargetGroups).
+struct WinShape {
+  int32_t n_slices, n_b, G, n_grp;
+};
+WinShape win_shape(const agcn_plan* p, int32_t F);
+// Workspace of the hub windows at F (0 when the plan has none or F < kWinMinF):
+// one partial row of F floats per (hub row, window group).
+size_t win_workspace_bytes(const agcn_plan* p, int32_t F);
+// Workspace of the hub chunks (and warp-level blocks) at F.
+size_t chunk_workspace_bytes(const agcn_plan* p, int32_t F);
 
 // H = X W on matrix cores (agcn_linear.hip).
 int run_linear(int64_t n, int32_t fin, int32_t fout, const float* X, int64_t ldx, const float* W,

@@ -1635,6 +1635,99 @@ __global__ __launch_bounds__(kThreads) void k_order_fill(int32_t* __restrict__ o
     order[i] = hub_first - 1 - (int32_t)(i - n_chunks);
 }
 
+// Hub-row windows: win_tab[k * n_hub + h] = first position of sorted hub row h
+// whose column is >= k * kWinCols (k = 0 and k = n_win give the row's ends).
+// search_lb: an 8-way search over [lo, hi) -- each round loads the last
+// element of the first seven of eight equal parts at once and keeps the part
+// after the m whose element is below the key (about 6 rounds for 10^5
+// elements where a binary search chains 17 loads); at most 8 elements left are
+// counted. Every choice is a count of elements below the key, which does not
+// decrease as the key grows, so over a fixed range the result does not
+// decrease in the key, whether or not the columns ascend.
+__device__ inline int32_t search_lb(const int32_t* __restrict__ a, int32_t lo, int32_t hi,
+                                    int64_t key) {
+  while (hi - lo > 8) {
+    const int64_t n = hi - lo;
+    int32_t m = 0;
+#pragma unroll
+    for (int q = 1; q < 8; ++q) m += a[lo + (int32_t)((n * q) >> 3) - 1] < key ? 1 : 0;
+    const int32_t nlo = lo + (int32_t)((n * m) >> 3);
+    hi = m < 7 ? lo + (int32_t)((n * (m + 1)) >> 3) - 1 : hi;
+    lo = nlo;
+  }
+  int32_t below = 0;
+  for (int32_t j = lo; j < hi; ++j) below += a[j] < key ? 1 : 0;
+  return lo + below;
+}
+
+// Windows one wave of k_hub_win_table covers: kWinTableLanes per lane.
+constexpr int kWinTableLanes = 4;
+constexpr int32_t kWinTableSpan = 64 * kWinTableLanes;
+
+// One wave per (hub row, kWinTableSpan consecutive windows from k0): every lane
+// first brackets the wave's positions by two searches over the whole row (the
+// same addresses in every lane, one request each), [b0, b1] = the positions
+// of k0 and k0 + kWinTableSpan; lane t then searches windows k0 + t + 64 q
+// within the bracket, the kWinTableLanes searches advancing side by side so
+// their loads are in flight together (the kernel waits on load latency, not
+// bandwidth). b1 is the next wave's b0, so positions do not decrease across
+// waves either, and the windows partition every row.
+__global__ __launch_bounds__(kThreads) void k_hub_win_table(const int32_t* __restrict__ rowptr_s,
+                                                            const int32_t* __restrict__ colidx_s,
+                                                            int32_t hub_first_row, int32_t n_hub,
+                                                            int32_t n_win,
+                                                            int32_t* __restrict__ win_tab) {
+  constexpr int Q = kWinTableLanes;
+  const int32_t per_row = n_win / kWinTableSpan + 1;  // waves per row: windows 0 .. n_win
+  const int64_t waves = (int64_t)n_hub * per_row;
+  const int lane = threadIdx.x & 63;
+  const int64_t stride = (int64_t)gridDim.x * (kThreads / 64);
+  for (int64_t w = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6); w < waves;
+       w += stride) {
+    const int32_t h = (int32_t)(w / per_row);
+    const int32_t k0 = (int32_t)(w - (int64_t)h * per_row) * kWinTableSpan;
+    const int32_t s = rowptr_s[hub_first_row + h], e = rowptr_s[hub_first_row + h + 1];
+    const int32_t b0 = k0 == 0 ? s : search_lb(colidx_s, s, e, (int64_t)k0 * kWinCols);
+    const int32_t b1 = k0 + kWinTableSpan >= n_win
+                           ? e
+                           : search_lb(colidx_s, s, e, (int64_t)(k0 + kWinTableSpan) * kWinCols);
+    int64_t key[Q];
+    int32_t lo[Q], hi[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      key[q] = (int64_t)(k0 + q * 64 + lane) * kWinCols;
+      lo[q] = b0;
+      hi[q] = b1;
+    }
+    // the 8-way search of search_lb, Q chains in step
+    for (bool more = b1 - b0 > 8; more;) {
+      more = false;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int64_t n = hi[q] - lo[q];
+        if (n > 8) {
+          int32_t m = 0;
+#pragma unroll
+          for (int t = 1; t < 8; ++t)
+            m += colidx_s[lo[q] + (int32_t)((n * t) >> 3) - 1] < key[q] ? 1 : 0;
+          const int32_t nlo = lo[q] + (int32_t)((n * m) >> 3);
+          hi[q] = m < 7 ? lo[q] + (int32_t)((n * (m + 1)) >> 3) - 1 : hi[q];
+          lo[q] = nlo;
+          more = more || hi[q] - lo[q] > 8;
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int32_t k = k0 + q * 64 + lane;
+      if (k > n_win) continue;
+      int32_t below = 0;
+      for (int32_t j = lo[q]; j < hi[q]; ++j) below += colidx_s[j] < key[q] ? 1 : 0;
+      win_tab[(int64_t)k * n_hub + h] = k == 0 ? s : (k == n_win ? e : lo[q] + below);
+    }
+  }
+}
+
 // --- warp-level partition (the baseline of the paper's Table II) -----------
 
 // Groups per row: ceil(deg / Z), at least one so an empty row is still written.
@@ -1789,6 +1882,11 @@ int scan_exclusive(const int32_t* in, int64_t n, int32_t* out, int32_t* total, i
 
 // Hub-chunk launch order by column (AGCN_HUB_ORDER=0 keeps the plain
 // heaviest-first order, for measurements).
+bool hub_windows_setting() {
+  const char* s = std::getenv("AGCN_HUB_WINDOWS");
+  return s == nullptr || std::atoi(s) != 0;
+}
+
 bool hub_order_setting() {
   static const bool v = [] {
     const char* s = std::getenv("AGCN_HUB_ORDER");
@@ -1982,6 +2080,30 @@ int build_plan_warp_level(agcn_plan* p, const int32_t* d_rowptr, const int32_t* 
   return AGCN_OK;
 }
 
+// The hub rows' column windows, for plans whose hub rows are dense enough
+// (kWinMinPairs nonzeros per row and window on average, counted from the hub
+// chunks: a row of c chunks holds more than (c - 1) * H nonzeros). Queued
+// after the summary read-back, last of the plan's kernels; the table lies in
+// the plan's working buffers (`space`, `cap` bytes). An execute on another
+// stream waits for it as for the plan's other kernels.
+int build_hub_windows(agcn_plan* p, int32_t n_chunks, int32_t* space, size_t cap,
+                      hipStream_t st) {
+  const int64_t n_hub = p->n_hub_rows;
+  if (p->flags != 0 || n_hub < kWinMinHubRows || !hub_windows_setting()) return AGCN_OK;
+  const int64_t n_win = ceil_div64(p->n_cols, kWinCols);
+  const int64_t hub_nnz_lb = ((int64_t)n_chunks - n_hub) * p->H;
+  if (hub_nnz_lb < (int64_t)kWinMinPairs * n_hub * n_win) return AGCN_OK;
+  if ((size_t)(n_win + 1) * (size_t)n_hub * sizeof(int32_t) > cap)
+    return fail(AGCN_ERR_HIP, "internal: hub window table larger than its reserved space");
+  p->win_tab = space;
+  p->n_win = (int32_t)n_win;
+  const int64_t waves = n_hub * ceil_div64(n_win + 1, kWinTableSpan);
+  const unsigned grid = (unsigned)std::min<int64_t>(grid_for(waves, kThreads / 64), 65536);
+  k_hub_win_table<<<grid, kThreads, 0, st>>>(p->rowptr_s, p->colidx_s, p->hub_first_row,
+                                             (int32_t)n_hub, (int32_t)n_win, p->win_tab);
+  return check_launch("k_hub_win_table");
+}
+
 int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_colidx,
                      const float* d_vals, hipStream_t st) {
   const int64_t n = p->n_rows, nnz = p->nnz;
@@ -2011,6 +2133,19 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   const size_t o_keys2 = L.take(4 * n);
   const size_t o_ids2 = L.take(4 * n);
   const size_t o_counts = L.take(4 * n_counts);
+  // The hub rows' window table, when the plan gets one, is written over these
+  // five buffers (its kernel is the plan's last; nothing reads them after the
+  // plan), padded to its largest size: a table is only built when the hub rows
+  // average kWinMinPairs nonzeros per window, so it holds at most
+  // nnz / kWinMinPairs + hub rows entries.
+  const int64_t n_win_max = ceil_div64(p->n_cols, kWinCols);
+  const int64_t win_ub =
+      p->flags == 0 && hub_ub >= kWinMinHubRows
+          ? std::min<int64_t>(hub_ub * (n_win_max + 1), nnz / kWinMinPairs + hub_ub)
+          : 0;
+  const size_t win_span = L.off - o_deg;
+  if ((size_t)(4 * win_ub) > win_span) L.take((size_t)(4 * win_ub) - win_span);
+  const size_t win_cap = std::max<size_t>(win_span, (size_t)(4 * win_ub));
   const size_t o_partials = L.take(4 * n_partials);
   const size_t o_cls = L.take(4 * (DB + 2));
   const size_t o_nb = L.take(4 * S);
@@ -2052,6 +2187,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
   p->meta = reinterpret_cast<int4*>(b + o_meta);
   p->hub_chunk_off = reinterpret_cast<int32_t*>(b + o_hub);
   p->order = reinterpret_cast<int32_t*>(b + o_order);
+  int32_t* const win_space = reinterpret_cast<int32_t*>(b + o_deg);
   int32_t* deg = reinterpret_cast<int32_t*>(b + o_deg);
   int32_t* keys = reinterpret_cast<int32_t*>(b + o_keys);
   int32_t* keys2 = reinterpret_cast<int32_t*>(b + o_keys2);
@@ -2325,7 +2461,8 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     k_order_fill<<<grid_for(p->n_entries, kThreads), kThreads, 0, st>>>(
         p->order, p->n_entries, p->hub_first_entry, n_chunks, sorted_ids, err);
   }
-  return check_launch("launch order");
+  if ((rc = check_launch("launch order"))) return rc;
+  return build_hub_windows(p, n_chunks, win_space, win_cap, st);
 }
 
 }  // namespace

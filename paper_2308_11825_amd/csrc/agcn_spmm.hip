@@ -306,6 +306,199 @@ __global__ __launch_bounds__(kFlatThreads) void k_hub_reduce_flat(
   __builtin_nontemporal_store(act_v(acc, act), yr + l);
 }
 
+// Hub rows over column windows (plans with a window table, F >= kWinMinF).
+// One workgroup of 1024 threads per (row batch, window group, slice of
+// kWinSliceCols columns); the row batches of one window group are adjacent
+// in the grid, so they run side by side and share that part of X in L2. For
+// each of its G windows of kWinCols columns the workgroup stages
+// X[window, slice] (128 KiB) and its rows' ranges in the window in LDS. Each
+// 16-lane group then takes kWinRowsPerGroup rows (batch row group + 64 r):
+// lane l loads one (column, value) pair of a batch of 16 and the group walks
+// the batch with row_newbcast DPP broadcasts, each pair one LDS float4 read
+// and four FMAs per lane (lane l owns columns 4l..4l+3 of the slice). The
+// next batch, of this row or of the next, is loaded before the current one is
+// used. A row's sum stays in registers over the G windows (pairs of a window
+// range alternate between two accumulators, added at the range's end) and
+// one partial row per (hub row, window group) goes to ws; k_hub_win_reduce
+// adds them in window order. Against the hub chunks, which gather every X row
+// of a hub row through L2 (about 27 GB of 128-byte requests for 1.1e8 hub
+// nonzeros at F = 64), X is read once per window group from HBM and the
+// gathers become LDS reads.
+// A row whose columns do not ascend still has its nonzeros split over the
+// windows (the table's positions do not decrease); a batch holding a column
+// outside the current window takes a path that reads those X rows from
+// global memory.
+template <int U>
+__device__ inline int32_t row_bcast(int32_t v) {
+  return __builtin_amdgcn_mov_dpp(v, 0x150 + U, 0xF, 0xF, true);  // row_newbcast:U
+}
+
+template <int U>
+struct WinSteps {
+  // Pairs 0..U-1 of the batch held by the group's lanes (o_l: byte offset of
+  // the pair's X row in the staged window; v_l: the value's bits).
+  __device__ static inline void run(int32_t o_l, int32_t v_l, const char* __restrict__ sxb,
+                                    int32_t l16, f4& a0, f4& a1) {
+    WinSteps<U - 1>::run(o_l, v_l, sxb, l16, a0, a1);
+    const f4 x = *reinterpret_cast<const f4*>(sxb + row_bcast<U - 1>(o_l) + l16);
+    const float v = __int_as_float(row_bcast<U - 1>(v_l));
+    f4& a = ((U - 1) & 1) ? a1 : a0;
+    a.x = __builtin_fmaf(v, x.x, a.x);
+    a.y = __builtin_fmaf(v, x.y, a.y);
+    a.z = __builtin_fmaf(v, x.z, a.z);
+    a.w = __builtin_fmaf(v, x.w, a.w);
+  }
+};
+template <>
+struct WinSteps<0> {
+  __device__ static inline void run(int32_t, int32_t, const char*, int32_t, f4&, f4&) {}
+};
+
+__global__ __launch_bounds__(1024) void k_hub_win(
+    const int32_t* __restrict__ win_tab, int32_t n_hub, int32_t n_win, int32_t G, int32_t n_grp,
+    const int32_t* __restrict__ colidx_s, const float* __restrict__ vals_s,
+    const float* __restrict__ X, int64_t ldx, int32_t n_cols, float* __restrict__ ws, int32_t F) {
+  constexpr int NR = kWinRowsPerGroup;
+  __shared__ f4 sx[kWinCols * 16];
+  __shared__ int32_t s_lo[kWinRows], s_hi[kWinRows];
+  const int32_t hb0 = (int32_t)blockIdx.x * kWinRows;
+  const int32_t kg = (int32_t)blockIdx.y;
+  const int32_t col0 = (int32_t)blockIdx.z * kWinSliceCols;
+  const int32_t cols = min(kWinSliceCols, F - col0);
+  const int t = threadIdx.x;
+  const int lane = t & 63, l = lane & 15;
+  const int32_t grp = (t >> 6) * 4 + (lane >> 4);
+  const int32_t l16 = l * 16;
+  const bool lane_cols = 4 * l < cols;
+  const int32_t k0 = kg * G, k1 = min(n_win, k0 + G);
+  const int32_t n_my = min(kWinRows, n_hub - hb0);
+  const char* sxb = reinterpret_cast<const char*>(sx);
+  f4 acc[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) acc[r] = f4(0.0f);
+  uint32_t stray_rows = 0;  // bit r: a pair of row r fell outside its window
+  for (int32_t k = k0; k < k1; ++k) {
+    __syncthreads();  // the previous window's reads are done
+    for (int i = t; i < kWinCols * 16; i += 1024) {
+      const int32_t xr = k * kWinCols + i / 16;
+      const int q = i % 16;
+      sx[i] = (xr < n_cols && 4 * q < cols)
+                  ? reinterpret_cast<const f4*>(X + (int64_t)xr * ldx + col0)[q]
+                  : f4(0.0f);
+    }
+    for (int i = t; i < n_my; i += 1024) {
+      s_lo[i] = win_tab[(int64_t)k * n_hub + hb0 + i];
+      s_hi[i] = win_tab[(int64_t)(k + 1) * n_hub + hb0 + i];
+    }
+    __syncthreads();
+    if (grp >= n_my) continue;
+    const int32_t cbase = k * kWinCols;
+    // The lane's pair of the batch at [j, end): loaded unconditionally from a
+    // clamped position (no branch around the loads) and used only in the next
+    // iteration, so the loads overlap the current batch's steps.
+    auto load_pair = [&](int32_t j, int32_t end, int32_t& c, int32_t& v, int32_t& in) {
+      in = j + l < end;
+      const int32_t at = in ? j + l : 0;
+      c = colidx_s[at];
+      v = __float_as_int(vals_s[at]);
+    };
+    int32_t s = s_lo[grp], e = s_hi[grp];
+    int32_t c_n, v_n, in_n;
+    load_pair(s, e, c_n, v_n, in_n);
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const int32_t i = grp + r * 64;
+      if (i < n_my) {
+        const bool more = r + 1 < NR && i + 64 < n_my;
+        const int32_t s_nx = more ? s_lo[i + 64] : 0, e_nx = more ? s_hi[i + 64] : 0;
+        f4 a1 = f4(0.0f);
+        for (int32_t j = s; j < e; j += 16) {
+          const int32_t c_c = c_n, v_c = v_n, in_c = in_n;
+          const bool same = j + 16 < e;
+          load_pair(same ? j + 16 : s_nx, same ? e : e_nx, c_n, v_n, in_n);
+          // A column outside the window (a row whose columns do not ascend)
+          // counts zero here; the reduction adds it from X.
+          const bool inside = (uint32_t)(c_c - cbase) < (uint32_t)kWinCols;
+          stray_rows |= (uint32_t)(in_c && !inside) << r;
+          const bool use = in_c && inside;
+          WinSteps<16>::run(use ? (c_c - cbase) * 256 : 0, use ? v_c : 0, sxb, l16, acc[r], a1);
+        }
+        acc[r] += a1;
+        if (s == e) load_pair(s_nx, e_nx, c_n, v_n, in_n);  // its preloaded batch was empty
+        s = s_nx;
+        e = e_nx;
+      }
+    }
+  }
+  // Stray flags after the partial rows, one word per (hub row, window group),
+  // written (0 or 1) by the first slice's workgroups.
+  if (blockIdx.z == 0) {
+    int32_t* flags = reinterpret_cast<int32_t*>(ws + (int64_t)n_hub * n_grp * F);
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const uint64_t any = __ballot((stray_rows >> r) & 1u);
+      const int32_t i = grp + r * 64;
+      if (l == 0 && i < n_my)
+        flags[(int64_t)(hb0 + i) * n_grp + kg] = ((any >> (lane & 48)) & 0xFFFFu) ? 1 : 0;
+    }
+  }
+  if (!lane_cols) return;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int32_t i = grp + r * 64;
+    if (i < n_my)
+      reinterpret_cast<f4*>(ws + ((int64_t)(hb0 + i) * n_grp + kg) * F + col0)[l] = acc[r];
+  }
+}
+
+// Y row of hub row h = the sum of its n_grp window-group partials, in window
+// order (four interleaved chains, kg mod 4, added pairwise), plus, for the
+// window groups flagged by k_hub_win, the pairs that lay outside their
+// window, gathered from X in position order.
+__global__ __launch_bounds__(256) void k_hub_win_reduce(
+    const float* __restrict__ ws, int32_t n_hub, int32_t n_win, int32_t G, int32_t n_grp,
+    int32_t F, const int32_t* __restrict__ win_tab, const int32_t* __restrict__ colidx_s,
+    const float* __restrict__ vals_s, const float* __restrict__ X, int64_t ldx,
+    const int32_t* __restrict__ perm, int32_t hub_first_row, float* __restrict__ Y, int64_t ldy,
+    int32_t act) {
+  const int32_t q = F / 4;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)n_hub * q) return;
+  const int32_t h = (int32_t)(t / q), c4 = (int32_t)(t - (int64_t)h * q);
+  const f4* src = reinterpret_cast<const f4*>(ws + (int64_t)h * n_grp * F) + c4;
+  f4 s0 = f4(0.0f), s1 = f4(0.0f), s2 = f4(0.0f), s3 = f4(0.0f);
+  int32_t kg = 0;
+  for (; kg + 4 <= n_grp; kg += 4) {
+    s0 += src[(int64_t)kg * q];
+    s1 += src[(int64_t)(kg + 1) * q];
+    s2 += src[(int64_t)(kg + 2) * q];
+    s3 += src[(int64_t)(kg + 3) * q];
+  }
+  for (; kg < n_grp; ++kg) s0 += src[(int64_t)kg * q];
+  f4 sum = (s0 + s1) + (s2 + s3);
+  const int32_t* flags = reinterpret_cast<const int32_t*>(ws + (int64_t)n_hub * n_grp * F) +
+                         (int64_t)h * n_grp;
+  for (kg = 0; kg < n_grp; ++kg) {
+    if (flags[kg] == 0) continue;
+    const int32_t k1 = min(n_win, (kg + 1) * G);
+    for (int32_t k = kg * G; k < k1; ++k) {
+      const int32_t lo = win_tab[(int64_t)k * n_hub + h], hi = win_tab[(int64_t)(k + 1) * n_hub + h];
+      for (int32_t j = lo; j < hi; ++j) {
+        const int32_t c = colidx_s[j];
+        if ((uint32_t)(c - k * kWinCols) < (uint32_t)kWinCols) continue;
+        const float v = vals_s[j];
+        const f4 x = reinterpret_cast<const f4*>(X + (int64_t)c * ldx)[c4];
+        sum.x = __builtin_fmaf(v, x.x, sum.x);
+        sum.y = __builtin_fmaf(v, x.y, sum.y);
+        sum.z = __builtin_fmaf(v, x.z, sum.z);
+        sum.w = __builtin_fmaf(v, x.w, sum.w);
+      }
+    }
+  }
+  f4* yr = reinterpret_cast<f4*>(Y + (int64_t)perm[hub_first_row + h] * ldy);
+  __builtin_nontemporal_store(act_v(sum, act), yr + c4);
+}
+
 // Small plans (no hub rows, every degree <= min(Z, kSmallMaxDeg), few rows):
 // the whole launch is a chain of dependent memory round trips on a mostly idle
 // GPU, so this path drops the two that k_spmm adds before its gathers (the
@@ -786,7 +979,62 @@ int run_aggregation(const SpmmArgs& a, Marks& mk) {
 }
 
 
+// The hub-window execute: the aggregation over every entry but the hub
+// chunks (first in the launch order), then k_hub_win and k_hub_win_reduce.
+int run_windows(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
+  const agcn_plan* p = a.p;
+  const int32_t n_chunks = p->n_entries - p->hub_first_entry;
+  hipError_t e;
+  if (n_chunks < p->n_entries) {
+    const int rc = run_phase<4>(a, false, mk, default_slice_cols<4>(),
+                                EntryRange{n_chunks, p->n_entries, p->deg_bound}, true);
+    if (rc) return rc;
+  } else {  // hub rows only: the marks frame an empty aggregation
+    for (hipEvent_t ev : {mk.start, mk.stop})
+      if (ev && (e = hipEventRecord(ev, a.st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  const WinShape w = win_shape(p, a.F);
+  k_hub_win<<<dim3((unsigned)w.n_b, (unsigned)w.n_grp, (unsigned)w.n_slices), 1024, 0, a.st>>>(
+      p->win_tab, p->n_hub_rows, p->n_win, w.G, w.n_grp, p->colidx_s, p->vals_s, a.X, a.ldx,
+      p->n_cols, a.ws, a.F);
+  if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_hub_win launch");
+  const int64_t threads = (int64_t)p->n_hub_rows * (a.F / 4);
+  k_hub_win_reduce<<<(unsigned)ceil_div64(threads, 256), 256, 0, a.st>>>(
+      a.ws, p->n_hub_rows, p->n_win, w.G, w.n_grp, a.F, p->win_tab, p->colidx_s, p->vals_s, a.X,
+      a.ldx, p->perm, p->hub_first_row, a.Y, a.ldy, a.act);
+  if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_hub_win_reduce launch");
+  if (ev_end && (e = hipEventRecord(ev_end, a.st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  return AGCN_OK;
+}
+
 }  // namespace
+
+WinShape win_shape(const agcn_plan* p, int32_t F) {
+  WinShape w{};
+  w.n_slices = (int32_t)ceil_div64(F, kWinSliceCols);
+  w.n_b = (int32_t)ceil_div64(p->n_hub_rows, kWinRows);
+  const int64_t per_group = std::max<int64_t>(1, (int64_t)w.n_slices * w.n_b);
+  const int64_t want = std::max<int64_t>(1, ceil_div64(kWinTargetGroups, per_group));
+  w.G = (int32_t)std::max<int64_t>(1, ceil_div64(p->n_win, want));
+  w.n_grp = (int32_t)ceil_div64(p->n_win, w.G);
+  return w;
+}
+
+size_t win_workspace_bytes(const agcn_plan* p, int32_t F) {
+  if (p->n_win <= 0 || p->n_hub_rows <= 0 || F < kWinMinF || ceil_div64(F, kWinSliceCols) > 65535)
+    return 0;
+  const WinShape w = win_shape(p, F);
+  // partial rows, then one stray flag per (hub row, window group)
+  return (size_t)p->n_hub_rows * (size_t)w.n_grp * ((size_t)F * sizeof(float) + sizeof(int32_t));
+}
+
+size_t chunk_workspace_bytes(const agcn_plan* p, int32_t F) {
+  const int64_t chunks =
+      p->flags & AGCN_PLAN_WARP_LEVEL
+          ? 2 * warp_level_blocks(p)
+          : (p->n_hub_rows > 0 ? (int64_t)p->n_entries - p->hub_first_entry : 0);
+  return (size_t)chunks * (size_t)F * sizeof(float);
+}
 
 size_t spmm_lds_bytes_max(int32_t W, int32_t max_entry_nnz) {
   // Worst case over slice widths: 64 lanes of float4 per vwarp.
@@ -921,7 +1169,7 @@ int noalloc_scratch(int device, float** out) {
 }
 
 int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* Y, int64_t ldy,
-             float* ws, hipStream_t st, hipEvent_t ev_begin, hipEvent_t ev_mid,
+             float* ws, size_t ws_bytes, hipStream_t st, hipEvent_t ev_begin, hipEvent_t ev_mid,
              hipEvent_t ev_end, int32_t act) {
   const bool vec = (F % 4 == 0) && (ldx % 4 == 0) && (ldy % 4 == 0) && aligned16(X) &&
                    aligned16(Y) && (ws == nullptr || aligned16(ws));
@@ -942,6 +1190,8 @@ int run_spmm(const agcn_plan* p, int32_t F, const float* X, int64_t ldx, float* 
     if (ev_end && (e = hipEventRecord(ev_end, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     return AGCN_OK;
   }
+  const size_t win_ws = vec ? win_workspace_bytes(p, F) : 0;
+  if (win_ws > 0 && ws_bytes >= win_ws) return run_windows(a, mk, ev_end);
   int rc = vec ? run_aggregation<4>(a, mk) : run_aggregation<1>(a, mk);
   if (rc) return rc;
   Marks none{};

@@ -113,8 +113,9 @@ def test_null_plan_calls(lib):
 
 
 def test_stats_struct_layout_matches_header():
-    # int32 x2, int64 x4, int32 x8, size_t
-    assert ctypes.sizeof(agcn.PlanStats) == 8 + 32 + 32 + 8
+    # int32 x2, int64 x4, int32 x8, size_t, int32 (+4 bytes of tail padding)
+    assert ctypes.sizeof(agcn.PlanStats) == 8 + 32 + 32 + 8 + 8
+    assert agcn.PlanStats.hub_windows.offset == 80
     assert ctypes.sizeof(agcn.PlanParams) == 16
 
 
