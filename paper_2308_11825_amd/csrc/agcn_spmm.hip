@@ -452,51 +452,73 @@ __global__ __launch_bounds__(1024) void k_hub_win(
 }
 
 // Y row of hub row h = the sum of its n_grp window-group partials, in window
-// order (four interleaved chains, kg mod 4, added pairwise), plus, for the
-// window groups flagged by k_hub_win, the pairs that lay outside their
-// window, gathered from X in position order.
-__global__ __launch_bounds__(256) void k_hub_win_reduce(
+// order, plus the pairs k_hub_win flagged as lying outside their window,
+// gathered from X in position order. One workgroup per (hub row, 64
+// columns): kWinReduceParts parts of 16 lanes (one float4 column each) take
+// contiguous runs of the window groups -- each summing its run in four
+// interleaved chains (kg mod 4, added pairwise), then its stray pairs -- and
+// the part sums are added in part order. With a thread per column walking
+// all the partials, the loads of a row were one dependent chain and the launch
+// had a workgroup per 16 rows (153 us on 1000 rows x 489 groups at F = 64).
+constexpr int kWinReduceParts = 8;
+
+__global__ __launch_bounds__(kWinReduceParts * 16) void k_hub_win_reduce(
     const float* __restrict__ ws, int32_t n_hub, int32_t n_win, int32_t G, int32_t n_grp,
     int32_t F, const int32_t* __restrict__ win_tab, const int32_t* __restrict__ colidx_s,
     const float* __restrict__ vals_s, const float* __restrict__ X, int64_t ldx,
     const int32_t* __restrict__ perm, int32_t hub_first_row, float* __restrict__ Y, int64_t ldy,
     int32_t act) {
+  __shared__ f4 s_part[kWinReduceParts][16];
   const int32_t q = F / 4;
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)n_hub * q) return;
-  const int32_t h = (int32_t)(t / q), c4 = (int32_t)(t - (int64_t)h * q);
-  const f4* src = reinterpret_cast<const f4*>(ws + (int64_t)h * n_grp * F) + c4;
-  f4 s0 = f4(0.0f), s1 = f4(0.0f), s2 = f4(0.0f), s3 = f4(0.0f);
-  int32_t kg = 0;
-  for (; kg + 4 <= n_grp; kg += 4) {
-    s0 += src[(int64_t)kg * q];
-    s1 += src[(int64_t)(kg + 1) * q];
-    s2 += src[(int64_t)(kg + 2) * q];
-    s3 += src[(int64_t)(kg + 3) * q];
-  }
-  for (; kg < n_grp; ++kg) s0 += src[(int64_t)kg * q];
-  f4 sum = (s0 + s1) + (s2 + s3);
-  const int32_t* flags = reinterpret_cast<const int32_t*>(ws + (int64_t)n_hub * n_grp * F) +
-                         (int64_t)h * n_grp;
-  for (kg = 0; kg < n_grp; ++kg) {
-    if (flags[kg] == 0) continue;
-    const int32_t k1 = min(n_win, (kg + 1) * G);
-    for (int32_t k = kg * G; k < k1; ++k) {
-      const int32_t lo = win_tab[(int64_t)k * n_hub + h], hi = win_tab[(int64_t)(k + 1) * n_hub + h];
-      for (int32_t j = lo; j < hi; ++j) {
-        const int32_t c = colidx_s[j];
-        if ((uint32_t)(c - k * kWinCols) < (uint32_t)kWinCols) continue;
-        const float v = vals_s[j];
-        const f4 x = reinterpret_cast<const f4*>(X + (int64_t)c * ldx)[c4];
-        sum.x = __builtin_fmaf(v, x.x, sum.x);
-        sum.y = __builtin_fmaf(v, x.y, sum.y);
-        sum.z = __builtin_fmaf(v, x.z, sum.z);
-        sum.w = __builtin_fmaf(v, x.w, sum.w);
+  const int32_t chunks = (q + 15) / 16;
+  const int32_t h = (int32_t)(blockIdx.x / chunks);
+  const int32_t c4 = (int32_t)(blockIdx.x - (int64_t)h * chunks) * 16 + (threadIdx.x & 15);
+  const int part = threadIdx.x >> 4;
+  const bool col_ok = c4 < q;
+  const int32_t per = (n_grp + kWinReduceParts - 1) / kWinReduceParts;
+  const int32_t g0 = min(n_grp, part * per), g1 = min(n_grp, g0 + per);
+  f4 sum = f4(0.0f);
+  if (col_ok) {
+    const f4* src = reinterpret_cast<const f4*>(ws + (int64_t)h * n_grp * F) + c4;
+    f4 s0 = f4(0.0f), s1 = f4(0.0f), s2 = f4(0.0f), s3 = f4(0.0f);
+    int32_t kg = g0;
+    for (; kg + 4 <= g1; kg += 4) {
+      s0 += src[(int64_t)kg * q];
+      s1 += src[(int64_t)(kg + 1) * q];
+      s2 += src[(int64_t)(kg + 2) * q];
+      s3 += src[(int64_t)(kg + 3) * q];
+    }
+    for (; kg < g1; ++kg) s0 += src[(int64_t)kg * q];
+    sum = (s0 + s1) + (s2 + s3);
+    const int32_t* flags = reinterpret_cast<const int32_t*>(ws + (int64_t)n_hub * n_grp * F) +
+                           (int64_t)h * n_grp;
+    for (kg = g0; kg < g1; ++kg) {
+      if (flags[kg] == 0) continue;
+      const int32_t k1 = min(n_win, (kg + 1) * G);
+      for (int32_t k = kg * G; k < k1; ++k) {
+        const int32_t lo = win_tab[(int64_t)k * n_hub + h];
+        const int32_t hi = win_tab[(int64_t)(k + 1) * n_hub + h];
+        for (int32_t j = lo; j < hi; ++j) {
+          const int32_t c = colidx_s[j];
+          if ((uint32_t)(c - k * kWinCols) < (uint32_t)kWinCols) continue;
+          const float v = vals_s[j];
+          const f4 x = reinterpret_cast<const f4*>(X + (int64_t)c * ldx)[c4];
+          sum.x = __builtin_fmaf(v, x.x, sum.x);
+          sum.y = __builtin_fmaf(v, x.y, sum.y);
+          sum.z = __builtin_fmaf(v, x.z, sum.z);
+          sum.w = __builtin_fmaf(v, x.w, sum.w);
+        }
       }
     }
   }
+  s_part[part][threadIdx.x & 15] = sum;
+  __syncthreads();
+  if (part != 0 || !col_ok) return;
+  f4 total = s_part[0][threadIdx.x];
+#pragma unroll
+  for (int p = 1; p < kWinReduceParts; ++p) total += s_part[p][threadIdx.x];
   f4* yr = reinterpret_cast<f4*>(Y + (int64_t)perm[hub_first_row + h] * ldy);
-  __builtin_nontemporal_store(act_v(sum, act), yr + c4);
+  __builtin_nontemporal_store(act_v(total, act), yr + c4);
 }
 
 // Small plans (no hub rows, every degree <= min(Z, kSmallMaxDeg), few rows):
@@ -998,8 +1020,8 @@ int run_windows(const SpmmArgs& a, Marks& mk, hipEvent_t ev_end) {
       p->win_tab, p->n_hub_rows, p->n_win, w.G, w.n_grp, p->colidx_s, p->vals_s, a.X, a.ldx,
       p->n_cols, a.ws, a.F);
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_hub_win launch");
-  const int64_t threads = (int64_t)p->n_hub_rows * (a.F / 4);
-  k_hub_win_reduce<<<(unsigned)ceil_div64(threads, 256), 256, 0, a.st>>>(
+  const int64_t blocks = (int64_t)p->n_hub_rows * ceil_div64(a.F / 4, 16);
+  k_hub_win_reduce<<<(unsigned)blocks, kWinReduceParts * 16, 0, a.st>>>(
       a.ws, p->n_hub_rows, p->n_win, w.G, w.n_grp, a.F, p->win_tab, p->colidx_s, p->vals_s, a.X,
       a.ldx, p->perm, p->hub_first_row, a.Y, a.ldy, a.act);
   if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "k_hub_win_reduce launch");
@@ -1021,7 +1043,9 @@ WinShape win_shape(const agcn_plan* p, int32_t F) {
 }
 
 size_t win_workspace_bytes(const agcn_plan* p, int32_t F) {
-  if (p->n_win <= 0 || p->n_hub_rows <= 0 || F < kWinMinF || ceil_div64(F, kWinSliceCols) > 65535)
+  // (grid limits: slices in grid z, the reduction's (hub row, 64 columns) in grid x)
+  if (p->n_win <= 0 || p->n_hub_rows <= 0 || F < kWinMinF || ceil_div64(F, kWinSliceCols) > 65535 ||
+      (int64_t)p->n_hub_rows * ceil_div64(F, kWinSliceCols) > INT32_MAX)
     return 0;
   const WinShape w = win_shape(p, F);
   // partial rows, then one stray flag per (hub row, window group)
