@@ -53,6 +53,22 @@ def _hub_graph(seed, n, n_cols, n_hub, lo, hi, sort_cols=True):
     return graphgen.random_csr(n, n_cols, deg, seed=seed + 1, sort_cols=sort_cols)
 
 
+def _stray_flags(plan, F):
+    """The stray flags k_hub_win leaves after the window partials in the
+    workspace of the last execute at F: one int32 per (hub row, window group),
+    n_grp = ceil(n_win / G) with G chosen for about 512 workgroups over
+    ceil(F / 64) slices and ceil(n_hub / 1024) row batches."""
+    st = plan.stats
+    n_hub, n_win = st.n_hub_rows, st.hub_windows
+    per = max(1, -(-F // 64) * -(-n_hub // 1024))
+    G = max(1, -(-n_win // max(1, -(-512 // per))))
+    n_grp = -(-n_win // G)
+    ws = plan.workspace(F)
+    assert ws.numel() * 4 >= n_hub * n_grp * (4 * F + 4)
+    off = n_hub * n_grp * F
+    return ws[off:off + n_hub * n_grp].view(torch.int32).cpu().numpy()
+
+
 def _X(g, F, seed):
     return np.random.default_rng(seed).standard_normal((g.n_cols, F)).astype(np.float32)
 
@@ -83,6 +99,10 @@ def test_windows_match_the_oracle(hub_case, F):
     Y = p.spmm(Xd).cpu().numpy()
     assert_all_rows_close(g, X, Y, f"windows F={F}")
     assert np.array_equal(Y.view(np.uint32), p.spmm(Xd).cpu().numpy().view(np.uint32))
+    # sorted rows: every pair lies in the window the table gives it (a table
+    # off by one anywhere would flag a stray; Y would still be right)
+    flags = _stray_flags(p, F)
+    assert flags.size > 0 and np.all(flags == 0), int(np.count_nonzero(flags))
     Yc = pc.spmm(Xd).cpu().numpy()
     _, S = oracle.spmm(g.rowptr, g.colidx, g.vals, X, n_cols=g.n_cols, want_scale=True)
     assert_close(Y, Yc, 2 * S, f"windows against hub chunks F={F}")
@@ -122,6 +142,8 @@ def test_windows_with_columns_out_of_order():
     for F in (64, 128):
         X = _X(g, F, 20 + F)
         assert_all_rows_close(g, X, p.spmm(_dev(X)).cpu().numpy(), f"unsorted F={F}")
+        flags = _stray_flags(p, F)
+        assert np.all((flags == 0) | (flags == 1)) and np.count_nonzero(flags) > 0
     p.destroy()
 
 
