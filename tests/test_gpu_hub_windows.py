@@ -226,3 +226,59 @@ def test_window_plan_destroyed_while_its_execute_runs_on_another_stream():
     p.destroy()                       # the table is freed after the side stream's execute
     torch.cuda.synchronize()
     assert_all_rows_close(g, X, Y.cpu().numpy(), "execute on another stream")
+
+
+def test_windows_with_empty_ranges():
+    # Half the hub rows keep their columns in the first 8 windows, so most of
+    # their (row, window) ranges are empty: a group's preloaded batch is then
+    # empty and it moves on to its next row's.
+    rng = np.random.default_rng(1700)
+    n, n_cols = 12000, 40000
+    deg = rng.integers(1, 9, size=n)
+    hubs = rng.choice(n, size=200, replace=False)
+    deg[hubs] = rng.integers(2500, 3500, size=200)
+    g = graphgen.random_csr(n, n_cols, deg, seed=1701)
+    ci = g.colidx.copy()
+    for r in hubs[:100]:
+        s, e = g.rowptr[r], g.rowptr[r + 1]
+        ci[s:e] = np.sort(rng.choice(8 * WIN, size=e - s, replace=False))
+    g = graphgen.Graph("clustered", g.n_rows, g.n_cols, g.rowptr, ci, g.vals)
+    p = _windowed(g)
+    for F in (64, 128):
+        X = _X(g, F, 70 + F)
+        assert_all_rows_close(g, X, p.spmm(_dev(X)).cpu().numpy(), f"empty ranges F={F}")
+        assert np.all(_stray_flags(p, F) == 0)
+    p.destroy()
+
+
+@pytest.mark.parametrize("cap,early,tiny", [(None, None, None), ("-1", None, "0"), (None, "0", "0")])
+def test_windows_after_every_degree_sort(cap, early, tiny):
+    # The table lies over the plan's working buffers whichever sort built the
+    # plan: the single-workgroup plan of a small graph, the short sort with
+    # the column check early or in the relayout, the multi-pass sort.
+    rng = np.random.default_rng(1800)
+    n, n_cols = 2000, 4096
+    deg = rng.integers(1, 9, size=n)
+    hubs = rng.choice(n, size=64, replace=False)
+    deg[hubs] = rng.integers(1200, 1700, size=64)
+    g = graphgen.random_csr(n, n_cols, deg, seed=1801)
+    assert g.nnz <= 1 << 17            # small enough for the single-workgroup plan
+    old = {k: os.environ.get(k) for k in ("AGCN_TEST_TAIL_CAP", "AGCN_TEST_EARLY_CHECK_NNZ",
+                                           "AGCN_TEST_TINY")}
+    try:
+        for k, v in zip(old, (cap, early, tiny)):
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+        p = _windowed(g)
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    X = _X(g, 64, 81)
+    assert_all_rows_close(g, X, p.spmm(_dev(X)).cpu().numpy(), f"windows cap={cap} early={early}")
+    assert np.all(_stray_flags(p, 64) == 0)
+    p.destroy()
