@@ -158,13 +158,27 @@ void agcn_default_params(agcn_plan_params* p);
  * that relayout runs (larger graphs: checked by the relayout, and the call
  * returns after it; the plan is the same either way); AGCN_TEST_TINY=0 keeps
  * graphs of at most 16384 rows and 2^17 nonzeros off the single-workgroup
- * plan (the same plan again). */
+ * plan (the same plan again).
+ *
+ * Hub-row windows: when the rows of degree > deg_bound average at least 16
+ * nonzeros per window of 512 columns, over at least 64 such rows, the plan
+ * also keeps, for each of those rows and each window, the position of the
+ * row's first nonzero in the window (built by the call's last kernel, in the
+ * plan's own memory; agcn_plan_stats.hub_windows = the number of windows).
+ * agcn_spmm at F >= 64 on the 128-bit path then aggregates those rows window
+ * by window from X staged in LDS. The columns of a row may come in any order;
+ * ascending is fastest. AGCN_HUB_WINDOWS=0 (read on every call) builds no
+ * table, so the hub chunks serve every F. */
 int agcn_plan_create(agcn_plan_t* out, int32_t n_rows, int32_t n_cols, int64_t nnz,
                      const int32_t* d_rowptr, const int32_t* d_colidx, const float* d_vals,
                      const agcn_plan_params* params, void* stream);
 
 /* Device workspace agcn_spmm needs for feature width F: n_hub_chunks * F * 4
- * bytes (partial rows of the hub chunks; 0 when the plan has no hub rows).
+ * bytes (partial rows of the hub chunks; 0 when the plan has no hub rows),
+ * or, for a plan with hub-row windows at F >= 64 when that is larger,
+ * n_hub_rows * n_groups * (F + 1) * 4 bytes (one partial row and one flag
+ * per hub row and group of windows, n_groups about 512 / (ceil(F / 64) *
+ * ceil(n_hub_rows / 1024)); 127 MB for 1000 hub rows at F = 64).
  * For AGCN_PLAN_WARP_LEVEL plans: 2 * workgroups * F * 4 bytes (partial rows
  * of the rows cut by workgroup boundaries). */
 int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes);
@@ -178,7 +192,10 @@ int agcn_spmm_workspace_size(agcn_plan_t plan, int32_t F, size_t* bytes);
  * The 128-bit path runs when F, ldx and ldy are multiples of 4 and X, Y, ws
  * are 16-byte aligned; otherwise a 32-bit path runs (same results up to
  * float rounding order, both deterministic).
- * Result: bitwise reproducible run to run; no atomics.
+ * Result: bitwise reproducible run to run; no atomics. The hub rows of a plan
+ * with hub-row windows are summed window by window at F >= 64 on the
+ * 128-bit path and by hub chunks otherwise (same sums, another rounding
+ * order).
  * The plan is read-only here: concurrent calls on different streams are
  * safe when each has its own Y and ws. Must run on the plan's device.
  * The call launches kernels only (no allocation, no memset, no host wait), so
@@ -194,7 +211,8 @@ int agcn_spmm(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float*
 /* agcn_spmm plus timing marks on the caller's hipEvent_t handles (each may be
  * NULL): ev_begin is recorded when the aggregation kernel starts and ev_mid
  * when it ends (attached to the kernel's own launch, so no marker packet sits
- * between kernels), ev_end after the hub-row reduction. Same kernels, same
+ * between kernels), ev_end after the hub-row reduction (or the hub-row
+ * windows and their reduction). Same kernels, same
  * launch shapes; used to time the aggregation kernel by itself. */
 int agcn_spmm_timed(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
                     int64_t ldy, void* d_ws, void* stream, void* ev_begin, void* ev_mid,
@@ -216,7 +234,9 @@ int agcn_spmm_ex(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
 /* agcn_spmm_ex for callers that cannot allocate memory: code being captured
  * into a HIP graph, tight serving loops, harnesses that forbid hipMalloc.
  * Same arguments, kernels and results (bit for bit) as agcn_spmm_ex, without
- * d_ws: the hub-row partial sums go to a fixed workspace the library keeps in
+ * d_ws, except that a plan whose hub-row window partials at this F exceed the
+ * fixed workspace takes the hub chunks (same sums, another rounding order):
+ * the hub-row partial sums go to a fixed workspace the library keeps in
  * device memory, AGCN_NOALLOC_MAX_WORKSPACE bytes on every GPU it runs on,
  * held until the process ends. The call allocates nothing (no device or host
  * memory, no HIP event): on a stream other than the plan's own on which the
@@ -226,8 +246,9 @@ int agcn_spmm_ex(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, flo
  * every part of it that it reads, so nothing needs clearing between calls;
  * calls that may overlap in time on one GPU (different streams, or graph
  * replays running concurrently) race on it and must be ordered by the caller.
- * Errors: those of agcn_spmm_ex, plus UNSUPPORTED when
- * agcn_spmm_workspace_size(plan, F) exceeds AGCN_NOALLOC_MAX_WORKSPACE. */
+ * Errors: those of agcn_spmm_ex, plus UNSUPPORTED when the hub chunks'
+ * workspace at F (agcn_spmm_workspace_size for a plan without hub-row
+ * windows) exceeds AGCN_NOALLOC_MAX_WORKSPACE. */
 #define AGCN_NOALLOC_MAX_WORKSPACE ((size_t)64 << 20)
 int agcn_spmm_noalloc(agcn_plan_t plan, int32_t F, const float* d_X, int64_t ldx, float* d_Y,
                       int64_t ldy, void* stream, int32_t epilogue);

@@ -36,6 +36,12 @@
 // and share them in L2; then the other entries heaviest first (the metadata
 // is in ascending degree order).
 //
+// Plans with hub-row windows (dense hub rows; the plan's window table), at
+// F >= 64 on the float4 path with room for the window partials: k_spmm runs
+// over the entries after the hub chunks only, and k_hub_win +
+// k_hub_win_reduce aggregate the hub rows window by window (described at the
+// kernels below).
+//
 // Every kernel that writes Y takes `act` and applies the layer's activation
 // there (ReLU, Sec. II-A), after a split row's final sum.
 //
