@@ -427,7 +427,9 @@ __global__ __launch_bounds__(1024) void k_hub_win(
           const bool inside = (uint32_t)(c_c - cbase) < (uint32_t)kWinCols;
           stray_rows |= (uint32_t)(in_c && !inside) << r;
           const bool use = in_c && inside;
-          WinSteps<16>::run(use ? (c_c - cbase) * 256 : 0, use ? v_c : 0, sxb, l16, acc[r], a1);
+          // (unsigned arithmetic: a masked lane's column may lie far outside)
+          const int32_t off = (int32_t)((uint32_t)(c_c - cbase) << 8);
+          WinSteps<16>::run(use ? off : 0, use ? v_c : 0, sxb, l16, acc[r], a1);
         }
         acc[r] += a1;
         if (s == e) load_pair(s_nx, e_nx, c_n, v_n, in_n);  // its preloaded batch was empty
