@@ -91,7 +91,7 @@ def hub_case():
     pc.destroy()
 
 
-@pytest.mark.parametrize("F", [64, 96, 128, 256])
+@pytest.mark.parametrize("F", [64, 96, 128, 256, 512])
 def test_windows_match_the_oracle(hub_case, F):
     g, p, pc = hub_case
     X = _X(g, F, F)
@@ -282,3 +282,36 @@ def test_windows_after_every_degree_sort(cap, early, tiny):
     assert_all_rows_close(g, X, p.spmm(_dev(X)).cpu().numpy(), f"windows cap={cap} early={early}")
     assert np.all(_stray_flags(p, 64) == 0)
     p.destroy()
+
+
+def test_windows_captured_in_a_hip_graph_replay_like_eager(hub_case):
+    """The window execute (k_spmm over the other rows, k_hub_win,
+    k_hub_win_reduce) launches kernels only: captured into a HIP graph, every
+    replay with new X (copied in eagerly, the device synchronised between
+    replays) equals the eager call bit for bit."""
+    g, p, _ = hub_case
+    F = 64
+    X = torch.zeros((g.n_cols, F), device=DEV)
+    Y = torch.empty((g.n_rows, F), device=DEV)
+    ws = torch.empty(p.workspace_bytes(F) // 4 + 1, device=DEV)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(graph, stream=s):
+            p.spmm(X, out=Y, ws=ws, stream=s)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(93)
+    for r in range(3):
+        Xr = rng.standard_normal((g.n_cols, F)).astype(np.float32)
+        X.copy_(_dev(Xr))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        Ye = p.spmm(_dev(Xr))
+        torch.cuda.synchronize()
+        assert torch.equal(Y, Ye), f"replay {r}"
+        if r == 0:
+            assert_all_rows_close(g, Xr, Y.cpu().numpy(), "graph replay")
+    del graph
