@@ -328,12 +328,12 @@ __global__ __launch_bounds__(kFlatThreads) void k_hub_reduce_flat(
 // one partial row per (hub row, window group) goes to ws; k_hub_win_reduce
 // adds them in window order. Against the hub chunks, which gather every X row
 // of a hub row through L2 (about 27 GB of 128-byte requests for 1.1e8 hub
-// nonzeros at F = 64), X is read once per window group from HBM and the
-// gathers become LDS reads.
+// nonzeros at F = 64), X crosses L2 once per row batch and the gathers become
+// LDS reads (measured on that graph: 1339 -> 582 us, the VALU then 84% busy).
 // A row whose columns do not ascend still has its nonzeros split over the
-// windows (the table's positions do not decrease); a batch holding a column
-// outside the current window takes a path that reads those X rows from
-// global memory.
+// windows (the table's positions do not decrease); a pair whose column lies
+// outside the current window counts zero here and flags its (row, window
+// group), and k_hub_win_reduce adds those pairs from X.
 template <int U>
 __device__ inline int32_t row_bcast(int32_t v) {
   return __builtin_amdgcn_mov_dpp(v, 0x150 + U, 0xF, 0xF, true);  // row_newbcast:U
