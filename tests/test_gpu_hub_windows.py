@@ -315,3 +315,16 @@ def test_windows_captured_in_a_hip_graph_replay_like_eager(hub_case):
         if r == 0:
             assert_all_rows_close(g, Xr, Y.cpu().numpy(), "graph replay")
     del graph
+
+
+def test_gcn_layer_over_the_windows(hub_case):
+    # agcn_gcn_layer passes its SpMM the layer workspace, sized with the
+    # window partials: fout = 64 takes the windows.
+    from test_gpu_layer import _check_layer
+    g, p, _ = hub_case
+    X = np.random.default_rng(95).standard_normal((g.n_cols, 32)).astype(np.float32)
+    W = graphgen.weights(32, 64, seed=96)
+    _check_layer(p, g, X, W, "relu")
+    H = agcn.linear(_dev(X), _dev(W))
+    Y = p.spmm(H, act="relu")
+    assert torch.equal(Y, p.gcn_layer(_dev(X), _dev(W), act="relu"))
