@@ -666,8 +666,8 @@ def main():
                     "kernel": "k_hub_win", "launches_per_step": len(win_F), "F": win_F,
                     "alg_bytes_per_launch": int(lds_b), "avg_launch_ms": round(hub_ms, 5),
                     "timed": "k_hub_win + k_hub_win_reduce",
-                    "hbm_bytes_per_launch": int(hbm_b),
-                    "hbm_GBps": round(hbm_b / (hub_ms * 1e-3) / 1e9, 1)}
+                    "alg_hbm_bytes_per_launch": int(hbm_b),
+                    "alg_hbm_GBps": round(hbm_b / (hub_ms * 1e-3) / 1e9, 1)}
     if traffic is not None and not win_roof:
         # counter-measured bytes past L2 (Infinity Cache hits included) over the same time
         tg = traffic / (mean_ms * 1e-3) / 1e9
