@@ -70,3 +70,32 @@ def test_gather_requests_model():
     assert bench.gather_requests(St, 16) == 1000
     assert bench.gather_requests(St, 32) == 1000
     assert bench.gather_requests(St, 256) == 8000
+
+
+class _WinStats:
+    n_rows, nnz, n_hub_rows, hub_first_entry, deg_bound = 1_000_000, 111_640_508, 1000, 270_000, 512
+    hub_windows = 1954
+
+
+def test_window_shape_and_bytes_model():
+    # skewed_hubs' shape: 1000 hub rows, 1954 windows of 512 columns; one row
+    # batch; F = 64 is one slice, so about 512 workgroups means G = 4 windows
+    # per group (489 groups); F = 256 has four slices, so G = 16 (123 groups).
+    st = _WinStats()
+    assert bench.win_shape(st, 64) == (1, 1, 4, 489)
+    assert bench.win_shape(st, 256) == (4, 1, 16, 123)
+    assert bench.win_shape(st, 96) == (2, 1, 8, 245)
+    hub = {"hub_nnz": 107_144_212, "n_cols": 1_000_000, "low_nnz": 4_496_296,
+           "low_entries": 270_000, "low_ref": 990_000}
+    b_low, b_hub = bench.window_bytes(st, 64, hub)
+    assert b_hub == (8 * hub["hub_nnz"] + 4 * 64 * hub["n_cols"] + 8 * 1000 * 1954
+                     + 2 * (4 * 64 + 4) * 1000 * 489 + (4 * 64 + 4) * 1000)
+    nonhub = st.n_rows - st.n_hub_rows
+    assert b_low == (8 * hub["low_nnz"] + 16 * hub["low_entries"] + 4 * nonhub
+                     + 4 * 64 * hub["low_ref"] + 4 * 64 * nonhub)
+    # the windows serve F >= 64 on the float4 path of the block-level plan only
+    assert bench.windows_used(st, 64) and bench.windows_used(st, 512)
+    assert not bench.windows_used(st, 32) and not bench.windows_used(st, 66)
+    assert not bench.windows_used(st, 64, "warp_level")
+    st.hub_windows = 0
+    assert not bench.windows_used(st, 64)
