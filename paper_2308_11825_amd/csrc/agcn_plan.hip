@@ -1021,6 +1021,145 @@ __device__ inline void relayout_tile(int64_t tile, bool active, int tid, int32_t
   if (bad) atomicOr(err, bad);
 }
 
+// A run of the relayout: sorted positions [p0, p1) filled by one workgroup,
+// in steps of kRelayTile positions. The rows of one step (its window, at most
+// kRelayTile rows, all non-empty) are consecutive: the row of the step's
+// first position, found once per run by a wave search and then carried from
+// step to step, and the rows after it that start before the step's end. A
+// step loads the window's row starts and permutation entries in rounds of
+// kThreads rows until a start at or past the step's end shows up (one round
+// unless the rows are short), then each window row's first nonzero in the
+// input CSR, then copies its positions, each finding its row by binary
+// lifting over the window's starts: three dependent global loads per step
+// where relayout_tile takes six. n bounds the rows searched (rowptr_s[n] >= p1
+// is final). Column indices are checked against check_cols (INT32_MAX when
+// they were checked before). Called by whole workgroups of kThreads.
+constexpr int kRelaySpanLds = 2 * (kRelayTile + 1) + kThreads / 64;
+
+__device__ __forceinline__ void relay_span(int64_t p0, int64_t p1, int32_t n, int32_t check_cols,
+                                           const int32_t* __restrict__ rowptr,
+                                           const int32_t* __restrict__ colidx,
+                                           const float* __restrict__ vals,
+                                           const int32_t* __restrict__ perm,
+                                           const int32_t* __restrict__ rowptr_s,
+                                           int32_t* __restrict__ colidx_s,
+                                           float* __restrict__ vals_s, uint32_t* err,
+                                           int32_t* lds) {
+  constexpr int G = kThreads, T = kRelayTile;
+  int32_t* s_ptr = lds;            // window row starts, [0, T]
+  int32_t* s_src = s_ptr + T + 1;  // window rows' permutation entries, then input starts
+  int32_t* s_cnt = s_src + T + 1;  // per wave: rows of a round starting before the end
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (p0 >= p1) return;  // uniform over the workgroup
+  if (tid < 64) {
+    const int32_t r = wave_row_of(rowptr_s, n, p0, tid);
+    if (tid == 0) s_cnt[0] = r;
+  }
+  __syncthreads();
+  int32_t lo = s_cnt[0];
+  uint32_t bad = 0;
+  for (int64_t e0 = p0; e0 < p1; e0 += T) {
+    // Positions as unsigned 32-bit values (nnz < 2^31; those past the step's
+    // end, whose searches go unused, stay below 2^32).
+    const uint32_t u0 = (uint32_t)e0, u1 = (uint32_t)(e0 + T < p1 ? e0 + T : p1);
+    __syncthreads();  // the previous step's readers of the LDS are done
+    // Window rows lo + k for k < K: those starting before the step's end u1.
+    // The starts ascend, so the rows below u1 are a prefix; a round that is
+    // not all below u1 holds the first start at or past it (s_ptr[K],
+    // rowptr_s[n] at the latest). Rows past k = T or past n are never
+    // counted, so the loop ends by round kRelayItems.
+    int32_t K = 0;
+    for (int c = 0;; ++c) {
+      const int32_t k = c * G + tid;
+      bool below = false;
+      if (k <= T && (int64_t)lo + k <= n) {
+        const int32_t v = rowptr_s[lo + k];
+        const bool row = (int64_t)lo + k < n;  // else the end of the rows
+        if (row) s_src[k] = perm[lo + k];
+        s_ptr[k] = v;
+        below = row && (uint32_t)v < u1;
+      }
+      const uint64_t m = __ballot(below);
+      if (lane == 0) s_cnt[wv] = __popcll(m);
+      __syncthreads();
+      int32_t cnt = 0;
+#pragma unroll
+      for (int w = 0; w < G / 64; ++w) cnt += s_cnt[w];
+      __syncthreads();
+      K += cnt;
+      if (cnt < G) break;
+    }
+    if (K < 1 || K > T) {  // cannot happen for a sorted row order (uniform)
+      if (tid == 0) atomicOr(err, kErrRelayout);
+      return;
+    }
+    // Each thread converts the permutation entries it loaded itself, all
+    // loads issued before the first store.
+    int32_t first[kRelayItems];
+#pragma unroll
+    for (int c = 0; c < kRelayItems; ++c)
+      if (c * G + tid < K) first[c] = rowptr[s_src[c * G + tid]];
+#pragma unroll
+    for (int c = 0; c < kRelayItems; ++c)
+      if (c * G + tid < K) s_src[c * G + tid] = first[c];
+    __syncthreads();
+    // Each position's row: the last window row starting at or before it; a
+    // lifting step past the window probes its last row, which is then the
+    // answer or stays unchosen. K is uniform, so every lane takes the same
+    // steps, and the kRelayItems searches advance side by side.
+    int32_t w[kRelayItems];
+#pragma unroll
+    for (int i = 0; i < kRelayItems; ++i) w[i] = 0;
+    for (int32_t step = K > 1 ? 1 << (31 - __builtin_clz((uint32_t)(K - 1))) : 0; step > 0;
+         step >>= 1) {
+      int32_t v[kRelayItems], m[kRelayItems];
+#pragma unroll
+      for (int i = 0; i < kRelayItems; ++i) {
+        m[i] = min(w[i] + step, K - 1);
+        v[i] = s_ptr[m[i]];
+      }
+#pragma unroll
+      for (int i = 0; i < kRelayItems; ++i)
+        if ((uint32_t)v[i] <= u0 + i * G + tid) w[i] = m[i];
+    }
+    int32_t src[kRelayItems];  // nnz < 2^31
+#pragma unroll
+    for (int i = 0; i < kRelayItems; ++i)
+      src[i] = s_src[w[i]] + (int32_t)(u0 + i * G + tid - (uint32_t)s_ptr[w[i]]);
+    int32_t cv[kRelayItems];
+    float vv[kRelayItems];
+#pragma unroll
+    for (int i = 0; i < kRelayItems; ++i) {
+      if (u0 + i * G + tid < u1) {
+        cv[i] = colidx[src[i]];
+        vv[i] = vals[src[i]];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kRelayItems; ++i) {
+      const uint32_t e = u0 + i * G + tid;
+      if (e < u1) {
+        if ((uint32_t)cv[i] >= (uint32_t)check_cols) bad = kErrColumn;
+        colidx_s[e] = cv[i];
+        vals_s[e] = vv[i];
+      }
+    }
+    // The next step's first row: the row starting exactly at u1, if any, else
+    // the window's last row.
+    lo = (int64_t)lo + K < n && (uint32_t)s_ptr[K] == u1 ? lo + K : lo + K - 1;
+  }
+  if (bad) atomicOr(err, bad);
+}
+
+// The share [t_a, t_b) of part b out of parts of `tiles` relayout tiles
+// (kRelayTile positions each), as sorted positions [p0, p1) clipped to end.
+__device__ inline void relay_share(int64_t first_tile, int64_t tiles, int64_t b, int64_t parts,
+                                   int64_t end, int64_t* p0, int64_t* p1) {
+  const int64_t ta = first_tile + tiles * b / parts, tb = first_tile + tiles * (b + 1) / parts;
+  *p0 = ta * kRelayTile < end ? ta * kRelayTile : end;
+  *p1 = tb * kRelayTile < end ? tb * kRelayTile : end;
+}
+
 // The error word as one workgroup sees it, read once (other workgroups may
 // raise flags meanwhile, and every thread must take the same branch).
 __device__ inline bool block_failed(const uint32_t* err) {
@@ -1032,15 +1171,18 @@ __device__ inline bool block_failed(const uint32_t* err) {
   return f;
 }
 
+// The multi-pass sort's relayout: workgroup b fills share b of the sorted
+// positions (whole tiles, gridDim.x shares).
 __global__ __launch_bounds__(kThreads) void k_relayout(
     int32_t n, int64_t nnz, int32_t n_cols, const int32_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, const float* __restrict__ vals,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ rowptr_s,
     int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, uint32_t* err) {
-  __shared__ int32_t lds[kRelayLds];
+  __shared__ int32_t lds[kRelaySpanLds];
   if (block_failed(err)) return;
-  relayout_tile(blockIdx.x, true, threadIdx.x, n, nnz, n_cols, rowptr, colidx, vals, perm, rowptr_s,
-                colidx_s, vals_s, err, lds);
+  int64_t p0, p1;
+  relay_share(0, (nnz + kRelayTile - 1) / kRelayTile, blockIdx.x, gridDim.x, nnz, &p0, &p1);
+  relay_span(p0, p1, n, n_cols, rowptr, colidx, vals, perm, rowptr_s, colidx_s, vals_s, err, lds);
 }
 
 // --- partition ---------------------------------------------------------------
@@ -1170,8 +1312,8 @@ __global__ __launch_bounds__(kThreads) void k_partition_fill(
 // The last partition launch of the short-sort plan: workgroups [0, n_fill)
 // fill the partition from the tail workgroup's segment scan while the other
 // n_copy build the sorted CSR from the tile holding the tail's first nonzero
-// on (the tiles before it went with the tail), tile after tile. Returns at
-// once when the tail is over the cap (the multi-pass sort follows).
+// on (the tiles before it went with the tail), each a run of whole tiles.
+// Returns at once when the tail is over the cap (the multi-pass sort follows).
 __global__ __launch_bounds__(kThreads) void k_relayout_fill(
     int32_t n_fill, int32_t n_copy, int32_t n, int64_t nnz, const int32_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, const float* __restrict__ vals,
@@ -1182,7 +1324,7 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
     int4* __restrict__ meta, int64_t cap, int32_t hub_ub, int32_t* __restrict__ hub_chunk_off,
     int32_t* __restrict__ order, const int32_t* __restrict__ dmax, int32_t tail_cap,
     int32_t check_cols, uint32_t* err) {
-  __shared__ int32_t lds[kRelayLds];
+  __shared__ int32_t lds[kRelaySpanLds];
   const TailShape ts = tail_shape(dmax, n, tail_cap);
   if (!ts.take || block_failed(err)) return;
   if ((int32_t)blockIdx.x < n_fill) {
@@ -1191,11 +1333,12 @@ __global__ __launch_bounds__(kThreads) void k_relayout_fill(
                    hub_chunk_off, order);
     return;
   }
-  const int64_t tiles = (nnz + kRelayTile - 1) / kRelayTile;
-  for (int64_t tile = ts.nnz_low / kRelayTile + (blockIdx.x - n_fill); tile < tiles;
-       tile += n_copy)
-    relayout_tile(tile, true, threadIdx.x, n, nnz, check_cols, rowptr, colidx, vals, perm, rowptr_s, colidx_s,
-                  vals_s, err, lds);
+  const int64_t first = ts.nnz_low / kRelayTile;
+  int64_t p0, p1;
+  relay_share(first, (nnz + kRelayTile - 1) / kRelayTile - first, blockIdx.x - n_fill, n_copy, nnz,
+              &p0, &p1);
+  relay_span(p0, p1, n, check_cols, rowptr, colidx, vals, perm, rowptr_s, colidx_s, vals_s, err,
+             lds);
 }
 
 // The rest of the plan up to the partition, in one workgroup of kTailThreads
@@ -1457,7 +1600,9 @@ __device__ inline void tail_block(const TailArgs& a, const TailShape& ts, int32_
 // either role carves. Returns at once when the tail is over the cap (the
 // multi-pass sort follows); on an input error workgroup 0 publishes it.
 constexpr int kTilesPerTailGroup = kTailThreads / kThreads;
-// Relayout workgroups of k_relayout_fill per CU (its LDS allows six).
+// Relayout workgroups of kThreads per CU (k_relayout, k_relayout_fill; their
+// registers allow six). Each copies one run of tiles, so the grids stay
+// within what the CUs hold at once: a late workgroup would add its whole run.
 constexpr int kRelayGroupsPerCu = 6;
 constexpr int kXLds = kTailLds > kTilesPerTailGroup * kRelayLds ? kTailLds
                                                                  : kTilesPerTailGroup * kRelayLds;
@@ -2303,7 +2448,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     if ((rc = check_launch("k_tail_relayout"))) return rc;
     const int32_t n_fill = (int32_t)std::min<int64_t>(grid_for(ent_ub, kThreads), 64);
     const int32_t n_copy = (int32_t)std::max<int64_t>(
-        1, std::min<int64_t>(max_tiles, (int64_t)kRelayGroupsPerCu * cus));
+        1, std::min<int64_t>(max_tiles, (int64_t)kRelayGroupsPerCu * cus - n_fill));
     k_relayout_fill<<<(unsigned)(n_fill + n_copy), kThreads, 0, st>>>(
         n_fill, n_copy, (int32_t)n, nnz, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
         p->colidx_s, p->vals_s, keys, cls, seg, info, W, Z, DB, H, p->meta, ent_ub,
@@ -2350,7 +2495,7 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
     const int32_t cus = device_cus(p->device);
     const int32_t n_fill = (int32_t)std::min<int64_t>(grid_for(ent_ub, kThreads), 64);
     const int32_t n_copy = (int32_t)std::max<int64_t>(
-        1, std::min<int64_t>(ceil_div64(nnz, kRelayTile), (int64_t)kRelayGroupsPerCu * cus));
+        1, std::min<int64_t>(ceil_div64(nnz, kRelayTile), (int64_t)kRelayGroupsPerCu * cus - n_fill));
     k_relayout_fill<<<(unsigned)(n_fill + n_copy), kThreads, 0, st>>>(
         n_fill, n_copy, (int32_t)n, nnz, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
         p->colidx_s, p->vals_s, keys, cls, seg, info, W, Z, DB, H, p->meta, ent_ub,
@@ -2394,7 +2539,9 @@ int build_plan_block(agcn_plan* p, const int32_t* d_rowptr, const int32_t* d_col
                              &chain)))
       return rc;
     if (nnz > 0) {
-      k_relayout<<<grid_for(nnz, kRelayTile), kThreads, 0, st>>>(
+      const unsigned rgrid = (unsigned)std::min<int64_t>(
+          ceil_div64(nnz, kRelayTile), (int64_t)kRelayGroupsPerCu * device_cus(p->device));
+      k_relayout<<<rgrid, kThreads, 0, st>>>(
           (int32_t)n, nnz, p->n_cols, d_rowptr, d_colidx, d_vals, p->perm, p->rowptr_s,
           p->colidx_s, p->vals_s, err);
       if ((rc = check_launch("k_relayout"))) return rc;
