@@ -1122,10 +1122,12 @@ __device__ __forceinline__ void relay_span(int64_t p0, int64_t p1, int32_t n, in
       for (int i = 0; i < kRelayItems; ++i)
         if ((uint32_t)v[i] <= u0 + i * G + tid) w[i] = m[i];
     }
-    int32_t src[kRelayItems];  // nnz < 2^31
+    // Input positions (below nnz < 2^31 for the positions copied; unsigned,
+    // so the unused ones past the step's end cannot overflow).
+    uint32_t src[kRelayItems];
 #pragma unroll
     for (int i = 0; i < kRelayItems; ++i)
-      src[i] = s_src[w[i]] + (int32_t)(u0 + i * G + tid - (uint32_t)s_ptr[w[i]]);
+      src[i] = (uint32_t)s_src[w[i]] + (u0 + i * G + tid - (uint32_t)s_ptr[w[i]]);
     int32_t cv[kRelayItems];
     float vv[kRelayItems];
 #pragma unroll

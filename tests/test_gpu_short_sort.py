@@ -201,3 +201,29 @@ def test_every_row_in_the_tail_and_none():
     g = graphgen.random_csr(5000, 3000, deg, seed=53)
     for p in _both(g, max_block_waves=16, max_wave_nzs=256):
         p.destroy()
+
+
+def test_relayout_runs_over_rows_of_one_nonzero():
+    """The relayout's runs of tiles look up each tile's rows in rounds of 256
+    row starts: a tile of rows of one nonzero needs the most rounds (2,048
+    rows), every tile of such rows ends exactly where a row starts (the next
+    tile's first row is then the one after the window), and the rows of no
+    nonzero sort first. Every plan path must give the oracle's plan (the
+    multi-pass sort relays out every row this way), and Y the oracle's."""
+    rng = np.random.default_rng(5)
+    n = 120_000
+    deg = np.ones(n, np.int64)
+    u = rng.random(n)
+    deg[u < 0.05] = 0
+    deg[(u >= 0.05) & (u < 0.15)] = 2
+    deg[(u >= 0.15) & (u < 0.20)] = rng.integers(3, 40, size=int(((u >= 0.15) & (u < 0.20)).sum()))
+    hubs = rng.choice(n, size=40, replace=False)
+    deg[hubs] = rng.integers(300, 5000, size=hubs.size)
+    g = graphgen.random_csr(n, n, deg, seed=11, dupes=True)
+    p0, pm = _both(g)
+    try:
+        _spmm_check(p0, g, 16)
+        _spmm_check(pm, g, 33)
+    finally:
+        p0.destroy()
+        pm.destroy()
