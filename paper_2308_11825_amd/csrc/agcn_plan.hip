@@ -1173,18 +1173,55 @@ __device__ inline bool block_failed(const uint32_t* err) {
   return f;
 }
 
-// The multi-pass sort's relayout: workgroup b fills share b of the sorted
-// positions (whole tiles, gridDim.x shares).
+// A tile's copy costs about as much per window row as per kRelayRowCost
+// positions (a tile of short rows, 455 rows of 1-8 nonzeros, took twice as
+// long as a tile inside one long row).
+constexpr int64_t kRelayRowCost = 4;
+
+// Start of part b of `parts` of the sorted positions when the parts share the
+// cost of positions plus kRelayRowCost per row: the tile holding the start of
+// the last row r with rowptr_s[r] + kRelayRowCost r <= b / parts of the total
+// (rows [0, n], rowptr_s[n] = nnz). Non-decreasing in b; part 0 starts at 0,
+// part `parts` at nnz. Called by one whole wave.
+__device__ inline int64_t relay_cost_bound(const int32_t* rowptr_s, int32_t n, int64_t nnz,
+                                           int64_t b, int64_t parts, int lane) {
+  if (b <= 0) return 0;
+  if (b >= parts) return nnz;
+  const int64_t target = (nnz + kRelayRowCost * n) * b / parts;
+  int32_t a = 0, c = n;  // invariant: cost(a) <= target, answer in [a, c]
+  while (c > a) {
+    const int64_t span = (int64_t)c - a;
+    const int32_t probe = a + (int32_t)((span * (lane + 1) + 63) / 64);  // in (a, c]
+    const bool le = (int64_t)rowptr_s[probe] + kRelayRowCost * probe <= target;
+    const int k = __popcll(__ballot(le));  // the costs ascend: a prefix of the probes
+    const int32_t na = k > 0 ? __shfl(probe, k - 1, 64) : a;
+    const int32_t nc = k < 64 ? __shfl(probe, k, 64) - 1 : c;
+    a = na;
+    c = nc;
+  }
+  const int64_t pos = (int64_t)rowptr_s[a] / kRelayTile * kRelayTile;
+  return pos < nnz ? pos : nnz;
+}
+
+// The multi-pass sort's relayout: workgroup b fills part b of the sorted
+// positions, the parts sharing the copy's cost (whole tiles but the last).
 __global__ __launch_bounds__(kThreads) void k_relayout(
     int32_t n, int64_t nnz, int32_t n_cols, const int32_t* __restrict__ rowptr,
     const int32_t* __restrict__ colidx, const float* __restrict__ vals,
     const int32_t* __restrict__ perm, const int32_t* __restrict__ rowptr_s,
     int32_t* __restrict__ colidx_s, float* __restrict__ vals_s, uint32_t* err) {
   __shared__ int32_t lds[kRelaySpanLds];
+  __shared__ int64_t s_bound[2];
   if (block_failed(err)) return;
-  int64_t p0, p1;
-  relay_share(0, (nnz + kRelayTile - 1) / kRelayTile, blockIdx.x, gridDim.x, nnz, &p0, &p1);
-  relay_span(p0, p1, n, n_cols, rowptr, colidx, vals, perm, rowptr_s, colidx_s, vals_s, err, lds);
+  const int w = threadIdx.x >> 6;
+  if (w < 2) {
+    const int64_t v =
+        relay_cost_bound(rowptr_s, n, nnz, (int64_t)blockIdx.x + w, gridDim.x, threadIdx.x & 63);
+    if ((threadIdx.x & 63) == 0) s_bound[w] = v;
+  }
+  __syncthreads();
+  relay_span(s_bound[0], s_bound[1], n, n_cols, rowptr, colidx, vals, perm, rowptr_s, colidx_s,
+             vals_s, err, lds);
 }
 
 // --- partition ---------------------------------------------------------------
